@@ -1,0 +1,107 @@
+"""Per-token loop version of the reuse-aware forward, for tiny inputs (test infrastructure only).
+
+It follows the same definition as the vectorised oracle (Section 3 of the
+paper: decision by the threshold gate on the cosine similarity cue, token
+filtration, recompute of C, reconstruction from the reference for R) but
+walks frames, layers, tokens, heads and keys one at a time with scalar
+softmax arithmetic.  It shares no helper with the vectorised oracle.
+"""
+import math
+
+import numpy as np
+
+
+def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
+    p, D, H, L, Dm = cfg["patch"], cfg["width"], cfg["heads"], cfg["depth"], cfg["mlp"]
+    S = cfg["image_size"]
+    gs = S // p
+    N = gs * gs + 1
+    dh = D // H
+    flat = np.asarray(blob, dtype=np.float64).ravel()
+    cur = [0]
+
+    def nxt(*shape):
+        n = int(np.prod(shape))
+        a = flat[cur[0]:cur[0] + n].reshape(shape)
+        cur[0] += n
+        return a
+
+    Wpe, bpe, cls, pos = nxt(D, 3 * p * p), nxt(D), nxt(D), nxt(N, D)
+    layers = []
+    for _ in range(L):
+        layers.append([nxt(D), nxt(D), nxt(3 * D, D), nxt(3 * D), nxt(D, D), nxt(D),
+                       nxt(D), nxt(D), nxt(Dm, D), nxt(Dm), nxt(D, Dm), nxt(D)])
+    lnfg, lnfb = nxt(D), nxt(D)
+
+    def norm(v, gamma, beta):
+        mean = sum(v) / len(v)
+        var = sum((t - mean) ** 2 for t in v) / len(v)
+        inv = 1.0 / math.sqrt(var + 1e-5)
+        return np.array([(v[j] - mean) * inv * gamma[j] + beta[j] for j in range(len(v))])
+
+    def cosine(a, b):
+        if all(a[j] == b[j] for j in range(len(a))):
+            return 1.0
+        ab = sum(a[j] * b[j] for j in range(len(a)))
+        aa = math.sqrt(sum(t * t for t in a))
+        bb = math.sqrt(sum(t * t for t in b))
+        return min(1.0, max(-1.0, ab / max(aa * bb, 1e-8)))
+
+    F = len(frames)
+    fr64 = np.asarray(frames, dtype=np.float64)
+    X = np.zeros((F, N, D))
+    for f in range(F):
+        X[f, 0] = cls + pos[0]
+        for r in range(gs):
+            for c in range(gs):
+                vec = fr64[f, :, r * p:(r + 1) * p, c * p:(c + 1) * p].reshape(-1)
+                X[f, 1 + r * gs + c] = Wpe @ vec + bpe + pos[1 + r * gs + c]
+
+    M = np.zeros((F, L, N), dtype=np.uint8)
+    for l in range(L):
+        g1, b1, Wqkv, bqkv, Wo, bo, g2, b2, W1, bb1, W2, bb2 = layers[l]
+        Y = np.zeros_like(X)
+        KEY = np.zeros((F, N, D))
+        VAL = np.zeros((F, N, D))
+        for f in range(F):                      # frames in order: the reference comes first
+            ref = (f // group_size) * group_size
+            reuse = [False] * N
+            if f != ref:
+                for i in range(1, N):
+                    if masks is not None:
+                        reuse[i] = bool(masks[f][l][i])
+                    elif tau == -math.inf:
+                        reuse[i] = False
+                    elif tau == math.inf:
+                        reuse[i] = True
+                    else:
+                        reuse[i] = cosine(X[f, i], X[ref, i]) >= tau
+            Q = {}
+            for i in range(N):
+                if reuse[i]:
+                    KEY[f, i] = KEY[ref, i]
+                    VAL[f, i] = VAL[ref, i]
+                    M[f, l, i] = 1
+                else:
+                    t = Wqkv @ norm(X[f, i], g1, b1) + bqkv
+                    Q[i], KEY[f, i], VAL[f, i] = t[:D], t[D:2 * D], t[2 * D:]
+            for i in range(N):
+                if reuse[i]:
+                    Y[f, i] = Y[ref, i]
+                    continue
+                o = np.zeros(D)
+                for h in range(H):
+                    lo, hi = h * dh, (h + 1) * dh
+                    sc = [float(Q[i][lo:hi] @ KEY[f, j, lo:hi]) / math.sqrt(dh) for j in range(N)]
+                    mx = max(sc)
+                    ex = [math.exp(s - mx) for s in sc]
+                    tot = sum(ex)
+                    for j in range(N):
+                        o[lo:hi] += (ex[j] / tot) * VAL[f, j, lo:hi]
+                z = X[f, i] + Wo @ o + bo
+                u = W1 @ norm(z, g2, b2) + bb1
+                u = np.array([0.5 * t * (1.0 + math.erf(t / math.sqrt(2.0))) for t in u])
+                Y[f, i] = z + W2 @ u + bb2
+        X = Y
+    emb = np.stack([norm(X[f, 0], lnfg, lnfb) for f in range(F)])
+    return {"emb": emb, "masks": M, "tokens": X}

@@ -1,0 +1,222 @@
+"""Vectorised CPU oracle of the reuse-aware ViT encoder forward (test infrastructure only).
+
+What it computes, following the paper's model description (Section 3):
+
+* ViT backbone (Section 2.3, Figure "ViT model architecture"): frames are cut
+  into p x p patches, each patch is embedded linearly, a class token is added
+  (placed at index 0 here) and a learned position table is added; then L
+  pre-norm encoder layers (LayerNorm -> multi-head self-attention ->
+  residual, LayerNorm -> 2-layer GELU MLP -> residual); the embedding is the
+  final LayerNorm of the class token.
+* Reference structure: frames are split into groups of G consecutive frames;
+  the group's first frame is the reference and is computed in full at every
+  layer (the periodic full recompute of Section 6.3, and the I-frame role of
+  Section 3.1 in a star topology: every other frame of the group references
+  frame 0).
+* Decision (Section 3.3, similarity cue s_i of Eq. 1 with a single reference
+  and the hard gate M_i = [d_i > 0] of the hard-gating equation): the learned
+  MLP is replaced by the threshold d_i = cos(x_f[i], x_ref[i]) - tau with a
+  ">=" tie rule, evaluated on the layer input (the residual stream before
+  LayerNorm).  The class token is never reused.
+* Token filtration (Section 3.3): recompute set C = {i : M_i = 0}, reuse set
+  R = {i : M_i = 1}.
+* Recompute on C: the whole encoder layer (QKV projection, attention,
+  output projection, MLP) runs only on the rows of C.  The attention of a
+  recomputed query sees all N keys/values of its frame: its own fresh K/V for
+  tokens in C and the reference frame's K/V for tokens in R.
+* Token reconstruction (Section 3.3): rows of C take the recomputed output,
+  rows of R copy the reference frame's layer output.  (No restoration MLP:
+  the learned restoration layer needs trained weights.)
+
+Modes: gate mode (``tau``) and mask-injection mode (``masks`` given; class
+token and reference-frame entries are forced to 0).  ``tau = -inf`` turns
+reuse off (dense), ``tau = +inf`` reuses every non-class token of every
+non-reference frame; finite tau applies the literal rule.
+
+Cosine: a.b / max(|a| |b|, 1e-8), clamped to [-1, 1], and exactly 1 when the
+two rows are elementwise equal.  Arithmetic is float64 unless ``dtype`` says
+otherwise.
+"""
+import numpy as np
+from scipy.special import erf
+
+LN_EPS = 1e-5
+COS_EPS = 1e-8
+
+
+def unpack_blob(blob, cfg, dtype=np.float64):
+    """Split the flat weight blob into named tensors (layout documented with the C ABI)."""
+    D, p, L, Dm = cfg["width"], cfg["patch"], cfg["depth"], cfg["mlp"]
+    N = (cfg["image_size"] // p) ** 2 + 1
+    blob = np.asarray(blob)
+    off = 0
+
+    def take(*shape):
+        nonlocal off
+        n = int(np.prod(shape))
+        if off + n > blob.size:
+            raise ValueError("weight blob too short")
+        a = blob[off:off + n].astype(dtype).reshape(shape)
+        off += n
+        return a
+
+    W = {"W_pe": take(D, 3, p, p), "b_pe": take(D), "cls": take(D), "pos": take(N, D),
+         "layers": []}
+    for _ in range(L):
+        lay = {}
+        lay["ln1_g"], lay["ln1_b"] = take(D), take(D)
+        lay["W_qkv"], lay["b_qkv"] = take(3 * D, D), take(3 * D)
+        lay["W_o"], lay["b_o"] = take(D, D), take(D)
+        lay["ln2_g"], lay["ln2_b"] = take(D), take(D)
+        lay["W_1"], lay["b_1"] = take(Dm, D), take(Dm)
+        lay["W_2"], lay["b_2"] = take(D, Dm), take(D)
+        W["layers"].append(lay)
+    W["lnf_g"], W["lnf_b"] = take(D), take(D)
+    if off != blob.size:
+        raise ValueError(f"weight blob has {blob.size} floats, layout needs {off}")
+    return W
+
+
+def layer_norm(x, g, b):
+    mu = x.mean(axis=-1, keepdims=True)
+    var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)   # biased variance
+    return (x - mu) / np.sqrt(var + LN_EPS) * g + b
+
+
+def gelu(x):
+    return 0.5 * x * (1.0 + erf(x / np.sqrt(2.0)))
+
+
+def embed(frames, W, cfg):
+    """Patch embedding + class token + position table -> x^0 [F, N, D]."""
+    F = frames.shape[0]
+    p = cfg["patch"]
+    g = cfg["image_size"] // p
+    D = cfg["width"]
+    fr = np.asarray(frames, dtype=W["W_pe"].dtype)
+    # patch k = (row r, col c) row-major; patch vector ordered (channel, ky, kx)
+    patches = fr.reshape(F, 3, g, p, g, p).transpose(0, 2, 4, 1, 3, 5).reshape(F, g * g, 3 * p * p)
+    tok = patches @ W["W_pe"].reshape(D, 3 * p * p).T + W["b_pe"]
+    x = np.empty((F, g * g + 1, D), dtype=tok.dtype)
+    x[:, 0] = W["cls"] + W["pos"][0]
+    x[:, 1:] = tok + W["pos"][1:]
+    return x
+
+
+def cosine_rows(a, b):
+    """Row-wise cosine similarity with the conventions stated in the module docstring."""
+    dot = np.einsum("nd,nd->n", a, b)
+    na = np.sqrt(np.einsum("nd,nd->n", a, a))
+    nb = np.sqrt(np.einsum("nd,nd->n", b, b))
+    c = np.clip(dot / np.maximum(na * nb, COS_EPS), -1.0, 1.0)
+    same = np.all(a == b, axis=1)
+    c[same] = 1.0
+    return c
+
+
+def gate_decision(cos, tau):
+    """Hard gate with d_i = cos_i - tau: 1 = reuse, 0 = recompute (class token excluded by caller)."""
+    if np.isnan(tau):
+        raise ValueError("tau must not be NaN")
+    if tau == -np.inf:
+        return np.zeros(cos.shape, dtype=bool)
+    if tau == np.inf:
+        return np.ones(cos.shape, dtype=bool)
+    return cos >= tau
+
+
+def attention(q, k, v, heads):
+    """Multi-head softmax attention: q [n, D] against all keys k, v [N, D]."""
+    n, D = q.shape
+    dh = D // heads
+    out = np.empty_like(q)
+    for h in range(heads):
+        s = slice(h * dh, (h + 1) * dh)
+        logits = (q[:, s] @ k[:, s].T) / np.sqrt(dh)
+        logits -= logits.max(axis=1, keepdims=True)
+        pr = np.exp(logits)
+        pr /= pr.sum(axis=1, keepdims=True)
+        out[:, s] = pr @ v[:, s]
+    return out
+
+
+def qkv_rows(x_rows, P):
+    D = x_rows.shape[1]
+    t = layer_norm(x_rows, P["ln1_g"], P["ln1_b"]) @ P["W_qkv"].T + P["b_qkv"]
+    return t[:, :D], t[:, D:2 * D], t[:, 2 * D:]
+
+
+def finish_rows(x_rows, o_rows, P):
+    """Output projection + residual, then the MLP sub-layer + residual."""
+    z = x_rows + o_rows @ P["W_o"].T + P["b_o"]
+    h = gelu(layer_norm(z, P["ln2_g"], P["ln2_b"]) @ P["W_1"].T + P["b_1"])
+    return z + h @ P["W_2"].T + P["b_2"]
+
+
+def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64,
+           return_layers=False):
+    """Reuse-aware encoder forward over ``frames`` [F, 3, S, S].
+
+    Returns a dict with
+      emb    [F, D]      final LayerNorm of each frame's class token
+      masks  [F, L, N]   uint8, 1 = token reused at that layer
+      cos    [F, L, N]   cosine to the reference token (NaN where not evaluated)
+      tokens [F, N, D]   output of the last layer
+      layers (optional)  list of the L+1 token buffers x^0..x^L
+    """
+    if (tau is None) == (masks is None):
+        raise ValueError("give exactly one of tau (gate mode) and masks (injection mode)")
+    W = unpack_blob(blob, cfg, dtype)
+    F = frames.shape[0]
+    L, H = cfg["depth"], cfg["heads"]
+    G = int(group_size)
+    if F < 1 or G < 1:
+        raise ValueError("need at least one frame and a group size >= 1")
+    x = embed(frames, W, cfg)
+    N = x.shape[1]
+    out_m = np.zeros((F, L, N), dtype=np.uint8)
+    out_c = np.full((F, L, N), np.nan)
+    hist = [x.copy()] if return_layers else None
+
+    for l in range(L):
+        P = W["layers"][l]
+        y = np.empty_like(x)
+        for r in range(0, F, G):
+            # reference frame: full layer on every token
+            q_r, k_r, v_r = qkv_rows(x[r], P)
+            y[r] = finish_rows(x[r], attention(q_r, k_r, v_r, H), P)
+            for f in range(r + 1, min(r + G, F)):
+                c = cosine_rows(x[f, 1:], x[r, 1:])
+                out_c[f, l, 1:] = c
+                if masks is not None:
+                    reuse = np.asarray(masks[f, l, 1:]) != 0
+                else:
+                    reuse = gate_decision(c, tau)
+                m = np.concatenate([[False], reuse])          # class token never reused
+                out_m[f, l] = m
+                C = np.flatnonzero(~m)                        # recompute tokens
+                q_c, k_c, v_c = qkv_rows(x[f, C], P)
+                k_t, v_t = k_r.copy(), v_r.copy()             # keys/values: reference ...
+                k_t[C], v_t[C] = k_c, v_c                     # ... overwritten by fresh rows
+                y_c = finish_rows(x[f, C], attention(q_c, k_t, v_t, H), P)
+                y[f] = y[r]                                   # reused rows: reference output
+                y[f, C] = y_c                                 # recomputed rows
+        x = y
+        if return_layers:
+            hist.append(x.copy())
+
+    emb = layer_norm(x[:, 0], W["lnf_g"], W["lnf_b"])
+    res = {"emb": emb, "masks": out_m, "cos": out_c, "tokens": x}
+    if return_layers:
+        res["layers"] = hist
+    return res
+
+
+def reuse_rate(masks, group_size):
+    """Mean of the reuse map over non-reference frames, all N tokens and all L layers
+    (the reuse-rate definition of the reuse-loss equation, Section 4)."""
+    F = masks.shape[0]
+    nonref = [f for f in range(F) if f % group_size != 0]
+    if not nonref:
+        return 0.0
+    return float(np.asarray(masks)[nonref].astype(np.float64).mean())

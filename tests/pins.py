@@ -1,0 +1,285 @@
+"""Checks that pin the CPU oracle to things other than itself.
+
+Each ``pin_*`` takes an oracle-like namespace (``encode``, ``cosine_rows``,
+``gate_decision``, ``reuse_rate``) and raises AssertionError on failure.  The
+oracle's own tests run them on ``oracle.reusevit``; the mutation test runs
+them on copies of that module with a planted mistake and requires that at
+least one pin fails for each mistake.
+
+What pins what:
+  library      dense forward == torch conv2d + TransformerEncoderLayer(norm_first) + layer_norm
+  dense_vit    reuse off == the separately written dense ViT
+  bruteforce   == the per-token loop implementation, gate and injection modes
+  copy         tau=+inf: every non-reference frame is a bitwise copy of its reference
+  ref_dense    reference frames equal the dense ViT for any tau; their mask rows are 0
+  monotone     gate mode: a reused token stays reused in later layers
+  static       identical frames are fully reused at layer 0 and copy the reference
+  g1           group size 1 is the dense ViT
+  groups       permuting whole groups permutes outputs; group-aligned splits change nothing
+  inject_one   one injected reused token: its row copies the reference output and the other
+               queries attend to the reference's K/V there (torch MHA with separate key input)
+  extremes     tau=2 == reuse off, tau=-2 == tau=+inf
+  star         every frame of a group references the group's first frame
+  cosine       closed-form cosines; equal rows give exactly 1; tie cos == tau reuses
+  partial      a short last group still has its first frame as reference
+  rate         reuse-rate denominator: non-reference frames x N tokens x L layers
+"""
+import numpy as np
+
+import synth
+from synth.configs import ModelConfig
+
+from oracle.bruteforce import encode_bruteforce
+from oracle.dense_vit import dense_vit
+
+from . import torch_ref
+
+M_A = ModelConfig(32, 16, 2, 8, 2, 16, "f32")       # N=5, D=8, L=2
+M_B = ModelConfig(48, 16, 2, 16, 2, 32, "f32")      # N=10, D=16, L=2
+M_1 = ModelConfig(48, 16, 1, 16, 2, 32, "f32")      # one layer
+
+
+def weights(m, seed=7, perturb=True):
+    w = synth.make_weights(m, seed, perturb_ln=perturb, std=0.3)
+    return w, synth.pack_weights(w, m)
+
+
+def mixed_frames(m, F, G, seed=11):
+    """Groups whose non-reference frames copy the reference patch-wise, with a random half of
+    the patches perturbed by noise of mixed strength (so cosines spread over [-1, 1])."""
+    rng = np.random.default_rng(seed)
+    S, p = m.image_size, m.patch
+    g = S // p
+    fr = np.empty((F, 3, S, S), np.float32)
+    for f in range(F):
+        if f % G == 0:
+            fr[f] = rng.standard_normal((3, S, S))
+            base = fr[f].copy()
+            continue
+        fr[f] = base
+        for r in range(g):
+            for c in range(g):
+                if rng.random() < 0.5:
+                    amp = rng.choice([0.05, 0.3, 1.0, 3.0])
+                    fr[f, :, r * p:(r + 1) * p, c * p:(c + 1) * p] += \
+                        amp * rng.standard_normal((3, p, p))
+    return fr
+
+
+def _close(a, b, tol, what):
+    a, b = np.asarray(a), np.asarray(b)
+    assert a.shape == b.shape, f"{what}: shape {a.shape} vs {b.shape}"
+    err = np.max(np.abs(a - b)) if a.size else 0.0
+    assert err <= tol, f"{what}: max abs diff {err:.3e} > {tol:.1e}"
+
+
+def assert_copy(r, f, ref):
+    """Frame f copies frame ref: reused rows bitwise; the class token, recomputed from an equal
+    input against equal keys/values, to rounding (BLAS may order a 1-row product differently
+    from a full-frame one)."""
+    assert np.array_equal(r["tokens"][f, 1:], r["tokens"][ref, 1:]), f"frame {f} rows not a copy"
+    _close(r["tokens"][f, 0], r["tokens"][ref, 0], 1e-12, f"frame {f} class token")
+    _close(r["emb"][f], r["emb"][ref], 1e-12, f"frame {f} embedding")
+
+
+def pin_library(ora):
+    for m in (M_A, M_B):
+        w, blob = weights(m)
+        fr = mixed_frames(m, 4, 4)
+        e_t, x_t = torch_ref.vit(fr, w, m)
+        r = ora.encode(fr, blob, m.as_dict(), 4, tau=-np.inf)
+        _close(r["tokens"], x_t, 1e-10, "tokens vs torch")
+        _close(r["emb"], e_t, 1e-10, "embeddings vs torch")
+
+
+def pin_dense_vit(ora):
+    m = M_B
+    w, blob = weights(m, 3)
+    fr = mixed_frames(m, 6, 3)
+    e, x = dense_vit(fr, blob, m.as_dict(), return_tokens=True)
+    r = ora.encode(fr, blob, m.as_dict(), 3, tau=-np.inf)
+    _close(r["emb"], e, 1e-11, "emb vs dense_vit")
+    _close(r["tokens"], x, 1e-11, "tokens vs dense_vit")
+    assert not r["masks"].any()
+
+
+def pin_bruteforce(ora):
+    for m, G in ((M_A, 4), (M_B, 3)):
+        w, blob = weights(m, 5)
+        fr = mixed_frames(m, 7, G, seed=5)
+        cfg = m.as_dict()
+        for tau in (-np.inf, 0.3, 0.8, 0.97, np.inf):
+            r = ora.encode(fr, blob, cfg, G, tau=tau)
+            b = encode_bruteforce(fr, blob, cfg, G, tau=tau)
+            assert np.array_equal(r["masks"], b["masks"]), f"masks differ at tau={tau}"
+            _close(r["tokens"], b["tokens"], 1e-12, f"tokens tau={tau}")
+            _close(r["emb"], b["emb"], 1e-12, f"emb tau={tau}")
+        rng = np.random.default_rng(9)
+        mk = (rng.random((7, m.depth, m.n_tokens)) < 0.5).astype(np.uint8)
+        r = ora.encode(fr, blob, cfg, G, masks=mk)
+        b = encode_bruteforce(fr, blob, cfg, G, masks=mk)
+        assert np.array_equal(r["masks"], b["masks"]), "effective injected masks differ"
+        _close(r["tokens"], b["tokens"], 1e-12, "tokens (injected)")
+
+
+def pin_copy(ora):
+    m = M_B
+    _, blob = weights(m, 8)
+    G = 4
+    fr = mixed_frames(m, 8, G, seed=8)
+    r = ora.encode(fr, blob, m.as_dict(), G, tau=np.inf)
+    for f in range(8):
+        ref = (f // G) * G
+        assert_copy(r, f, ref)
+        if f != ref:
+            assert r["masks"][f, :, 1:].all() and not r["masks"][f, :, 0].any()
+
+
+def pin_ref_dense(ora):
+    m = M_B
+    _, blob = weights(m, 12)
+    G = 3
+    fr = mixed_frames(m, 7, G, seed=12)
+    e = dense_vit(fr, blob, m.as_dict())
+    for tau in (0.2, 0.9, np.inf):
+        r = ora.encode(fr, blob, m.as_dict(), G, tau=tau)
+        for f in range(0, 7, G):
+            _close(r["emb"][f], e[f], 1e-11, f"reference frame {f}")
+            assert not r["masks"][f].any()
+        assert not r["masks"][:, :, 0].any(), "class token must never be reused"
+
+
+def pin_monotone(ora):
+    m = M_B
+    _, blob = weights(m, 13)
+    fr = mixed_frames(m, 8, 4, seed=13)
+    seen_reuse = False
+    for tau in (0.3, 0.7, 0.95, 0.999, 1.0):
+        mk = ora.encode(fr, blob, m.as_dict(), 4, tau=tau)["masks"]
+        assert np.all(mk[:, 1:] >= mk[:, :-1]), f"reuse not monotone over layers at tau={tau}"
+        seen_reuse |= bool(mk.any())
+    assert seen_reuse
+
+
+def pin_static(ora):
+    m = M_B
+    _, blob = weights(m, 14)
+    one = mixed_frames(m, 1, 1, seed=14)
+    fr = np.repeat(one, 4, axis=0)
+    for tau in (-0.5, 0.5, 0.99, 1.0):
+        r = ora.encode(fr, blob, m.as_dict(), 4, tau=tau)
+        assert r["masks"][1:, :, 1:].all(), f"static video not fully reused at tau={tau}"
+        for f in range(1, 4):
+            assert_copy(r, f, 0)
+    r = ora.encode(fr, blob, m.as_dict(), 4, tau=1.0 + 1e-9)
+    assert not r["masks"].any(), "tau above 1 must reuse nothing"
+
+
+def pin_g1(ora):
+    m = M_B
+    _, blob = weights(m, 15)
+    fr = mixed_frames(m, 5, 2, seed=15)
+    e = dense_vit(fr, blob, m.as_dict())
+    r = ora.encode(fr, blob, m.as_dict(), 1, tau=-1.0)
+    _close(r["emb"], e, 1e-11, "G=1")
+    assert not r["masks"].any()
+
+
+def pin_groups(ora):
+    m = M_B
+    _, blob = weights(m, 16)
+    G = 3
+    fr = mixed_frames(m, 9, G, seed=16)
+    cfg = m.as_dict()
+    a = ora.encode(fr, blob, cfg, G, tau=0.8)
+    perm = [2, 0, 1]
+    fr_p = np.concatenate([fr[g * G:(g + 1) * G] for g in perm])
+    b = ora.encode(fr_p, blob, cfg, G, tau=0.8)
+    for k, g in enumerate(perm):
+        assert np.array_equal(b["emb"][k * G:(k + 1) * G], a["emb"][g * G:(g + 1) * G])
+        assert np.array_equal(b["masks"][k * G:(k + 1) * G], a["masks"][g * G:(g + 1) * G])
+    c1 = ora.encode(fr[:6], blob, cfg, G, tau=0.8)
+    c2 = ora.encode(fr[6:], blob, cfg, G, tau=0.8)
+    assert np.array_equal(np.concatenate([c1["emb"], c2["emb"]]), a["emb"])
+
+
+def pin_inject_one(ora):
+    m = M_1
+    w, blob = weights(m, 17)
+    fr = mixed_frames(m, 2, 2, seed=17)
+    j = 4
+    mk = np.zeros((2, 1, m.n_tokens), np.uint8)
+    mk[1, 0, j] = 1
+    r = ora.encode(fr, blob, m.as_dict(), 2, masks=mk, return_layers=True)
+    x0 = torch_ref.embed(fr, w, m).numpy()
+    _close(r["layers"][0], x0, 1e-12, "layer input vs conv2d embedding")
+    ref_out = torch_ref.layer_with_substituted_kv(x0[0], x0[0], j, w, 0, m)
+    f_out = torch_ref.layer_with_substituted_kv(x0[1], x0[0], j, w, 0, m)
+    y = r["layers"][1]
+    _close(y[0], ref_out, 1e-11, "reference frame layer output")
+    assert np.array_equal(y[1, j], y[0, j]), "reused row must copy the reference output"
+    rows = [i for i in range(m.n_tokens) if i != j]
+    _close(y[1, rows], f_out[rows], 1e-11, "other queries with the reference's K/V at j")
+
+
+def pin_extremes(ora):
+    m = M_B
+    _, blob = weights(m, 18)
+    fr = mixed_frames(m, 8, 4, seed=18)
+    cfg = m.as_dict()
+    lo, hi = ora.encode(fr, blob, cfg, 4, tau=-np.inf), ora.encode(fr, blob, cfg, 4, tau=2.0)
+    assert np.array_equal(lo["tokens"], hi["tokens"]) and not hi["masks"].any()
+    a, b = ora.encode(fr, blob, cfg, 4, tau=np.inf), ora.encode(fr, blob, cfg, 4, tau=-2.0)
+    assert np.array_equal(a["tokens"], b["tokens"])
+    assert np.array_equal(a["masks"], b["masks"])
+
+
+def pin_star(ora):
+    m = M_B
+    _, blob = weights(m, 19)
+    fr = mixed_frames(m, 4, 4, seed=19)
+    fr[2] = fr[0]                 # frame 2 repeats the group's first frame exactly
+    r = ora.encode(fr, blob, m.as_dict(), 4, tau=0.9999)
+    assert r["masks"][2, :, 1:].all(), "frame equal to the reference must be fully reused"
+    assert_copy(r, 2, 0)
+    assert not r["masks"][1, 0, 1:].all(), "frame 1 differs from the reference"
+
+
+def pin_cosine(ora):
+    th = np.linspace(0.0, np.pi, 7)
+    a = np.stack([np.ones_like(th), np.zeros_like(th), np.zeros_like(th)], 1) * 2.5
+    b = np.stack([np.cos(th), np.sin(th), np.zeros_like(th)], 1) * 0.7
+    c = ora.cosine_rows(a, b)
+    assert np.allclose(c, np.cos(th), atol=1e-15, rtol=0), f"cosine {c} vs {np.cos(th)}"
+    assert ora.cosine_rows(a, -a)[0] == -1.0
+    v = np.random.default_rng(1).standard_normal((5, 9))
+    assert np.all(ora.cosine_rows(v, v) == 1.0), "equal rows must give exactly 1"
+    z = np.zeros((1, 4))
+    assert ora.cosine_rows(z, z)[0] == 1.0
+    assert ora.cosine_rows(z, np.ones((1, 4)))[0] == 0.0
+    cs = np.array([0.5, 0.94999, 0.95, 0.96])
+    assert list(ora.gate_decision(cs, 0.95)) == [False, False, True, True], "tie must reuse"
+
+
+def pin_partial(ora):
+    m = M_B
+    _, blob = weights(m, 20)
+    fr = mixed_frames(m, 6, 4, seed=20)
+    e = dense_vit(fr, blob, m.as_dict())
+    r = ora.encode(fr, blob, m.as_dict(), 4, tau=np.inf)
+    _close(r["emb"][4], e[4], 1e-11, "first frame of the short last group")
+    assert_copy(r, 5, 4)
+
+
+def pin_rate(ora):
+    mk = np.zeros((6, 2, 5), np.uint8)
+    mk[1, 0, 1:3] = 1       # 2 reused
+    mk[5, 1, :] = 1         # 5 reused (a reference frame's entries would not count)
+    mk[4, 1, :] = 1         # frame 4 is a reference at G=4: not counted
+    # non-reference frames at G=4: 1, 2, 3, 5 -> denominator 4 * 2 * 5 = 40
+    assert abs(ora.reuse_rate(mk, 4) - 7 / 40) < 1e-15
+
+
+ALL_PINS = [pin_library, pin_dense_vit, pin_bruteforce, pin_copy, pin_ref_dense, pin_monotone,
+            pin_static, pin_g1, pin_groups, pin_inject_one, pin_extremes, pin_star, pin_cosine,
+            pin_partial, pin_rate]
