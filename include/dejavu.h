@@ -1,0 +1,183 @@
+/*
+ * dejavu.h -- C ABI of the reuse-aware ViT encoder for AMD Instinct MI355X (gfx950).
+ *
+ * The library computes the ViT embedding of every frame of a video batch while
+ * reusing per-token work across frames, following "DejaVu: Efficient
+ * Video-Language Query Engine with Learning-based Inter-Frame Computation
+ * Reuse" (PVLDB 18(10), 2025):
+ *
+ *   - ViT backbone: patch embedding, class token, learned position table, L
+ *     pre-norm encoder layers, final LayerNorm of the class token
+ *     (Section 2.3, ViT architecture figure).
+ *   - Frames are cut into groups of G consecutive frames; the first frame of
+ *     a group is the reference and is computed in full at every layer (the
+ *     periodic full recompute of Section 6.3; a star form of the reference
+ *     structure of Section 3.1).
+ *   - Per layer and token, a reuse decision (Section 3.3, similarity cue of
+ *     Eq. 1 with one reference and the hard gate M_i = [d_i > 0]) with the
+ *     learned decision MLP replaced by a threshold: token i of a
+ *     non-reference frame is reused when cos(x_f[i], x_ref[i]) >= tau, on the
+ *     layer input x (residual stream).  The class token is never reused.
+ *   - Token filtration (Section 3.3): recompute tokens are stream-compacted
+ *     across all frames of the batch into dense rows (sparse computation
+ *     compaction, Section 5.3) and run the whole encoder layer (QKV
+ *     projection, attention over all N keys/values of the frame -- fresh rows
+ *     for recomputed tokens, the reference's rows for reused ones --, output
+ *     projection, MLP) on those rows only.
+ *   - Token reconstruction (Section 3.3): reused tokens take the reference's
+ *     layer output.  Layers run over the whole batch one at a time
+ *     (layer-wise scheduling, Section 5.1); the reference's per-layer state
+ *     lives in the batch buffers for one layer step only (cached memory
+ *     compaction, Section 5.2).
+ *
+ * Cosine convention: a.b / max(|a||b|, 1e-8) in fp32, clamped to [-1, 1],
+ * and exactly 1 when the two rows are elementwise equal.
+ *
+ * Conventions for every entry point:
+ *   - Return value: DV_OK (0) or a negative DV_E* code; dv_last_error() gives
+ *     a message for the calling thread.
+ *   - Arguments are validated on the host before any work is enqueued; on a
+ *     validation error nothing is launched and no device memory is touched.
+ *   - "device" pointers are HIP device allocations on the current device;
+ *     "host" pointers are ordinary host memory.  The caller owns every buffer
+ *     it passes; outputs must not alias inputs.
+ *   - All layouts are dense, row-major, little-endian.
+ *   - A handle is not re-entrant: use one handle per concurrently used stream.
+ */
+#ifndef DEJAVU_H
+#define DEJAVU_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define DV_OK 0
+#define DV_EINVAL (-1)        /* bad argument: null pointer, size < 1, NaN tau, size mismatch */
+#define DV_ENOMEM (-2)        /* a device or host allocation failed */
+#define DV_EHIP (-3)          /* a HIP runtime call failed (message names it) */
+#define DV_EUNSUPPORTED (-4)  /* configuration outside what the kernels support */
+
+/* arithmetic type of the GEMM and attention operands (the residual stream,
+ * LayerNorm statistics, softmax and the reuse gate are always fp32) */
+#define DV_F32 0
+#define DV_BF16 1
+
+typedef struct dv_config {
+    int image_size;        /* S: frames are 3 x S x S */
+    int patch;             /* p: S % p == 0; P = (S/p)^2 patches, N = P + 1 tokens */
+    int depth;             /* L encoder layers */
+    int width;             /* D */
+    int heads;             /* H: D % H == 0, head dim D/H a multiple of 16 and <= 128 */
+    int mlp;               /* Dm: MLP hidden width */
+    int dtype;             /* DV_F32 or DV_BF16 */
+    int max_batch_frames;  /* frames per internal batch (rounded down to whole groups per call) */
+    unsigned flags;        /* reserved, must be 0 */
+} dv_config;
+
+typedef struct dv_handle dv_handle;
+
+/* Number of floats the weight blob of `cfg` must hold (0 if cfg is NULL or invalid).
+ * Blob layout (fp32, tensors back to back):
+ *   W_pe [D,3,p,p], b_pe [D], cls [D], pos [N,D]
+ *   per layer: ln1_g [D], ln1_b [D], W_qkv [3D,D], b_qkv [3D], W_o [D,D], b_o [D],
+ *              ln2_g [D], ln2_b [D], W_1 [Dm,D], b_1 [Dm], W_2 [D,Dm], b_2 [D]
+ *   lnf_g [D], lnf_b [D]
+ * Linear layers map x -> x W^T + b.  W_qkv rows: Q, then K, then V; heads are
+ * contiguous slices of D/H rows within each.  LayerNorm eps is 1e-5. */
+size_t dv_weights_floats(const dv_config* cfg);
+
+/* Create a handle: validates cfg, copies the weight blob (`weights`, host,
+ * `weights_bytes` bytes, the caller may free it on return) to the device,
+ * rounds the matrices to bf16 (nearest, ties to even) when dtype is
+ * DV_BF16, and allocates the workspace for max_batch_frames frames.
+ * Synchronous.  Errors: DV_EINVAL (null pointer, wrong blob size, sizes < 1),
+ * DV_EUNSUPPORTED (S % p, D % H, head dim, flags), DV_ENOMEM, DV_EHIP.
+ * On error *out is set to NULL. */
+int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, dv_handle** out);
+
+/* Release a handle and its device memory (synchronises the device first).
+ * A NULL handle is accepted. */
+int dv_destroy(dv_handle* h);
+
+/* Message of the last error raised on the calling thread ("" if none). */
+const char* dv_last_error(void);
+
+/* Bytes of device workspace the handle holds (weights excluded). */
+int dv_workspace_bytes(const dv_handle* h, size_t* bytes);
+
+/* Gate mode.  frames: device fp32 [n_frames, 3, S, S], already normalised.
+ * out_embeddings: device fp32 [n_frames, D] (final LayerNorm of the class token).
+ * out_masks: device u8 [n_frames, depth, N] (1 = reused) or NULL.
+ * Frame f's reference is frame G*floor(f/G) (frame indices within this call;
+ * a short last group still uses its first frame).  Work is split into
+ * internal batches of whole groups, so the result does not depend on
+ * max_batch_frames.  tau = -INFINITY turns reuse off (the same kernels run
+ * densely, masks all 0); tau = +INFINITY reuses every non-class token of
+ * every non-reference frame; a finite tau applies the rule above
+ * (tau > 1 reuses nothing, tau <= -1 everything).  NaN tau -> DV_EINVAL.
+ * Enqueued on `stream`, asynchronous, no host synchronisation.
+ * Errors: DV_EINVAL (null handle/frames/embeddings, n_frames < 1,
+ * group_size < 1 or > max_batch_frames, NaN tau), DV_EHIP. */
+int dv_encode(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
+              float* out_embeddings, uint8_t* out_masks, hipStream_t stream);
+
+/* Mask-injection mode: the reuse map comes from `masks`, device u8
+ * [n_frames, depth, N] (nonzero = reuse), instead of the gate.  Entries of
+ * class tokens and of reference frames are forced to 0; out_masks (optional)
+ * receives the effective map.  Masks need not be monotone over layers: a
+ * token reused at layer l holds the reference's row at layer l+1.
+ * Other arguments and errors as dv_encode (masks NULL -> DV_EINVAL). */
+int dv_encode_masked(dv_handle* h, const float* frames, int n_frames, int group_size,
+                     const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,
+                     hipStream_t stream);
+
+/* Either mode (masks != NULL selects injection and ignores tau), plus the
+ * last layer's full token buffer: out_tokens device fp32 [n_frames, N, D]
+ * (NULL allowed).  Used to check whole outputs, not only embeddings. */
+int dv_encode_tokens(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
+                     const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,
+                     float* out_tokens, hipStream_t stream);
+
+/* Stream compaction of a reuse map on its own (token filtration, Section 3.3;
+ * stream compaction across the frames of a batch, Section 5.3).
+ * masks: device u8 [n_frames, n_tokens], 1 = reused; entries of reference
+ * frames (f % group_size == 0) must be 0 (the caller's contract; reference
+ * rows are counted as recomputed whatever they hold).
+ * Outputs (device, int32): idx [n_frames*n_tokens] -- the recomputed tokens
+ * f*n_tokens+i in frame-major order in idx[0..count); pos
+ * [n_frames*n_tokens] -- packed slot of each token, for a reused token the
+ * slot of the same token of its reference frame; qoff [n_frames+1] -- first
+ * packed slot of each frame, qoff[n_frames] = count; count [1].
+ * Errors: DV_EINVAL (null pointer, sizes < 1, n_frames*n_tokens > 2^30), DV_EHIP. */
+int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size, int32_t* idx,
+               int32_t* pos, int32_t* qoff, int32_t* count, hipStream_t stream);
+
+/* Stage timing with HIP events recorded on the encode stream around every
+ * launch of a stage (0 = off).  While on, every dv_encode* call records; read
+ * the totals after synchronising the stream.  dv_profile resets the totals. */
+#define DV_STAGE_PATCH 0
+#define DV_STAGE_GATE 1
+#define DV_STAGE_COMPACT 2
+#define DV_STAGE_LN1 3
+#define DV_STAGE_QKV 4
+#define DV_STAGE_ATTN 5
+#define DV_STAGE_OPROJ 6
+#define DV_STAGE_LN2 7
+#define DV_STAGE_FC1 8
+#define DV_STAGE_FC2 9
+#define DV_STAGE_MERGE 10
+#define DV_STAGE_FINAL 11
+#define DV_NUM_STAGES 12
+int dv_profile(dv_handle* h, int enable);
+/* total_ms: summed event time of the stage's launches; launches: how many. */
+int dv_profile_read(dv_handle* h, int stage, double* total_ms, long long* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DEJAVU_H */

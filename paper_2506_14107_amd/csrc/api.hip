@@ -1,0 +1,661 @@
+// C ABI and host orchestrator of the reuse-aware ViT encoder.
+//
+// Per internal batch of whole groups (layer-wise scheduling: one layer over every frame of
+// the batch before the next), the launch sequence is
+//   im2col -> patch GEMM (+bias +pos) ; class-token rows
+//   for each layer:
+//     gate (cosine to the reference, or injected map) + per-frame counts
+//     compaction (idx / pos / qoff / M, all on the device)
+//     LN1 of the gathered recompute rows -> QKV GEMM -> attention over fresh + reference K/V
+//     -> out-proj GEMM (+bias, +gathered residual) -> LN2 -> FC1 GEMM (+bias, GELU)
+//     -> FC2 GEMM (+bias, +residual) written straight back into the token rows
+//     [injection mode: copy the reference's new row into every reused row]
+//   final LayerNorm of the class tokens.
+// Nothing is read back to the host inside an encode call.
+//
+// Gate mode needs no merge pass: once a token is reused its row would be a copy of the
+// reference's, whose cosine is exactly 1, so it stays reused in every later layer; the gate
+// answers such tokens from the previous layer's map and nobody reads their rows again.  Only
+// when the caller asks for the full token buffer are those rows filled in at the end.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/dejavu.h"
+#include "dv_internal.h"
+
+using namespace dv;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                          \
+    do {                                                                                       \
+        hipError_t e_ = (expr);                                                                \
+        if (e_ != hipSuccess)                                                                  \
+            return fail(e_ == hipErrorOutOfMemory ? DV_ENOMEM : DV_EHIP, "%s: %s (%s:%d)", #expr, \
+                        hipGetErrorString(e_), __FILE__, __LINE__);                            \
+    } while (0)
+
+constexpr int ROW_PAD = 256;  // GEMM operand rows are padded to a multiple of the tallest tile
+
+size_t round_up(size_t v, size_t m) { return (v + m - 1) / m * m; }
+
+struct LayerW {
+    const float *ln1_g, *ln1_b, *b_qkv, *b_o, *ln2_g, *ln2_b, *b_1, *b_2;
+    const void *W_qkv, *W_o, *W_1, *W_2;
+};
+
+struct Dims {
+    int S, p, L, D, H, Dm, N, P, Kp, B;
+    bool bf16;
+};
+
+// validates a configuration; fills dims
+int check_config(const dv_config* c, Dims* d) {
+    if (!c) return fail(DV_EINVAL, "config is NULL");
+    if (c->image_size < 1 || c->patch < 1 || c->depth < 1 || c->width < 1 || c->heads < 1 ||
+        c->mlp < 1 || c->max_batch_frames < 1)
+        return fail(DV_EINVAL, "config sizes must be >= 1");
+    if (c->dtype != DV_F32 && c->dtype != DV_BF16) return fail(DV_EINVAL, "unknown dtype %d", c->dtype);
+    if (c->flags != 0) return fail(DV_EUNSUPPORTED, "flags must be 0");
+    if (c->image_size % c->patch) return fail(DV_EUNSUPPORTED, "image_size %% patch != 0");
+    if (c->width % c->heads) return fail(DV_EUNSUPPORTED, "width %% heads != 0");
+    const int dh = c->width / c->heads;
+    if (dh % 16 || dh > 128) return fail(DV_EUNSUPPORTED, "head dim %d must be a multiple of 16, <= 128", dh);
+    const bool bf = c->dtype == DV_BF16;
+    const int tile = bf ? 128 : 64;
+    if (c->width % tile || c->mlp % tile)
+        return fail(DV_EUNSUPPORTED, "width and mlp must be multiples of %d for this dtype", tile);
+    if (c->width > 2048) return fail(DV_EUNSUPPORTED, "width above 2048");
+    d->S = c->image_size;
+    d->p = c->patch;
+    d->L = c->depth;
+    d->D = c->width;
+    d->H = c->heads;
+    d->Dm = c->mlp;
+    const int g = c->image_size / c->patch;
+    d->P = g * g;
+    d->N = d->P + 1;
+    d->Kp = (int)round_up((size_t)3 * c->patch * c->patch, 64);
+    d->B = c->max_batch_frames;
+    d->bf16 = bf;
+    if (attention_lds_bytes(bf, d->N, dh) > 160 * 1024)
+        return fail(DV_EUNSUPPORTED, "attention tile for N=%d, head dim %d exceeds LDS", d->N, dh);
+    const size_t T = (size_t)d->B * d->N;
+    const size_t widest = (size_t)std::max(std::max(3 * d->D, d->Dm), d->Kp);
+    if (round_up(T, ROW_PAD) * widest >= (1ull << 31) || T >= (1ull << 30))
+        return fail(DV_EUNSUPPORTED, "max_batch_frames * tokens too large for 32-bit row indices");
+    return DV_OK;
+}
+
+size_t blob_floats(const Dims& d) {
+    const size_t D = d.D, Dm = d.Dm, N = d.N, p = d.p;
+    size_t per_layer = 2 * D + 3 * D * D + 3 * D + D * D + D + 2 * D + Dm * D + Dm + D * Dm + D;
+    return D * 3 * p * p + D + D + N * D + (size_t)d.L * per_layer + 2 * D;
+}
+
+struct Stage {
+    double ms = 0;
+    long long launches = 0;
+};
+
+}  // namespace
+
+struct dv_handle {
+    Dims d;
+    int device = 0;
+    void* wmem = nullptr;   // weights
+    void* ws = nullptr;     // workspace
+    size_t ws_bytes = 0;
+    // weights
+    const void* W_pe;
+    const float *b_pe, *cls, *pos, *lnf_g, *lnf_b;
+    std::vector<LayerW> layers;
+    // workspace views
+    float* x;         // [T, D] fp32 token rows
+    void* A;          // [Tp, max(D, Kp)] elem: LN output / patch rows
+    void* qkv;        // [Tp, 3D] elem
+    void* O;          // [Tp, D] elem: attention output
+    float* Z;         // [Tp, D] fp32: after attention residual
+    void* Hb;         // [Tp, Dm] elem: MLP hidden
+    uint8_t* mask[2]; // [T] per-layer maps (ping-pong)
+    int *idx, *pos_, *qoff, *cnt, *M;
+    int *idx_id, *pos_id, *qoff_id;  // identity lists (reuse off)
+    int id_frames = -1;              // frames the identity lists were built for
+    // profiling
+    bool prof = false;
+    Stage stages[DV_NUM_STAGES];
+    struct Pending {
+        int stage;
+        hipEvent_t a, b;
+    };
+    std::vector<Pending> pending;
+    std::vector<hipEvent_t> pool;
+};
+
+namespace {
+
+// ---- stage timing -----------------------------------------------------------------------------
+struct Scope {
+    dv_handle* h;
+    int stage;
+    hipStream_t s;
+    hipEvent_t b = nullptr;
+    Scope(dv_handle* h_, int st, hipStream_t s_) : h(h_), stage(st), s(s_) {
+        if (!h->prof) return;
+        hipEvent_t a = take(), bb = take();
+        if (!a || !bb) return;
+        (void)hipEventRecord(a, s);
+        b = bb;
+        h->pending.push_back({stage, a, bb});
+    }
+    ~Scope() {
+        if (b) (void)hipEventRecord(b, s);
+    }
+    hipEvent_t take() {
+        if (!h->pool.empty()) {
+            hipEvent_t e = h->pool.back();
+            h->pool.pop_back();
+            return e;
+        }
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
+    }
+};
+
+int collect(dv_handle* h) {
+    for (auto& p : h->pending) {
+        HIP_TRY(hipEventSynchronize(p.b));
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, p.a, p.b));
+        h->stages[p.stage].ms += ms;
+        h->stages[p.stage].launches += 1;
+        h->pool.push_back(p.a);
+        h->pool.push_back(p.b);
+    }
+    h->pending.clear();
+    return DV_OK;
+}
+
+// ---- one batch of whole groups --------------------------------------------------------------
+int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float tau,
+              const uint8_t* inj, float* emb, uint8_t* om, float* tokens, hipStream_t s) {
+    const Dims& d = h->d;
+    const bool bf = d.bf16;
+    const int N = d.N, D = d.D, L = d.L;
+    const int T = F * N;
+    const bool dense = mode == GATE_NONE;
+
+    // identity row lists for the dense pass (built once per batch size)
+    if (dense && h->id_frames != F) {
+        launch_compact(nullptr, nullptr, F, N, 1, h->idx_id, h->pos_id, h->qoff_id, s);
+        h->id_frames = F;
+    }
+
+    {   // patch embedding + class-token rows
+        Scope sc(h, DV_STAGE_PATCH, s);
+        launch_im2col(bf, frames, F, d.S, d.p, d.Kp, h->A, s);
+        launch_cls_init(h->x, h->cls, h->pos, F, N, D, s);
+        GemmArgs g{};
+        g.A = h->A;
+        g.W = h->W_pe;
+        g.bias = h->b_pe;
+        g.K = d.Kp;
+        g.Nout = D;
+        g.Mdev = nullptr;
+        g.Mconst = F * d.P;
+        g.Mmax = F * d.P;
+        g.out = h->x;
+        g.pos = h->pos;
+        g.P = d.P;
+        g.N = N;
+        launch_gemm(Epi::Patch, bf, g, s);
+    }
+
+    const int* idx = dense ? h->idx_id : h->idx;
+    const int* pos = dense ? h->pos_id : h->pos_;
+    const int* qoff = dense ? h->qoff_id : h->qoff;
+    const int* Mdev = dense ? nullptr : h->M;
+
+    for (int l = 0; l < L; ++l) {
+        const LayerW& w = h->layers[l];
+        uint8_t* cur = h->mask[l & 1];
+        uint8_t* prev = l > 0 ? h->mask[(l - 1) & 1] : nullptr;
+        if (dense) {
+            if (om) launch_zero_mask_layer(om, F, L, N, l, s);
+        } else {
+            {
+                Scope sc(h, DV_STAGE_GATE, s);
+                GateArgs ga{};
+                ga.x = h->x;
+                ga.F = F;
+                ga.N = N;
+                ga.D = D;
+                ga.G = G;
+                ga.L = L;
+                ga.layer = l;
+                ga.mode = mode;
+                ga.tau = tau;
+                ga.prev = (mode == GATE_COS) ? prev : nullptr;
+                ga.inj = inj;
+                ga.cur = cur;
+                ga.out_masks = om;
+                ga.cnt = h->cnt;
+                launch_gate(ga, s);
+            }
+            {
+                Scope sc(h, DV_STAGE_COMPACT, s);
+                launch_scan(h->cnt, F, h->qoff, h->M, s);
+                launch_compact(cur, h->qoff, F, N, G, h->idx, h->pos_, nullptr, s);
+            }
+        }
+        {
+            Scope sc(h, DV_STAGE_LN1, s);
+            launch_ln_rows(bf, h->x, idx, Mdev, T, D, w.ln1_g, w.ln1_b, h->A, s);
+        }
+        GemmArgs g{};
+        g.Mdev = Mdev;
+        g.Mconst = T;
+        g.Mmax = T;
+        g.idx = idx;
+        {
+            Scope sc(h, DV_STAGE_QKV, s);
+            g.A = h->A;
+            g.W = w.W_qkv;
+            g.bias = w.b_qkv;
+            g.K = D;
+            g.Nout = 3 * D;
+            g.out = h->qkv;
+            launch_gemm(Epi::Qkv, bf, g, s);
+        }
+        {
+            Scope sc(h, DV_STAGE_ATTN, s);
+            AttnArgs at{};
+            at.qkv = h->qkv;
+            at.pos = pos;
+            at.qoff = qoff;
+            at.out = h->O;
+            at.F = F;
+            at.N = N;
+            at.D = D;
+            at.H = d.H;
+            launch_attention(bf, at, s);
+        }
+        {
+            Scope sc(h, DV_STAGE_OPROJ, s);
+            g.A = h->O;
+            g.W = w.W_o;
+            g.bias = w.b_o;
+            g.K = D;
+            g.Nout = D;
+            g.out = h->Z;
+            g.resid = h->x;
+            launch_gemm(Epi::OProj, bf, g, s);
+        }
+        {
+            Scope sc(h, DV_STAGE_LN2, s);
+            launch_ln_rows(bf, h->Z, nullptr, Mdev, T, D, w.ln2_g, w.ln2_b, h->A, s);
+        }
+        {
+            Scope sc(h, DV_STAGE_FC1, s);
+            g.A = h->A;
+            g.W = w.W_1;
+            g.bias = w.b_1;
+            g.K = D;
+            g.Nout = d.Dm;
+            g.out = h->Hb;
+            g.resid = nullptr;
+            launch_gemm(Epi::Fc1, bf, g, s);
+        }
+        {
+            Scope sc(h, DV_STAGE_FC2, s);
+            g.A = h->Hb;
+            g.W = w.W_2;
+            g.bias = w.b_2;
+            g.K = d.Dm;
+            g.Nout = D;
+            g.out = h->x;
+            g.resid = h->Z;
+            launch_gemm(Epi::Fc2, bf, g, s);
+        }
+        if (mode == GATE_INJECT || mode == GATE_ALL || (mode == GATE_COS && tokens && l == L - 1)) {
+            // reused rows take the reference's new row (gate mode: only to hand out tokens)
+            Scope sc(h, DV_STAGE_MERGE, s);
+            launch_merge(h->x, cur, F, N, D, G, s);
+        }
+    }
+    {
+        Scope sc(h, DV_STAGE_FINAL, s);
+        launch_final_ln(h->x, F, N, D, h->lnf_g, h->lnf_b, emb, s);
+    }
+    if (tokens)
+        HIP_TRY(hipMemcpyAsync(tokens, h->x, (size_t)T * D * sizeof(float), hipMemcpyDeviceToDevice, s));
+    return DV_OK;
+}
+
+int encode_impl(dv_handle* h, const float* frames, int n, int G, float tau, const uint8_t* masks,
+                float* emb, uint8_t* om, float* tokens, hipStream_t s) {
+    if (!h) return fail(DV_EINVAL, "handle is NULL");
+    if (!frames || !emb) return fail(DV_EINVAL, "frames and out_embeddings must not be NULL");
+    if (n < 1) return fail(DV_EINVAL, "n_frames must be >= 1 (got %d)", n);
+    if (G < 1) return fail(DV_EINVAL, "group_size must be >= 1 (got %d)", G);
+    if (G > h->d.B) return fail(DV_EINVAL, "group_size %d exceeds max_batch_frames %d", G, h->d.B);
+    int mode;
+    if (masks) {
+        mode = GATE_INJECT;
+    } else {
+        if (std::isnan(tau)) return fail(DV_EINVAL, "tau is NaN");
+        mode = (tau == -INFINITY) ? GATE_NONE : (tau == INFINITY) ? GATE_ALL : GATE_COS;
+    }
+    const Dims& d = h->d;
+    const int per = (d.B / G) * G;
+    const size_t img = (size_t)3 * d.S * d.S;
+    HIP_TRY(hipSetDevice(h->device));
+    for (int f0 = 0; f0 < n; f0 += per) {
+        const int F = std::min(per, n - f0);
+        const size_t ml = (size_t)d.L * d.N;
+        int rc = run_batch(h, frames + (size_t)f0 * img, F, G, mode, tau,
+                           masks ? masks + (size_t)f0 * ml : nullptr, emb + (size_t)f0 * d.D,
+                           om ? om + (size_t)f0 * ml : nullptr,
+                           tokens ? tokens + (size_t)f0 * d.N * d.D : nullptr, s);
+        if (rc) return rc;
+    }
+    HIP_TRY(hipGetLastError());
+    return DV_OK;
+}
+
+template <class T>
+T* carve(char*& p, size_t count) {
+    T* r = (T*)p;
+    p += round_up(count * sizeof(T), 256);
+    return r;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t dv_weights_floats(const dv_config* cfg) {
+    Dims d;
+    std::string keep = g_err;
+    if (check_config(cfg, &d) != DV_OK) {
+        g_err = keep;
+        return 0;
+    }
+    return blob_floats(d);
+}
+
+const char* dv_last_error(void) { return g_err.c_str(); }
+
+int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, dv_handle** out) {
+    if (!out) return fail(DV_EINVAL, "out is NULL");
+    *out = nullptr;
+    Dims d;
+    int rc = check_config(cfg, &d);
+    if (rc) return rc;
+    if (!weights) return fail(DV_EINVAL, "weights is NULL");
+    const size_t nf = blob_floats(d);
+    if (weights_bytes != nf * sizeof(float))
+        return fail(DV_EINVAL, "weight blob has %zu bytes, configuration needs %zu", weights_bytes,
+                    nf * sizeof(float));
+    const bool bf = d.bf16;
+    const size_t el = bf ? 2 : 4;
+    const size_t D = d.D, Dm = d.Dm, N = d.N, L = d.L;
+
+    // --- weights: matrices in elem (bf16 rounded or fp32), vectors in fp32 -------------------
+    std::vector<char> host;
+    struct Off { size_t o; };
+    size_t wbytes = 0;
+    auto reserve = [&](size_t bytes) {
+        size_t o = wbytes;
+        wbytes += round_up(bytes, 256);
+        return o;
+    };
+    const size_t o_pe = reserve(D * d.Kp * el), o_bpe = reserve(D * 4), o_cls = reserve(D * 4),
+                 o_pos = reserve(N * D * 4);
+    struct LO { size_t ln1_g, ln1_b, W_qkv, b_qkv, W_o, b_o, ln2_g, ln2_b, W_1, b_1, W_2, b_2; };
+    std::vector<LO> lo(L);
+    for (size_t l = 0; l < L; ++l) {
+        lo[l].ln1_g = reserve(D * 4);
+        lo[l].ln1_b = reserve(D * 4);
+        lo[l].W_qkv = reserve(3 * D * D * el);
+        lo[l].b_qkv = reserve(3 * D * 4);
+        lo[l].W_o = reserve(D * D * el);
+        lo[l].b_o = reserve(D * 4);
+        lo[l].ln2_g = reserve(D * 4);
+        lo[l].ln2_b = reserve(D * 4);
+        lo[l].W_1 = reserve(Dm * D * el);
+        lo[l].b_1 = reserve(Dm * 4);
+        lo[l].W_2 = reserve(D * Dm * el);
+        lo[l].b_2 = reserve(D * 4);
+    }
+    const size_t o_lnf_g = reserve(D * 4), o_lnf_b = reserve(D * 4);
+    try {
+        host.assign(wbytes, 0);
+    } catch (const std::bad_alloc&) {
+        return fail(DV_ENOMEM, "host staging buffer of %zu bytes", wbytes);
+    }
+    const float* src = weights;
+    auto put_vec = [&](size_t off, size_t count) {
+        memcpy(host.data() + off, src, count * 4);
+        src += count;
+    };
+    auto put_mat = [&](size_t off, size_t rows, size_t cols, size_t ld) {
+        for (size_t r = 0; r < rows; ++r)
+            for (size_t c = 0; c < cols; ++c) {
+                const float v = src[r * cols + c];
+                if (bf) ((uint16_t*)(host.data() + off))[r * ld + c] = f32_to_bf16(v);
+                else ((float*)(host.data() + off))[r * ld + c] = v;
+            }
+        src += rows * cols;
+    };
+    put_mat(o_pe, D, 3 * (size_t)d.p * d.p, d.Kp);  // [D, 3p^2] padded to Kp with zeros
+    put_vec(o_bpe, D);
+    put_vec(o_cls, D);
+    put_vec(o_pos, N * D);
+    for (size_t l = 0; l < L; ++l) {
+        put_vec(lo[l].ln1_g, D);
+        put_vec(lo[l].ln1_b, D);
+        put_mat(lo[l].W_qkv, 3 * D, D, D);
+        put_vec(lo[l].b_qkv, 3 * D);
+        put_mat(lo[l].W_o, D, D, D);
+        put_vec(lo[l].b_o, D);
+        put_vec(lo[l].ln2_g, D);
+        put_vec(lo[l].ln2_b, D);
+        put_mat(lo[l].W_1, Dm, D, D);
+        put_vec(lo[l].b_1, Dm);
+        put_mat(lo[l].W_2, D, Dm, Dm);
+        put_vec(lo[l].b_2, D);
+    }
+    put_vec(o_lnf_g, D);
+    put_vec(o_lnf_b, D);
+
+    dv_handle* h = new (std::nothrow) dv_handle();
+    if (!h) return fail(DV_ENOMEM, "handle");
+    h->d = d;
+    auto cleanup = [&](int code) {
+        if (h->wmem) (void)hipFree(h->wmem);
+        if (h->ws) (void)hipFree(h->ws);
+        delete h;
+        return code;
+    };
+    if (hipGetDevice(&h->device) != hipSuccess) return cleanup(fail(DV_EHIP, "hipGetDevice failed"));
+    {
+        hipError_t e = hipMalloc(&h->wmem, wbytes);
+        if (e != hipSuccess) {
+            h->wmem = nullptr;
+            return cleanup(fail(e == hipErrorOutOfMemory ? DV_ENOMEM : DV_EHIP, "weights: %s",
+                                hipGetErrorString(e)));
+        }
+        e = hipMemcpy(h->wmem, host.data(), wbytes, hipMemcpyHostToDevice);
+        if (e != hipSuccess) return cleanup(fail(DV_EHIP, "weight upload: %s", hipGetErrorString(e)));
+    }
+    char* wb = (char*)h->wmem;
+    h->W_pe = wb + o_pe;
+    h->b_pe = (const float*)(wb + o_bpe);
+    h->cls = (const float*)(wb + o_cls);
+    h->pos = (const float*)(wb + o_pos);
+    h->lnf_g = (const float*)(wb + o_lnf_g);
+    h->lnf_b = (const float*)(wb + o_lnf_b);
+    h->layers.resize(L);
+    for (size_t l = 0; l < L; ++l) {
+        LayerW& w = h->layers[l];
+        w.ln1_g = (const float*)(wb + lo[l].ln1_g);
+        w.ln1_b = (const float*)(wb + lo[l].ln1_b);
+        w.W_qkv = wb + lo[l].W_qkv;
+        w.b_qkv = (const float*)(wb + lo[l].b_qkv);
+        w.W_o = wb + lo[l].W_o;
+        w.b_o = (const float*)(wb + lo[l].b_o);
+        w.ln2_g = (const float*)(wb + lo[l].ln2_g);
+        w.ln2_b = (const float*)(wb + lo[l].ln2_b);
+        w.W_1 = wb + lo[l].W_1;
+        w.b_1 = (const float*)(wb + lo[l].b_1);
+        w.W_2 = wb + lo[l].W_2;
+        w.b_2 = (const float*)(wb + lo[l].b_2);
+    }
+
+    // --- workspace ----------------------------------------------------------------------------
+    const size_t T = (size_t)d.B * N, Tp = round_up(T, ROW_PAD);
+    const size_t Awide = std::max((size_t)D, (size_t)d.Kp);
+    size_t need = 0;
+    auto sz = [&](size_t bytes) { need += round_up(bytes, 256); };
+    sz(T * D * 4);        // x
+    sz(Tp * Awide * el);  // A
+    sz(Tp * 3 * D * el);  // qkv
+    sz(Tp * D * el);      // O
+    sz(Tp * D * 4);       // Z
+    sz(Tp * Dm * el);     // H
+    sz(T);
+    sz(T);                // masks
+    for (int i = 0; i < 2; ++i) {
+        sz(T * 4);
+        sz(T * 4);
+        sz((d.B + 1) * 4);
+    }
+    sz(d.B * 4);
+    sz(4 * 4);
+    {
+        hipError_t e = hipMalloc(&h->ws, need);
+        if (e != hipSuccess) {
+            h->ws = nullptr;
+            return cleanup(fail(e == hipErrorOutOfMemory ? DV_ENOMEM : DV_EHIP,
+                                "workspace of %zu bytes: %s", need, hipGetErrorString(e)));
+        }
+        // defined contents in the row padding that GEMM tiles read past M
+        e = hipMemset(h->ws, 0, need);
+        if (e != hipSuccess) return cleanup(fail(DV_EHIP, "workspace clear: %s", hipGetErrorString(e)));
+    }
+    h->ws_bytes = need;
+    char* p = (char*)h->ws;
+    h->x = carve<float>(p, T * D);
+    h->A = carve<char>(p, Tp * Awide * el);
+    h->qkv = carve<char>(p, Tp * 3 * D * el);
+    h->O = carve<char>(p, Tp * D * el);
+    h->Z = carve<float>(p, Tp * D);
+    h->Hb = carve<char>(p, Tp * Dm * el);
+    h->mask[0] = carve<uint8_t>(p, T);
+    h->mask[1] = carve<uint8_t>(p, T);
+    h->idx = carve<int>(p, T);
+    h->pos_ = carve<int>(p, T);
+    h->qoff = carve<int>(p, d.B + 1);
+    h->idx_id = carve<int>(p, T);
+    h->pos_id = carve<int>(p, T);
+    h->qoff_id = carve<int>(p, d.B + 1);
+    h->cnt = carve<int>(p, d.B);
+    h->M = carve<int>(p, 4);
+    *out = h;
+    return DV_OK;
+}
+
+int dv_destroy(dv_handle* h) {
+    if (!h) return DV_OK;
+    (void)hipSetDevice(h->device);
+    (void)hipDeviceSynchronize();
+    for (auto& pe : h->pending) {
+        (void)hipEventDestroy(pe.a);
+        (void)hipEventDestroy(pe.b);
+    }
+    for (auto e : h->pool) (void)hipEventDestroy(e);
+    if (h->wmem) (void)hipFree(h->wmem);
+    if (h->ws) (void)hipFree(h->ws);
+    delete h;
+    return DV_OK;
+}
+
+int dv_workspace_bytes(const dv_handle* h, size_t* bytes) {
+    if (!h || !bytes) return fail(DV_EINVAL, "NULL argument");
+    *bytes = h->ws_bytes;
+    return DV_OK;
+}
+
+int dv_encode(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
+              float* out_embeddings, uint8_t* out_masks, hipStream_t stream) {
+    return encode_impl(h, frames, n_frames, group_size, tau, nullptr, out_embeddings, out_masks,
+                       nullptr, stream);
+}
+
+int dv_encode_masked(dv_handle* h, const float* frames, int n_frames, int group_size,
+                     const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,
+                     hipStream_t stream) {
+    if (!masks) return fail(DV_EINVAL, "masks is NULL");
+    return encode_impl(h, frames, n_frames, group_size, 0.f, masks, out_embeddings, out_masks,
+                       nullptr, stream);
+}
+
+int dv_encode_tokens(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
+                     const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,
+                     float* out_tokens, hipStream_t stream) {
+    return encode_impl(h, frames, n_frames, group_size, tau, masks, out_embeddings, out_masks,
+                       out_tokens, stream);
+}
+
+int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size, int32_t* idx,
+               int32_t* pos, int32_t* qoff, int32_t* count, hipStream_t stream) {
+    if (!masks || !idx || !pos || !qoff || !count) return fail(DV_EINVAL, "NULL argument");
+    if (n_frames < 1 || n_tokens < 1 || group_size < 1) return fail(DV_EINVAL, "sizes must be >= 1");
+    if ((long long)n_frames * n_tokens > (1ll << 30)) return fail(DV_EINVAL, "too many tokens");
+    // per-frame counts land in qoff[0..n) and are turned into the prefix in place by one block
+    launch_count(masks, n_frames, n_tokens, group_size, qoff, stream);
+    launch_scan(qoff, n_frames, qoff, count, stream);
+    launch_compact(masks, qoff, n_frames, n_tokens, group_size, idx, pos, nullptr, stream);
+    HIP_TRY(hipGetLastError());
+    return DV_OK;
+}
+
+int dv_profile(dv_handle* h, int enable) {
+    if (!h) return fail(DV_EINVAL, "handle is NULL");
+    int rc = collect(h);
+    if (rc) return rc;
+    for (auto& st : h->stages) st = Stage();
+    h->prof = enable != 0;
+    return DV_OK;
+}
+
+int dv_profile_read(dv_handle* h, int stage, double* total_ms, long long* launches) {
+    if (!h || !total_ms || !launches) return fail(DV_EINVAL, "NULL argument");
+    if (stage < 0 || stage >= DV_NUM_STAGES) return fail(DV_EINVAL, "stage %d out of range", stage);
+    int rc = collect(h);
+    if (rc) return rc;
+    *total_ms = h->stages[stage].ms;
+    *launches = h->stages[stage].launches;
+    return DV_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,96 @@
+// Internal interface between the orchestrator (api.hip) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dv {
+
+// ---- bf16 storage helpers (raw 16-bit patterns) ---------------------------------------------
+__host__ __device__ inline uint16_t f32_to_bf16(float f) {
+    uint32_t u = __builtin_bit_cast(uint32_t, f);
+    u += 0x7FFFu + ((u >> 16) & 1u);  // round to nearest, ties to even (finite inputs)
+    return (uint16_t)(u >> 16);
+}
+__host__ __device__ inline float bf16_to_f32(uint16_t h) {
+    return __builtin_bit_cast(float, (uint32_t)h << 16);
+}
+
+// ---- GEMM ------------------------------------------------------------------------------------
+// C[M, Nout] = A[M, K] * W[Nout, K]^T with a fused epilogue.  M is read on the device.
+enum class Epi : int {
+    Patch = 0,  // x[(r/P)*N + 1 + r%P, c] = acc + bias[c] + pos[(1 + r%P), c]        (fp32 out)
+    Qkv = 1,    // qkv[r, c] = acc + bias[c]                                           (elem out)
+    OProj = 2,  // z[r, c] = acc + bias[c] + x[idx[r], c]                              (fp32 out)
+    Fc1 = 3,    // h[r, c] = gelu(acc + bias[c])                                       (elem out)
+    Fc2 = 4,    // x[idx[r], c] = acc + bias[c] + z[r, c]                              (fp32 out)
+};
+
+struct GemmArgs {
+    const void* A;       // [rows, K] row-major; rows padded to the tile height
+    const void* W;       // [Nout, K] row-major
+    const float* bias;   // [Nout]
+    int K, Nout;
+    const int* Mdev;     // device row count (nullptr: use Mconst)
+    int Mconst;
+    int Mmax;            // upper bound on M (grid sizing)
+    void* out;
+    const float* resid;  // OProj: x rows; Fc2: z rows
+    const int* idx;      // packed row -> token row
+    const float* pos;    // Patch: position table [N, D]
+    int P, N;            // Patch: patches and tokens per frame
+};
+
+void launch_gemm(Epi e, bool bf16, const GemmArgs& a, hipStream_t s);
+
+// ---- attention -------------------------------------------------------------------------------
+struct AttnArgs {
+    const void* qkv;   // packed rows [M, 3D] (Q | K | V), elem
+    const int* pos;    // [F*N] packed row of each token's K/V (reused -> reference's row)
+    const int* qoff;   // [F+1] packed query rows of frame f: qoff[f] .. qoff[f+1]
+    void* out;         // [M, D] elem
+    int F, N, D, H;
+};
+void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
+size_t attention_lds_bytes(bool bf16, int N, int dh);
+
+// ---- row kernels -----------------------------------------------------------------------------
+void launch_im2col(bool bf16, const float* frames, int F, int S, int p, int Kp, void* A,
+                   hipStream_t s);
+void launch_cls_init(float* x, const float* cls, const float* pos, int F, int N, int D,
+                     hipStream_t s);
+
+enum GateMode : int { GATE_COS = 0, GATE_INJECT = 1, GATE_ALL = 2, GATE_NONE = 3 };
+struct GateArgs {
+    const float* x;       // [F*N, D]
+    int F, N, D, G, L, layer;
+    int mode;
+    float tau;
+    const uint8_t* prev;  // previous layer's map (gate mode, monotone shortcut) or nullptr
+    const uint8_t* inj;   // injected maps [F, L, N] (batch base) or nullptr
+    uint8_t* cur;         // [F*N] this layer's map
+    uint8_t* out_masks;   // [F, L, N] (batch base) or nullptr
+    int* cnt;             // [F] recomputed tokens per frame
+};
+void launch_gate(const GateArgs& a, hipStream_t s);
+void launch_count(const uint8_t* m, int F, int N, int G, int* cnt, hipStream_t s);
+// qoff[0..F] = exclusive prefix of cnt[0..F), *M = qoff[F]
+void launch_scan(const int* cnt, int F, int* qoff, int* M, hipStream_t s);
+// idx/pos from a per-layer map and its qoff (cur == nullptr: every token recomputed, identity
+// lists, qoff_in ignored and qoff_out written)
+void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,
+                    int* pos, int* qoff_out, hipStream_t s);
+
+// LayerNorm of rows (optionally gathered through idx) into elem rows: dst[r] = LN(src[g(r)])
+void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* Mdev, int Mmax,
+                    int D, const float* g, const float* b, void* dst, hipStream_t s);
+// x[f*N+i] = x[ref(f)*N+i] for every token with cur[f*N+i] != 0
+void launch_merge(float* x, const uint8_t* cur, int F, int N, int D, int G, hipStream_t s);
+// emb[f] = LN(x[f*N]) (class token)
+void launch_final_ln(const float* x, int F, int N, int D, const float* g, const float* b,
+                     float* emb, hipStream_t s);
+void launch_fill_u8(uint8_t* p, size_t n, uint8_t v, hipStream_t s);
+// out_masks[f, layer, :] = 0 for all f (dense mode)
+void launch_zero_mask_layer(uint8_t* out_masks, int F, int L, int N, int layer, hipStream_t s);
+
+}  // namespace dv

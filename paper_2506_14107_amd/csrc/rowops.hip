@@ -1,0 +1,378 @@
+// Row-wise kernels: patch gather, class-token init, reuse gate, stream compaction,
+// LayerNorm (gathered), merge of reused rows, final LayerNorm.  All are HBM-bound;
+// one 64-lane wavefront owns one row, loads are float4 and coalesced.
+#include "dv_internal.h"
+
+namespace dv {
+
+namespace {
+
+constexpr int WAVE = 64;
+constexpr int MAX_CHUNKS = 8;  // float4 chunks per lane: D <= 2048
+
+__device__ inline float wave_sum(float v) {
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, WAVE);
+    return v;
+}
+
+// --- patch gather: A[f*P + k, e] = frame[f][c][py*p+ky][px*p+kx], e = (c, ky, kx); zero pad to Kp
+template <bool BF>
+__global__ void im2col_k(const float* __restrict__ frames, int F, int S, int p, int Kp, void* A) {
+    const int g = S / p, P = g * g, kk = 3 * p * p;
+    const size_t total = (size_t)F * P * Kp;
+    for (size_t t = blockIdx.x * (size_t)blockDim.x + threadIdx.x; t < total;
+         t += (size_t)gridDim.x * blockDim.x) {
+        const int e = (int)(t % Kp);
+        const size_t row = t / Kp;
+        const int f = (int)(row / P), k = (int)(row % P);
+        float v = 0.f;
+        if (e < kk) {
+            const int c = e / (p * p), ky = (e / p) % p, kx = e % p;
+            const int py = k / g, px = k % g;
+            v = frames[(((size_t)f * 3 + c) * S + (py * p + ky)) * S + px * p + kx];
+        }
+        if (BF) ((uint16_t*)A)[t] = f32_to_bf16(v);
+        else ((float*)A)[t] = v;
+    }
+}
+
+__global__ void cls_init_k(float* x, const float* cls, const float* pos, int F, int N, int D) {
+    const size_t total = (size_t)F * D;
+    for (size_t t = blockIdx.x * (size_t)blockDim.x + threadIdx.x; t < total;
+         t += (size_t)gridDim.x * blockDim.x) {
+        const int f = (int)(t / D), d = (int)(t % D);
+        x[(size_t)f * N * D + d] = cls[d] + pos[d];
+    }
+}
+
+// --- reuse gate: one block per frame, one wavefront per token --------------------------------
+// cnt[f] = number of recomputed tokens of frame f.
+__global__ __launch_bounds__(1024) void gate_k(GateArgs a) {
+    const int f = blockIdx.x;
+    const int N = a.N, D = a.D;
+    const int r = (f / a.G) * a.G;
+    const int lane = threadIdx.x & (WAVE - 1), wave = threadIdx.x / WAVE;
+    const int nwaves = blockDim.x / WAVE;
+    __shared__ int wcount[16];
+    uint8_t* om = a.out_masks ? a.out_masks + ((size_t)f * a.L + a.layer) * N : nullptr;
+    int active = 0;
+    for (int i = wave; i < N; i += nwaves) {
+        int reuse = 0;
+        if (f != r && i != 0) {
+            if (a.mode == GATE_INJECT) {
+                reuse = a.inj[((size_t)f * a.L + a.layer) * N + i] != 0;
+            } else if (a.mode == GATE_ALL) {
+                reuse = 1;
+            } else if (a.mode == GATE_COS) {
+                if (a.prev && a.prev[(size_t)f * N + i]) {
+                    // a reused token holds a copy of the reference's row: cosine exactly 1
+                    reuse = a.tau <= 1.0f;
+                } else {
+                    const float4* xf = (const float4*)(a.x + ((size_t)f * N + i) * D);
+                    const float4* xr = (const float4*)(a.x + ((size_t)r * N + i) * D);
+                    float dot = 0.f, na = 0.f, nb = 0.f;
+                    int eq = 1;
+                    for (int c = lane; c < D / 4; c += WAVE) {
+                        const float4 u = xf[c], v = xr[c];
+                        dot += u.x * v.x + u.y * v.y + u.z * v.z + u.w * v.w;
+                        na += u.x * u.x + u.y * u.y + u.z * u.z + u.w * u.w;
+                        nb += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+                        eq &= (u.x == v.x) & (u.y == v.y) & (u.z == v.z) & (u.w == v.w);
+                    }
+                    dot = wave_sum(dot);
+                    na = wave_sum(na);
+                    nb = wave_sum(nb);
+                    const bool same = __all(eq);
+                    float cs = dot / fmaxf(sqrtf(na) * sqrtf(nb), 1e-8f);
+                    cs = fminf(1.0f, fmaxf(-1.0f, cs));
+                    if (same) cs = 1.0f;
+                    reuse = cs >= a.tau;
+                }
+            }
+        }
+        if (lane == 0) {
+            a.cur[(size_t)f * N + i] = (uint8_t)reuse;
+            if (om) om[i] = (uint8_t)reuse;
+            active += !reuse;
+        }
+    }
+    if (lane == 0) wcount[wave] = active;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int s = 0;
+        for (int w = 0; w < nwaves; ++w) s += wcount[w];
+        a.cnt[f] = s;
+    }
+}
+
+__global__ __launch_bounds__(256) void count_k(const uint8_t* m, int F, int N, int G, int* cnt) {
+    const int f = blockIdx.x;
+    const bool ref = (f % G) == 0;
+    int c = 0;
+    for (int i = threadIdx.x; i < N; i += blockDim.x) c += ref || m[(size_t)f * N + i] == 0;
+    __shared__ int red[256];
+    red[threadIdx.x] = c;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) cnt[f] = red[0];
+}
+
+// --- exclusive prefix over frames: qoff[f] = sum_{g<f} cnt[g], qoff[F] = *M = total ---------
+// one block; qoff may equal cnt (each thread reads its entry before any write to it)
+__global__ __launch_bounds__(1024) void scan_k(const int* cnt, int F, int* qoff, int* M) {
+    __shared__ int part[1024];
+    __shared__ int carry_s;
+    const int tid = threadIdx.x;
+    if (tid == 0) carry_s = 0;
+    __syncthreads();
+    for (int base = 0; base < F; base += 1024) {
+        const int f = base + tid;
+        const int v = f < F ? cnt[f] : 0;
+        part[tid] = v;
+        __syncthreads();
+        for (int o = 1; o < 1024; o <<= 1) {  // Hillis-Steele inclusive scan
+            const int add = tid >= o ? part[tid - o] : 0;
+            __syncthreads();
+            part[tid] += add;
+            __syncthreads();
+        }
+        const int carry = carry_s;
+        if (f < F) qoff[f] = carry + part[tid] - v;
+        __syncthreads();
+        if (tid == 1023) carry_s = carry + part[1023];
+        __syncthreads();
+    }
+    if (tid == 0) {
+        qoff[F] = carry_s;
+        *M = carry_s;
+    }
+}
+
+// --- stream compaction: one block (256 threads) per frame ------------------------------------
+// Frame f's recomputed tokens go to packed slots qoff[f] .. qoff[f+1] in token order; the rank
+// inside the frame comes from a wavefront ballot + popcount and a prefix over the block's four
+// wavefronts.  A reused token points at the slot of the same token of its reference frame
+// (reference frames keep all their tokens, in order).  cur == nullptr: every token recomputed,
+// qoff ignored (identity lists).
+__global__ __launch_bounds__(256) void compact_k(const uint8_t* cur, const int* qoff_in, int F,
+                                                 int N, int G, int* idx, int* pos, int* qoff_out) {
+    const int f = blockIdx.x;
+    const int r = (f / G) * G;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __shared__ int wtot[4];
+    const int off = cur ? qoff_in[f] : f * N;
+    const int refoff = cur ? qoff_in[r] : r * N;
+    int running = 0;
+    for (int base = 0; base < N; base += 256) {
+        const int i = base + tid;
+        const bool valid = i < N;
+        const bool act = valid && (cur == nullptr || f == r || cur[(size_t)f * N + i] == 0);
+        const unsigned long long bal = __ballot(act);
+        const int lpre = __popcll(bal & ((1ull << lane) - 1ull));
+        __syncthreads();  // previous chunk's wtot reads are done
+        if (lane == 0) wtot[wave] = __popcll(bal);
+        __syncthreads();
+        int wpre = 0;
+        for (int w = 0; w < wave; ++w) wpre += wtot[w];
+        const int rank = running + wpre + lpre;
+        if (act) {
+            idx[off + rank] = f * N + i;
+            pos[(size_t)f * N + i] = off + rank;
+        } else if (valid) {
+            pos[(size_t)f * N + i] = refoff + i;
+        }
+        running += wtot[0] + wtot[1] + wtot[2] + wtot[3];
+    }
+    if (!cur && tid == 0) {
+        qoff_out[f] = off;
+        if (f == F - 1) qoff_out[F] = F * N;
+    }
+}
+
+// --- LayerNorm of (gathered) rows -> elem rows ------------------------------------------------
+template <bool BF>
+__global__ __launch_bounds__(256) void ln_rows_k(const float* __restrict__ src,
+                                                 const int* __restrict__ gather,
+                                                 const int* __restrict__ Mdev, int Mmax, int D,
+                                                 const float* __restrict__ g,
+                                                 const float* __restrict__ b, void* dst) {
+    const int M = Mdev ? *Mdev : Mmax;
+    const int lane = threadIdx.x & 63;
+    const int nchunk = D / 4;
+    const float4* g4 = (const float4*)g;
+    const float4* b4 = (const float4*)b;
+    for (int row = (blockIdx.x * blockDim.x + threadIdx.x) / 64; row < M;
+         row += gridDim.x * blockDim.x / 64) {
+        const int srow = gather ? gather[row] : row;
+        const float4* s4 = (const float4*)(src + (size_t)srow * D);
+        float4 v[MAX_CHUNKS];
+        float sum = 0.f;
+#pragma unroll
+        for (int k = 0; k < MAX_CHUNKS; ++k) {
+            const int c = lane + k * 64;
+            if (c < nchunk) {
+                v[k] = s4[c];
+                sum += (v[k].x + v[k].y) + (v[k].z + v[k].w);
+            }
+        }
+        const float mean = wave_sum(sum) / (float)D;
+        float sq = 0.f;
+#pragma unroll
+        for (int k = 0; k < MAX_CHUNKS; ++k) {
+            const int c = lane + k * 64;
+            if (c < nchunk) {
+                const float a0 = v[k].x - mean, a1 = v[k].y - mean, a2 = v[k].z - mean,
+                            a3 = v[k].w - mean;
+                sq += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+            }
+        }
+        const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + 1e-5f);
+#pragma unroll
+        for (int k = 0; k < MAX_CHUNKS; ++k) {
+            const int c = lane + k * 64;
+            if (c < nchunk) {
+                const float4 gg = g4[c], bb = b4[c];
+                float4 o;
+                o.x = (v[k].x - mean) * rstd * gg.x + bb.x;
+                o.y = (v[k].y - mean) * rstd * gg.y + bb.y;
+                o.z = (v[k].z - mean) * rstd * gg.z + bb.z;
+                o.w = (v[k].w - mean) * rstd * gg.w + bb.w;
+                if (BF) {
+                    uint2 pk;
+                    pk.x = (uint32_t)f32_to_bf16(o.x) | ((uint32_t)f32_to_bf16(o.y) << 16);
+                    pk.y = (uint32_t)f32_to_bf16(o.z) | ((uint32_t)f32_to_bf16(o.w) << 16);
+                    ((uint2*)dst)[(size_t)row * nchunk + c] = pk;
+                } else {
+                    ((float4*)dst)[(size_t)row * nchunk + c] = o;
+                }
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void merge_k(float* x, const uint8_t* cur, int F, int N, int D,
+                                               int G) {
+    const int lane = threadIdx.x & 63;
+    const int total = F * N;
+    for (int t = (blockIdx.x * blockDim.x + threadIdx.x) / 64; t < total;
+         t += gridDim.x * blockDim.x / 64) {
+        if (!cur[t]) continue;
+        const int f = t / N, i = t % N;
+        const int r = (f / G) * G;
+        if (r == f) continue;
+        const float4* s = (const float4*)(x + ((size_t)r * N + i) * D);
+        float4* d = (float4*)(x + (size_t)t * D);
+        for (int c = lane; c < D / 4; c += 64) d[c] = s[c];
+    }
+}
+
+__global__ __launch_bounds__(256) void final_ln_k(const float* x, int F, int N, int D,
+                                                  const float* g, const float* b, float* emb) {
+    const int lane = threadIdx.x & 63;
+    for (int f = (blockIdx.x * blockDim.x + threadIdx.x) / 64; f < F;
+         f += gridDim.x * blockDim.x / 64) {
+        const float* row = x + (size_t)f * N * D;
+        float s = 0.f;
+        for (int d = lane; d < D; d += 64) s += row[d];
+        const float mean = wave_sum(s) / (float)D;
+        float q = 0.f;
+        for (int d = lane; d < D; d += 64) {
+            const float a = row[d] - mean;
+            q += a * a;
+        }
+        const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + 1e-5f);
+        for (int d = lane; d < D; d += 64) emb[(size_t)f * D + d] = (row[d] - mean) * rstd * g[d] + b[d];
+    }
+}
+
+__global__ void fill_u8_k(uint8_t* p, size_t n, uint8_t v) {
+    for (size_t t = blockIdx.x * (size_t)blockDim.x + threadIdx.x; t < n;
+         t += (size_t)gridDim.x * blockDim.x)
+        p[t] = v;
+}
+
+__global__ void zero_mask_layer_k(uint8_t* om, int F, int L, int N, int layer) {
+    const size_t total = (size_t)F * N;
+    for (size_t t = blockIdx.x * (size_t)blockDim.x + threadIdx.x; t < total;
+         t += (size_t)gridDim.x * blockDim.x) {
+        const size_t f = t / N, i = t % N;
+        om[(f * L + layer) * N + i] = 0;
+    }
+}
+
+inline int grid_for(size_t work, int per_block, int cap = 8192) {
+    size_t g = (work + per_block - 1) / per_block;
+    if (g < 1) g = 1;
+    return (int)(g < (size_t)cap ? g : (size_t)cap);
+}
+
+}  // namespace
+
+void launch_im2col(bool bf16, const float* frames, int F, int S, int p, int Kp, void* A,
+                   hipStream_t s) {
+    const int P = (S / p) * (S / p);
+    const size_t total = (size_t)F * P * Kp;
+    const int grid = grid_for(total, 256, 65536);
+    if (bf16) hipLaunchKernelGGL(im2col_k<true>, dim3(grid), dim3(256), 0, s, frames, F, S, p, Kp, A);
+    else hipLaunchKernelGGL(im2col_k<false>, dim3(grid), dim3(256), 0, s, frames, F, S, p, Kp, A);
+}
+
+void launch_cls_init(float* x, const float* cls, const float* pos, int F, int N, int D,
+                     hipStream_t s) {
+    hipLaunchKernelGGL(cls_init_k, dim3(grid_for((size_t)F * D, 256)), dim3(256), 0, s, x, cls,
+                       pos, F, N, D);
+}
+
+void launch_gate(const GateArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(gate_k, dim3(a.F), dim3(1024), 0, s, a);
+}
+
+void launch_count(const uint8_t* m, int F, int N, int G, int* cnt, hipStream_t s) {
+    hipLaunchKernelGGL(count_k, dim3(F), dim3(256), 0, s, m, F, N, G, cnt);
+}
+
+void launch_scan(const int* cnt, int F, int* qoff, int* M, hipStream_t s) {
+    hipLaunchKernelGGL(scan_k, dim3(1), dim3(1024), 0, s, cnt, F, qoff, M);
+}
+
+void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,
+                    int* pos, int* qoff_out, hipStream_t s) {
+    hipLaunchKernelGGL(compact_k, dim3(F), dim3(256), 0, s, cur, qoff_in, F, N, G, idx, pos,
+                       qoff_out);
+}
+
+void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* Mdev, int Mmax,
+                    int D, const float* g, const float* b, void* dst, hipStream_t s) {
+    const int grid = grid_for((size_t)Mmax, 4, 4096);
+    if (bf16)
+        hipLaunchKernelGGL(ln_rows_k<true>, dim3(grid), dim3(256), 0, s, src, gather, Mdev, Mmax,
+                           D, g, b, dst);
+    else
+        hipLaunchKernelGGL(ln_rows_k<false>, dim3(grid), dim3(256), 0, s, src, gather, Mdev, Mmax,
+                           D, g, b, dst);
+}
+
+void launch_merge(float* x, const uint8_t* cur, int F, int N, int D, int G, hipStream_t s) {
+    hipLaunchKernelGGL(merge_k, dim3(grid_for((size_t)F * N, 4, 4096)), dim3(256), 0, s, x, cur,
+                       F, N, D, G);
+}
+
+void launch_final_ln(const float* x, int F, int N, int D, const float* g, const float* b,
+                     float* emb, hipStream_t s) {
+    hipLaunchKernelGGL(final_ln_k, dim3(grid_for((size_t)F, 4)), dim3(256), 0, s, x, F, N, D, g,
+                       b, emb);
+}
+
+void launch_fill_u8(uint8_t* p, size_t n, uint8_t v, hipStream_t s) {
+    hipLaunchKernelGGL(fill_u8_k, dim3(grid_for(n, 256)), dim3(256), 0, s, p, n, v);
+}
+
+void launch_zero_mask_layer(uint8_t* om, int F, int L, int N, int layer, hipStream_t s) {
+    hipLaunchKernelGGL(zero_mask_layer_k, dim3(grid_for((size_t)F * N, 256)), dim3(256), 0, s, om,
+                       F, L, N, layer);
+}
+
+}  // namespace dv
