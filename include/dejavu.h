@@ -158,8 +158,9 @@ int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size,
                int32_t* pos, int32_t* qoff, int32_t* count, hipStream_t stream);
 
 /* Stage timing with HIP events recorded on the encode stream around every
- * launch of a stage (0 = off).  While on, every dv_encode* call records; read
- * the totals after synchronising the stream.  dv_profile resets the totals. */
+ * launch of the selected stages.  stage_mask: bit s selects stage s (0 = off,
+ * DV_PROFILE_ALL = every stage).  While on, every dv_encode* call records;
+ * read the totals after synchronising the stream.  dv_profile resets them. */
 #define DV_STAGE_PATCH 0
 #define DV_STAGE_GATE 1
 #define DV_STAGE_COMPACT 2
@@ -173,7 +174,8 @@ int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size,
 #define DV_STAGE_MERGE 10
 #define DV_STAGE_FINAL 11
 #define DV_NUM_STAGES 12
-int dv_profile(dv_handle* h, int enable);
+#define DV_PROFILE_ALL 0xFFF
+int dv_profile(dv_handle* h, unsigned stage_mask);
 /* total_ms: summed event time of the stage's launches; launches: how many. */
 int dv_profile_read(dv_handle* h, int stage, double* total_ms, long long* launches);
 

@@ -95,8 +95,9 @@ int check_config(const dv_config* c, Dims* d) {
     d->Kp = (int)round_up((size_t)3 * c->patch * c->patch, 64);
     d->B = c->max_batch_frames;
     d->bf16 = bf;
-    if (attention_lds_bytes(bf, d->N, dh) > 160 * 1024)
-        return fail(DV_EUNSUPPORTED, "attention tile for N=%d, head dim %d exceeds LDS", d->N, dh);
+    if (!attention_supported(bf, d->N, dh))
+        return fail(DV_EUNSUPPORTED, "attention for N=%d tokens, head dim %d is not supported "
+                    "(bf16: head dim 64/80/96/128; keys and values of a head must fit in LDS)", d->N, dh);
     const size_t T = (size_t)d->B * d->N;
     const size_t widest = (size_t)std::max(std::max(3 * d->D, d->Dm), d->Kp);
     if (round_up(T, ROW_PAD) * widest >= (1ull << 31) || T >= (1ull << 30))
@@ -139,7 +140,7 @@ struct dv_handle {
     int *idx_id, *pos_id, *qoff_id;  // identity lists (reuse off)
     int id_frames = -1;              // frames the identity lists were built for
     // profiling
-    bool prof = false;
+    unsigned prof = 0;  // bit s: time stage s
     Stage stages[DV_NUM_STAGES];
     struct Pending {
         int stage;
@@ -158,7 +159,7 @@ struct Scope {
     hipStream_t s;
     hipEvent_t b = nullptr;
     Scope(dv_handle* h_, int st, hipStream_t s_) : h(h_), stage(st), s(s_) {
-        if (!h->prof) return;
+        if (!(h->prof >> stage & 1u)) return;
         hipEvent_t a = take(), bb = take();
         if (!a || !bb) return;
         (void)hipEventRecord(a, s);
@@ -639,12 +640,12 @@ int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size,
     return DV_OK;
 }
 
-int dv_profile(dv_handle* h, int enable) {
+int dv_profile(dv_handle* h, unsigned stage_mask) {
     if (!h) return fail(DV_EINVAL, "handle is NULL");
     int rc = collect(h);
     if (rc) return rc;
     for (auto& st : h->stages) st = Stage();
-    h->prof = enable != 0;
+    h->prof = stage_mask & DV_PROFILE_ALL;
     return DV_OK;
 }
 

@@ -3,18 +3,35 @@
 // One block per (frame f, head h).  The block stages the frame's N keys and values of
 // head h in LDS, reading each key row through pos[]: a recomputed token's own packed row,
 // or -- for a reused token -- the packed row of the same token of the reference frame.
-// Each wavefront then takes the frame's packed query rows qoff[f] .. qoff[f+1] in turn:
-// scores (lane-strided over keys), softmax in fp32 with wave reductions, then P.V with one
-// lane per output dimension.
+// The frame's packed query rows qoff[f] .. qoff[f+1] are cut into tiles of 32 that the
+// block's wavefronts take in turn.
+//
+// bf16 path (MFMA 32x32x16, fp32 accumulate), every quantity kept with one query per lane:
+//   S^T = K . Q^T      A = K rows from LDS, B = the query tile (registers); lane l holds the
+//                      scores of query l%32 against 16 of the 32 keys of a key block
+//   online softmax     max / sum over a lane's 16 registers plus one shuffle with lane l^32
+//   O^T += V^T . P^T   A = V^T, read from row-major V with the transposing LDS read
+//                      ds_read_b64_tr_b16; B = the probabilities as they sit in the S^T
+//                      accumulators; the contraction runs over the 32 keys in the order the
+//                      accumulator layout gives (the same order on both operands)
+// so a lane rescales and normalises its own query's output without any shuffle.  When a frame
+// has fewer query tiles than wavefronts, the key blocks of a tile are split across wavefronts
+// and their partial (max, sum, output) states are merged through LDS.
+//
+// fp32 path: scalar scores, softmax and P.V (small fp32 models).
+#include <algorithm>
+
 #include "dv_internal.h"
 
 namespace dv {
 
 namespace {
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
 constexpr int NWAVE = 4;
 
-// Orders LDS writes and reads of one wavefront (its lanes exchange data through LDS).
 __device__ inline void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -30,33 +47,292 @@ __device__ inline float wsum(float v) {
     return v;
 }
 
-template <bool BF>
-struct Lds {
-    static constexpr int pad = BF ? 2 : 1;
-    typedef typename std::conditional<BF, uint16_t, float>::type T;
+// ---- LDS geometry of the bf16 kernel (shared by host sizing and the kernel) ------------------
+// K rows: the MFMA reads 16 bytes (one chunk) of 16 consecutive rows; V rows: the transposing
+// read ds_read_b64_tr_b16 reads 8 bytes (4 dims) of 4 consecutive keys x 4 dim-words.  Row
+// strides and XOR swizzles (in 16-byte chunks) keep both patterns on distinct banks:
+//   head dim 64:  K chunk c of row r at c ^ ((r>>1)&7),  V chunk c of row j at c ^ 2((j>>1)&3)
+//   head dim 128: K chunk c of row r at c ^ (r&15),      V chunk c of row j at c ^ 2(j&3)
+//   head dim 80/96: no swizzle; K rows padded to dh+8, V rows to 96 elements.
+struct Geo {
+    int npad, dhp, ldk, ldv, dh;
+    __host__ __device__ Geo(int N, int d) : dh(d) {
+        npad = (N + 31) / 32 * 32;
+        dhp = (d + 31) / 32 * 32;
+        ldk = (d == 64 || d == 128) ? d : d + 8;
+        ldv = (d == 64 || d == 128) ? d : 96;
+    }
+    __host__ __device__ int kofs(int r, int c) const {
+        const int x = dh == 64 ? ((r >> 1) & 7) : dh == 128 ? (r & 15) : 0;
+        return r * ldk + (c ^ x) * 8;
+    }
+    __host__ __device__ int vofs(int j, int c) const {
+        const int x = dh == 64 ? 2 * ((j >> 1) & 3) : dh == 128 ? 2 * (j & 3) : 0;
+        return j * ldv + (c ^ x) * 8;
+    }
+    __host__ __device__ size_t bytes() const {
+        return ((size_t)npad * ldk + (size_t)npad * ldv) * 2;
+    }
 };
 
-template <bool BF>
-__device__ inline float ld(const void* p, size_t i) {
-    if (BF) return bf16_to_f32(((const uint16_t*)p)[i]);
-    return ((const float*)p)[i];
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));   // native vector: stays in VGPRs
+
+// The value a lane's partner in the other half of the wavefront (lane l ^ 32) holds.
+__device__ inline float other_half(float x) {
+    const unsigned u = __builtin_bit_cast(unsigned, x);
+    const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return __builtin_bit_cast(float, (threadIdx.x & 32) ? r[0] : r[1]);
 }
 
-template <bool BF>
-__global__ __launch_bounds__(256) void attn_k(AttnArgs a) {
-    typedef typename Lds<BF>::T T;
+constexpr int AW = 8;   // wavefronts per attention block
+
+// Work split: T = ceil(q/32) query tiles over AW wavefronts.  With T < AW a tile's key blocks
+// are split S = AW / T ways and the partial softmax states are merged through LDS.  Each
+// softmax step takes two key blocks (two independent MFMA chains, one rescale).
+template <int DH>
+__global__ __launch_bounds__(AW * 64) __attribute__((amdgpu_waves_per_eu(DH == 64 ? 4 : 2, DH == 64 ? 4 : 2)))
+void attn_mfma_k(AttnArgs a) {
+    constexpr int KS = DH / 16;          // k-steps of S^T
+    constexpr int DB = (DH + 31) / 32;   // 32-row blocks of O^T
+    constexpr int CH = DH / 8;           // 16-byte chunks per row
+    constexpr int NT = AW * 64;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int f = blockIdx.x, h = blockIdx.y;
+    const int N = a.N, D = a.D;
+    const Geo g(N, DH);
+    uint16_t* Ks = (uint16_t*)smem;
+    uint16_t* Vs = Ks + (size_t)g.npad * g.ldk;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int hl = lane >> 5, lr = lane & 31;
+    const size_t ld3 = 3 * (size_t)D;
+    const uint16_t* qkv = (const uint16_t*)a.qkv;
+    const int q0 = a.qoff[f], q1 = a.qoff[f + 1];
+    const int ntile = (q1 - q0 + 31) / 32;
+    if (ntile == 0) return;   // uniform across the block
+
+    // stage K and V rows (row-major, 16-byte chunks); keys past N repeat key N-1 (finite data
+    // whose scores are masked).  Up to four chunks per thread are gathered before any store.
+    const int total = g.npad * CH;
+    for (int c0 = tid; c0 < total; c0 += 4 * NT) {
+        size_t rowoff[4];
+        u32x4 kv[4], vv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int c = min(c0 + u * NT, total - 1);
+            const int j = min(c / CH, N - 1);
+            rowoff[u] = (size_t)a.pos[(size_t)f * N + j] * ld3 + h * DH + (c % CH) * 8;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            kv[u] = *(const u32x4*)(qkv + rowoff[u] + D);
+            vv[u] = *(const u32x4*)(qkv + rowoff[u] + 2 * D);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int c = c0 + u * NT;
+            if (c < total) {
+                const int j = c / CH, part = c % CH;
+                *(u32x4*)(Ks + g.kofs(j, part)) = kv[u];
+                *(u32x4*)(Vs + g.vofs(j, part)) = vv[u];
+            }
+        }
+    }
+    __syncthreads();
+
+    const float sl2 = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(dh)
+    const int nkb = g.npad / 32;
+    const int S = ntile >= AW ? 1 : AW / ntile;   // key-block split per tile
+    const int grp = lane >> 4, gi = lane & 15;    // 16-lane group of the transposing read
+    const int tr_key = hl * 4 + (gi >> 2);
+    const int tr_dim = (grp & 1) * 16 + (gi & 3) * 4;
+
+    // scores of key block kb against the query tile (raw, unscaled)
+    auto scores = [&](int kb, const bf16x8 (&qf)[KS]) {
+        f32x16 sc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8 kf = *(const bf16x8*)(Ks + g.kofs(kb * 32 + lr, ks * 2 + hl));
+            sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc, 0, 0, 0);
+        }
+        if ((kb + 1) * 32 > N) {   // ragged last block: keys past N get -inf
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int key = kb * 32 + (r >> 2) * 8 + hl * 4 + (r & 3);
+                sc[r] = key < N ? sc[r] : -INFINITY;
+            }
+        }
+        return sc;
+    };
+    // O^T += V^T(kb) . P^T(kb)
+    auto accumulate = [&](int kb, const bf16x8 (&pf)[2], f32x16 (&o)[DB]) {
+#pragma unroll
+        for (int b = 0; b < DB; ++b) {
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                // lane (group grp, index gi) names key kb*32 + ks*16 + hl*4 + gi/4 (+8) and
+                // dims b*32 + (grp&1)*16 + 4*(gi%4); it receives dim b*32 + (grp&1)*16 + gi
+                // of the 4 keys named by lanes 4e + gi/4 of its group
+                const int key = kb * 32 + ks * 16 + tr_key;
+                int d = b * 32 + tr_dim;
+                d = d < DH ? d : DH - 4;   // head dims past DH: any finite row data
+                const uint16_t* p0 = Vs + g.vofs(key, d >> 3) + (d & 7);
+                const uint16_t* p1 = Vs + g.vofs(key + 8, d >> 3) + (d & 7);
+                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4*)p0);
+                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4*)p1);
+                const s16x4 both[2] = {lo, hi};
+                const bf16x8 vf = __builtin_bit_cast(bf16x8, both);
+                o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
+            }
+        }
+    };
+
+    float m = -INFINITY, l = 0.f;   // running max (raw score units) and sum
+    f32x16 o[DB];
+    int my_t = -1, my_s = 0;
+    for (int item = wave; item < ntile * S; item += AW) {
+        const int t = item / S, sp = item % S;
+        my_t = t;
+        my_s = sp;
+        const int myq = q0 + t * 32 + lr;
+        const int qrow = myq < q1 ? myq : q1 - 1;   // tail lanes compute on a valid row
+        bf16x8 qf[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            qf[ks] = *(const bf16x8*)(qkv + (size_t)qrow * ld3 + h * DH + ks * 16 + hl * 8);
+#pragma unroll
+        for (int b = 0; b < DB; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) o[b][r] = 0.f;
+        m = -INFINITY;
+        l = 0.f;
+        for (int kb = sp; kb < nkb; kb += 2 * S) {
+            const int kb1 = kb + S;
+            const bool two = kb1 < nkb;
+            const f32x16 s0 = scores(kb, qf);
+            f32x16 s1;
+            if (two) {
+                s1 = scores(kb1, qf);
+            } else {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) s1[r] = -INFINITY;
+            }
+            float bm = -INFINITY;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) bm = fmaxf(bm, fmaxf(s0[r], s1[r]));
+            bm = fmaxf(bm, other_half(bm));
+            if (__any(bm > m)) {   // rescale only when some lane's running max moved
+                const float mn = fmaxf(m, bm);
+                const float alpha = __builtin_amdgcn_exp2f((m - mn) * sl2);
+                l *= alpha;
+#pragma unroll
+                for (int b = 0; b < DB; ++b)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) o[b][r] *= alpha;
+                m = mn;
+            }
+            const float nm = -m * sl2;
+            float ps = 0.f;
+            bf16x8 p0[2], p1[2];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], sl2, nm));
+                const float e1 = __builtin_amdgcn_exp2f(fmaf(s1[r], sl2, nm));
+                ps += e0 + e1;
+                p0[r >> 3][r & 7] = (__bf16)e0;
+                p1[r >> 3][r & 7] = (__bf16)e1;
+            }
+            l += ps + other_half(ps);
+            accumulate(kb, p0, o);
+            if (two) accumulate(kb1, p1, o);
+        }
+        if (S == 1 && myq < q1) {
+            const float inv = 1.0f / l;
+            uint16_t* dst = (uint16_t*)a.out + (size_t)myq * D + h * DH;
+#pragma unroll
+            for (int b = 0; b < DB; ++b)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int d = b * 32 + q4 * 8 + hl * 4;
+                    if (d < DH) {
+                        uint2 pk;
+                        pk.x = (uint32_t)f32_to_bf16(o[b][q4 * 4 + 0] * inv) |
+                               ((uint32_t)f32_to_bf16(o[b][q4 * 4 + 1] * inv) << 16);
+                        pk.y = (uint32_t)f32_to_bf16(o[b][q4 * 4 + 2] * inv) |
+                               ((uint32_t)f32_to_bf16(o[b][q4 * 4 + 3] * inv) << 16);
+                        *(uint2*)(dst + d) = pk;
+                    }
+                }
+        }
+    }
+    if (S == 1) return;   // uniform across the block: S depends only on the frame
+
+    // merge the S partial states of each tile (LDS reused: K/V are no longer read)
+    __syncthreads();
+    float* part = (float*)smem;                       // [AW][2 + DB*32][32] floats
+    constexpr int STRIDE = (2 + DB * 32) * 32;
+    if (my_t >= 0) {
+        float* pw = part + wave * STRIDE;
+        if (hl == 0) {
+            pw[lr] = m;
+            pw[32 + lr] = l;
+        }
+#pragma unroll
+        for (int b = 0; b < DB; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int d = b * 32 + (r >> 2) * 8 + hl * 4 + (r & 3);
+                pw[(2 + d) * 32 + lr] = o[b][r];
+            }
+    }
+    __syncthreads();
+    if (my_t >= 0 && my_s == 0) {
+        const int myq = q0 + my_t * 32 + lr;
+        float M = -INFINITY;
+        for (int sp = 0; sp < S; ++sp) M = fmaxf(M, part[(wave + sp) * STRIDE + lr]);
+        float L = 0.f;
+        for (int sp = 0; sp < S; ++sp)
+            L += __builtin_amdgcn_exp2f((part[(wave + sp) * STRIDE + lr] - M) * sl2) *
+                 part[(wave + sp) * STRIDE + 32 + lr];
+        if (myq < q1) {
+            const float inv = 1.0f / L;
+            uint16_t* dst = (uint16_t*)a.out + (size_t)myq * D + h * DH;
+            for (int d0 = hl * 4; d0 < DH; d0 += 8) {
+                float v[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float acc = 0.f;
+                    for (int sp = 0; sp < S; ++sp)
+                        acc += __builtin_amdgcn_exp2f((part[(wave + sp) * STRIDE + lr] - M) * sl2) *
+                               part[(wave + sp) * STRIDE + (2 + d0 + e) * 32 + lr];
+                    v[e] = acc * inv;
+                }
+                uint2 pk;
+                pk.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+                pk.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+                *(uint2*)(dst + d0) = pk;
+            }
+        }
+    }
+}
+
+// ---- fp32 path ---------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void attn_f32_k(AttnArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int f = blockIdx.x, h = blockIdx.y;
     const int N = a.N, D = a.D, dh = D / a.H;
-    const int ldk = dh + Lds<BF>::pad;
-    T* Ks = (T*)smem;
-    T* Vs = Ks + (size_t)N * ldk;
-    float* qs = (float*)(((uintptr_t)(Vs + (size_t)N * dh) + 15) & ~(uintptr_t)15);
+    const int ldk = dh + 1;
+    float* Ks = (float*)smem;
+    float* Vs = Ks + (size_t)N * ldk;
+    float* qs = Vs + (size_t)N * dh;
     float* ps = qs + NWAVE * dh;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const size_t ld3 = 3 * (size_t)D;
-    const T* qkv = (const T*)a.qkv;
-
+    const float* qkv = (const float*)a.qkv;
     for (int e = tid; e < N * dh; e += 256) {
         const int j = e / dh, d = e % dh;
         const size_t row = (size_t)a.pos[(size_t)f * N + j];
@@ -64,24 +340,17 @@ __global__ __launch_bounds__(256) void attn_k(AttnArgs a) {
         Vs[j * dh + d] = qkv[row * ld3 + 2 * D + h * dh + d];
     }
     __syncthreads();
-
     const float scale = 1.0f / sqrtf((float)dh);
     const int q0 = a.qoff[f], q1 = a.qoff[f + 1];
     float* myq = qs + wave * dh;
     float* myp = ps + wave * N;
     for (int q = q0 + wave; q < q1; q += NWAVE) {
-        for (int d = lane; d < dh; d += 64) myq[d] = ld<BF>(qkv, (size_t)q * ld3 + h * dh + d) * scale;
+        for (int d = lane; d < dh; d += 64) myq[d] = qkv[(size_t)q * ld3 + h * dh + d] * scale;
         wave_lds_sync();
         float mx = -INFINITY;
         for (int j = lane; j < N; j += 64) {
             float s = 0.f;
-            const T* kr = Ks + j * ldk;
-            for (int d = 0; d < dh; ++d) {
-                float kv;
-                if (BF) kv = bf16_to_f32(((const uint16_t*)kr)[d]);
-                else kv = ((const float*)kr)[d];
-                s = fmaf(myq[d], kv, s);
-            }
+            for (int d = 0; d < dh; ++d) s = fmaf(myq[d], Ks[j * ldk + d], s);
             myp[j] = s;
             mx = fmaxf(mx, s);
         }
@@ -97,41 +366,66 @@ __global__ __launch_bounds__(256) void attn_k(AttnArgs a) {
         const float inv = 1.0f / sum;
         for (int d = lane; d < dh; d += 64) {
             float o = 0.f;
-            for (int j = 0; j < N; ++j) {
-                float vv;
-                if (BF) vv = bf16_to_f32(((const uint16_t*)Vs)[j * dh + d]);
-                else vv = ((const float*)Vs)[j * dh + d];
-                o = fmaf(myp[j], vv, o);
-            }
-            o *= inv;
-            if (BF) ((uint16_t*)a.out)[(size_t)q * D + h * dh + d] = f32_to_bf16(o);
-            else ((float*)a.out)[(size_t)q * D + h * dh + d] = o;
+            for (int j = 0; j < N; ++j) o = fmaf(myp[j], Vs[j * dh + d], o);
+            ((float*)a.out)[(size_t)q * D + h * dh + d] = o * inv;
         }
         wave_lds_sync();  // this wave's myq/myp are rewritten by its next query
     }
 }
 
+size_t f32_lds_bytes(int N, int dh) {
+    return ((size_t)N * (dh + 1) + (size_t)N * dh + (size_t)NWAVE * dh + (size_t)NWAVE * N) * 4;
+}
+
+template <int DH>
+void launch_bf16(const AttnArgs& a, hipStream_t s) {
+    static bool raised = false;
+    const size_t merge = (size_t)AW * (2 + (DH + 31) / 32 * 32) * 32 * 4;
+    const size_t lds = std::max(Geo(a.N, DH).bytes(), merge);
+    if (!raised) {  // allow more than the default dynamic LDS (gfx950 has 160 KiB per CU)
+        (void)hipFuncSetAttribute((const void*)attn_mfma_k<DH>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        raised = true;
+    }
+    hipLaunchKernelGGL(attn_mfma_k<DH>, dim3(a.F, a.H), dim3(AW * 64), lds, s, a);
+}
+
 }  // namespace
 
 size_t attention_lds_bytes(bool bf16, int N, int dh) {
-    const size_t el = bf16 ? 2 : 4;
-    const size_t ldk = dh + (bf16 ? 2 : 1);
-    size_t b = (size_t)N * ldk * el + (size_t)N * dh * el;
-    b = (b + 15) & ~(size_t)15;
-    return b + (size_t)NWAVE * dh * 4 + (size_t)NWAVE * N * 4;
+    return bf16 ? Geo(N, dh).bytes() : f32_lds_bytes(N, dh);
+}
+
+bool attention_supported(bool bf16, int N, int dh) {
+    if (attention_lds_bytes(bf16, N, dh) > 160 * 1024) return false;
+    if (bf16) {
+        // the merge of split partial states reuses the K/V area
+        const size_t merge = (size_t)AW * (2 + (dh + 31) / 32 * 32) * 32 * 4;
+        return (dh == 64 || dh == 80 || dh == 96 || dh == 128) &&
+               std::max(attention_lds_bytes(true, N, dh), merge) <= 160 * 1024;
+    }
+    return dh % 16 == 0;
 }
 
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s) {
     const int dh = a.D / a.H;
-    const size_t lds = attention_lds_bytes(bf16, a.N, dh);
-    static bool raised[2] = {false, false};
-    if (!raised[bf16]) {  // allow more than the default dynamic LDS (gfx950 has 160 KiB per CU)
-        (void)hipFuncSetAttribute(bf16 ? (const void*)attn_k<true> : (const void*)attn_k<false>,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-        raised[bf16] = true;
+    if (!bf16) {
+        static bool raised = false;
+        if (!raised) {
+            (void)hipFuncSetAttribute((const void*)attn_f32_k,
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            raised = true;
+        }
+        hipLaunchKernelGGL(attn_f32_k, dim3(a.F, a.H), dim3(256), f32_lds_bytes(a.N, dh), s, a);
+        return;
     }
-    if (bf16) hipLaunchKernelGGL(attn_k<true>, dim3(a.F, a.H), dim3(256), lds, s, a);
-    else hipLaunchKernelGGL(attn_k<false>, dim3(a.F, a.H), dim3(256), lds, s, a);
+    switch (dh) {
+        case 64: launch_bf16<64>(a, s); break;
+        case 80: launch_bf16<80>(a, s); break;
+        case 96: launch_bf16<96>(a, s); break;
+        case 128: launch_bf16<128>(a, s); break;
+        default: break;  // rejected at handle creation
+    }
 }
 
 }  // namespace dv

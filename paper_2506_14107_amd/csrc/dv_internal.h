@@ -53,6 +53,7 @@ struct AttnArgs {
 };
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
 size_t attention_lds_bytes(bool bf16, int N, int dh);
+bool attention_supported(bool bf16, int N, int dh);
 
 // ---- row kernels -----------------------------------------------------------------------------
 void launch_im2col(bool bf16, const float* frames, int F, int S, int p, int Kp, void* A,

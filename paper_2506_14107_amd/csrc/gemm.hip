@@ -1,14 +1,29 @@
 // Packed-row GEMMs: C[M, Nout] = A[M, K] * W[Nout, K]^T + fused epilogue.
 //
-// bf16 path: MFMA v_mfma_f32_32x32x16_bf16 (fp32 accumulate) on LDS-staged tiles.
-// Both operands are K-contiguous rows, so A and B fragments are the same kind of
-// 16-byte LDS read: lane l takes row (l % 32) and k-slice (l / 32) * 8 .. +8.
-// The accumulator of lane l, register j holds row (j/4)*8 + (l/32)*4 + j%4, column l%32.
+// M (the number of packed recompute rows) lives in device memory; the grid is sized for the
+// largest possible M and blocks past the live tiles return at once.
 //
-// fp32 path: a plain LDS-tiled VALU GEMM (used by fp32 models).
+// bf16 path: MFMA v_mfma_f32_32x32x16_bf16 with fp32 accumulation.
+//   * Block tile BM x BN, 4 wavefronts in 2 x 2, each owning (BM/2) x (BN/2) of 32 x 32 tiles.
+//   * k-slices of BK travel global -> LDS with global_load_lds_dwordx4 (no staging registers)
+//     through a ring of S stages: S-1 slices are in flight while one is consumed.  One
+//     wavefront instruction writes 1 KiB of LDS (lane i at base + 16 i).  LDS rows are BK*2
+//     bytes without padding; lane i fetches the global chunk that belongs at its slot: chunk
+//     c of tile row r sits at slot c ^ swz(r), so 16 lanes reading one chunk of 16 rows hit
+//     distinct banks.
+//   * Both operands are K-contiguous rows, so A and B fragments are the same 16-byte LDS read:
+//     lane l takes row l%32 and k-slice (l/32)*8 .. +8.  The weight fragment is the MFMA's
+//     first operand, so the accumulator is the transposed tile: lane l, register j holds output
+//     column (j/4)*8 + (l/32)*4 + j%4 of token row l%32 -- four consecutive columns per
+//     register group, stored as one vector by the epilogue.
+//   * The fragments of k-step ks+1 are read while the MFMAs of k-step ks run.
+//   * Tile order: the live tiles (ceil(M/BM) * Nout/BN) go round-robin over the 8 XCDs in
+//     contiguous chunks, each chunk walking groups of 8 tile-rows across all tile-columns, so
+//     an XCD's L2 sees few distinct A and W tiles.
 //
-// M (the number of packed recompute rows) lives in device memory; the grid is sized for
-// the largest possible M and row tiles past M return at once.
+// fp32 path: a plain LDS-tiled VALU GEMM (small fp32 models).
+#include <cstdlib>
+
 #include "dv_internal.h"
 
 namespace dv {
@@ -16,9 +31,34 @@ namespace dv {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ inline float gelu_erf(float v) { return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f)); }
+
+// GELU with the normal CDF from Abramowitz & Stegun, Handbook of Mathematical Functions,
+// formula 7.1.26 (|error of erf| <= 1.5e-7): for z = |x|/sqrt(2), t = 1/(1 + p z),
+// Phi(-|x|) = 0.5 (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-z^2), which keeps its relative
+// accuracy in the tail; Phi(x) = 1 - Phi(-|x|) for x >= 0.  Used where the result is rounded to
+// bf16 (bf16 step 2^-8 relative, far above the approximation error).
+__device__ inline float gelu_as(float x) {
+    const float z = fabsf(x) * 0.70710678118654752f;
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, z, 1.0f));
+    float p = fmaf(1.061405429f, t, -1.453152027f);
+    p = fmaf(p, t, 1.421413741f);
+    p = fmaf(p, t, -0.284496736f);
+    p = fmaf(p, t, 0.254829592f);
+    p *= t;
+    const float q = 0.5f * p * __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);
+    return x * (x >= 0.0f ? 1.0f - q : q);
+}
+
+__device__ inline u32x2 pack_bf16x4(f32x4 v) {
+    bf16x4 h = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};  // v_cvt_pk_bf16_f32 (RNE)
+    return __builtin_bit_cast(u32x2, h);
+}
 
 template <Epi E, bool BF>
 __device__ inline void epi_store(const GemmArgs& a, int row, int col, float acc) {
@@ -44,91 +84,179 @@ __device__ inline void epi_store(const GemmArgs& a, int row, int col, float acc)
     }
 }
 
-// ---------------- bf16 MFMA GEMM: block tile 128 x 128, k-step 32, 4 waves of 64 x 64 --------
-constexpr int BM = 128, BN = 128, BK = 32;
-constexpr int LDK = BK + 8;  // padded LDS row (bf16 elements): 80 bytes, conflict-free b128 reads
-
+// Epilogue on four consecutive columns col .. col+3 of one row (bf16 path).
+// trow: the token row the output (Patch, Fc2) or the residual (OProj) lives in.
 template <Epi E>
-__global__ __launch_bounds__(256) void gemm_bf16_k(GemmArgs a) {
-    __shared__ __attribute__((aligned(16))) uint16_t sA[BM * LDK];
-    __shared__ __attribute__((aligned(16))) uint16_t sB[BN * LDK];
+__device__ inline void epi_store4(const GemmArgs& a, int row, int trow, int col, f32x4 v) {
+    v += *(const f32x4*)(a.bias + col);
+    const size_t Nout = a.Nout;
+    if constexpr (E == Epi::Patch) {
+        v += *(const f32x4*)(a.pos + (size_t)(1 + row % a.P) * Nout + col);
+        *(f32x4*)((float*)a.out + (size_t)trow * Nout + col) = v;
+    } else if constexpr (E == Epi::Qkv) {
+        *(u32x2*)((uint16_t*)a.out + (size_t)row * Nout + col) = pack_bf16x4(v);
+    } else if constexpr (E == Epi::Fc1) {
+        f32x4 g = {gelu_as(v[0]), gelu_as(v[1]), gelu_as(v[2]), gelu_as(v[3])};
+        *(u32x2*)((uint16_t*)a.out + (size_t)row * Nout + col) = pack_bf16x4(g);
+    } else if constexpr (E == Epi::OProj) {
+        v += *(const f32x4*)(a.resid + (size_t)trow * Nout + col);
+        *(f32x4*)((float*)a.out + (size_t)row * Nout + col) = v;
+    } else {  // Fc2
+        v += *(const f32x4*)(a.resid + (size_t)row * Nout + col);
+        *(f32x4*)((float*)a.out + (size_t)trow * Nout + col) = v;
+    }
+}
+
+// s_waitcnt vmcnt(n) lgkmcnt(0) (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4 left
+// at its maximum, lgkmcnt 11:8): all of this wave's loads but the last n have landed in LDS and
+// its own LDS reads are complete.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0070 | (N & 15) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier without the memory fence of __syncthreads() (that fence would wait for
+// every load in flight, i.e. drain the LDS ring).  Callers order memory with wait_vm first; the
+// signal fences stop the compiler from moving memory accesses across the barrier.
+__device__ __forceinline__ void bare_barrier() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+template <int BM, int BN, int BKD, int S>
+constexpr size_t dma_lds_bytes() { return (size_t)S * (BM + BN) * BKD * 2; }
+
+template <Epi E, int BM, int BN, int BKD, int S, int WPE>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
+void gemm_bf16_k(GemmArgs a) {
+    constexpr int WM = BM / 2, WN = BN / 2, TI = WM / 32, TJ = WN / 32;
+    constexpr int CPR = BKD / 8;                 // 16-byte chunks per LDS row
+    constexpr int RPI = 64 / CPR;                // rows one wavefront instruction fills
+    constexpr int SH = (CPR == 8) ? 1 : 2;       // slot = chunk ^ ((row >> SH) & (CPR - 1))
+    constexpr int LA = BM / RPI / 4, LB = BN / RPI / 4;   // load instructions per wave per stage
+    constexpr int L = LA + LB;
+    constexpr int STAGE = (BM + BN) * BKD;       // elements per stage
+    constexpr int KS = BKD / 16;
+    static_assert(CPR == 4 || CPR == 8, "BK must be 32 or 64");
+    static_assert(LA >= 1 && LB >= 1, "tile too small for 4 wavefronts");
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    uint16_t* sm = (uint16_t*)smem;
+
     const int M = a.Mdev ? *a.Mdev : a.Mconst;
     const int tilesN = a.Nout / BN;
-    const int tm = blockIdx.x / tilesN, tn = blockIdx.x % tilesN;
-    if (tm * BM >= M) return;
+    const int mt = (M + BM - 1) / BM;
+    const int active = mt * tilesN;
+    const int bid = blockIdx.x;
+    if (bid >= active) return;
+    int lid = bid;
+    const int per = active / 8;
+    if (bid < per * 8) lid = (bid % 8) * per + bid / 8;
+    constexpr int GM = 8;
+    const int group = lid / (GM * tilesN);
+    const int first_m = group * GM;
+    const int gsize = min(mt - first_m, GM);
+    const int w_in = lid - group * GM * tilesN;
+    const int tm = first_m + w_in % gsize;
+    const int tn = w_in / gsize;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
+    const int lr = lane & 31, hl = lane >> 5;
     const int K = a.K;
-    const uint16_t* Ab = (const uint16_t*)a.A + (size_t)tm * BM * K;
-    const uint16_t* Wb = (const uint16_t*)a.W + (size_t)tn * BN * K;
 
-    // each thread moves 2 16-byte chunks of A and 2 of B per k-step
-    int lrow[2], lk[2];
+    // this lane's global source for each of its load instructions (k offset added per stage)
+    const int lrow = lane / CPR, lslot = lane % CPR;
+    const uint16_t* srcA[LA];
+    const uint16_t* srcB[LB];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int c = tid + 256 * i;
-        lrow[i] = c >> 2;
-        lk[i] = (c & 3) * 8;
+    for (int t = 0; t < LA; ++t) {
+        const int r = (wave * LA + t) * RPI + lrow;
+        const int c = lslot ^ ((r >> SH) & (CPR - 1));
+        srcA[t] = (const uint16_t*)a.A + (size_t)(tm * BM + r) * K + c * 8;
     }
-    uint4 ra[2], rb[2];
-    auto gload = [&](int k0) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            ra[i] = *(const uint4*)(Ab + (size_t)lrow[i] * K + k0 + lk[i]);
-            rb[i] = *(const uint4*)(Wb + (size_t)lrow[i] * K + k0 + lk[i]);
-        }
+    for (int t = 0; t < LB; ++t) {
+        const int r = (wave * LB + t) * RPI + lrow;
+        const int c = lslot ^ ((r >> SH) & (CPR - 1));
+        srcB[t] = (const uint16_t*)a.W + (size_t)(tn * BN + r) * K + c * 8;
+    }
+    auto issue = [&](int kt) {
+        uint16_t* st = sm + (kt % S) * STAGE;
+#pragma unroll
+        for (int t = 0; t < LA; ++t)
+            __builtin_amdgcn_global_load_lds((const void*)(srcA[t] + kt * BKD),
+                (__attribute__((address_space(3))) void*)(st + (wave * LA + t) * RPI * BKD), 16, 0, 0);
+#pragma unroll
+        for (int t = 0; t < LB; ++t)
+            __builtin_amdgcn_global_load_lds((const void*)(srcB[t] + kt * BKD),
+                (__attribute__((address_space(3))) void*)(st + BM * BKD + (wave * LB + t) * RPI * BKD), 16, 0, 0);
     };
 
-    f32x16 acc[2][2];
+    f32x16 acc[TI][TJ];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TI; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < TJ; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    gload(0);
-    for (int k0 = 0; k0 < K; k0 += BK) {
-        __syncthreads();
+    const int nk = K / BKD;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            *(uint4*)(sA + lrow[i] * LDK + lk[i]) = ra[i];
-            *(uint4*)(sB + lrow[i] * LDK + lk[i]) = rb[i];
-        }
-        __syncthreads();
-        if (k0 + BK < K) gload(k0 + BK);
+    for (int p = 0; p < S - 1; ++p)
+        if (p < nk) issue(p);
+    for (int kt = 0; kt < nk; ++kt) {
+        // slices kt .. min(kt+S-2, nk-1) are in flight: wait for slice kt only
+        if (kt + S - 2 < nk) wait_vm<(S - 2) * L>();
+        else wait_vm<0>();
+        bare_barrier();
+        if (kt + S - 1 < nk) issue(kt + S - 1);   // reuses the slot consumed at kt-1
+        const uint16_t* st = sm + (kt % S) * STAGE;
+        bf16x8 fa[2][TI], fb[2][TJ];
+        auto frag = [&](int ks, bf16x8 (&xa)[TI], bf16x8 (&xb)[TJ]) {
+            const int c = ks * 2 + hl;
 #pragma unroll
-        for (int ks = 0; ks < BK; ks += 16) {
-            bf16x8 fa[2], fb[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int row = wm * 64 + i * 32 + (lane & 31);
-                fa[i] = *(const bf16x8*)(sA + row * LDK + ks + (lane >> 5) * 8);
+            for (int i = 0; i < TI; ++i) {
+                const int r = wm * WM + i * 32 + lr;
+                xa[i] = *(const bf16x8*)(st + r * BKD + (c ^ ((r >> SH) & (CPR - 1))) * 8);
             }
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int row = wn * 64 + j * 32 + (lane & 31);
-                fb[j] = *(const bf16x8*)(sB + row * LDK + ks + (lane >> 5) * 8);
+            for (int j = 0; j < TJ; ++j) {
+                const int r = wn * WN + j * 32 + lr;
+                xb[j] = *(const bf16x8*)(st + BM * BKD + r * BKD + (c ^ ((r >> SH) & (CPR - 1))) * 8);
             }
+        };
+        frag(0, fa[0], fb[0]);
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks + 1 < KS) frag(ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+            for (int i = 0; i < TI; ++i)
+#pragma unroll
+                for (int j = 0; j < TJ; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks & 1][j], fa[ks & 1][i],
+                                                                        acc[i][j], 0, 0, 0);
         }
     }
 
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TI; ++i) {
+        const int row = tm * BM + wm * WM + i * 32 + lr;
+        if (row >= M) continue;
+        int trow = row;
+        if constexpr (E == Epi::OProj || E == Epi::Fc2) trow = a.idx[row];
+        if constexpr (E == Epi::Patch) trow = (row / a.P) * a.N + 1 + row % a.P;
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < TJ; ++j)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int row = tm * BM + wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                const int col = tn * BN + wn * 64 + j * 32 + (lane & 31);
-                if (row < M) epi_store<E, true>(a, row, col, acc[i][j][r]);
+            for (int g = 0; g < 4; ++g) {
+                const int col = tn * BN + wn * WN + j * 32 + g * 8 + hl * 4;
+                f32x4 v = {acc[i][j][g * 4 + 0], acc[i][j][g * 4 + 1], acc[i][j][g * 4 + 2],
+                           acc[i][j][g * 4 + 3]};
+                epi_store4<E>(a, row, trow, col, v);
             }
+    }
 }
 
 // ---------------- fp32 VALU GEMM: block tile 64 x 64, k-step 16, 4 x 4 outputs per thread ---
@@ -180,14 +308,55 @@ __global__ __launch_bounds__(256) void gemm_f32_k(GemmArgs a) {
     }
 }
 
+
+template <Epi E, int BM, int BN, int BKD, int S, int WPE>
+void launch_cfg(const GemmArgs& a, hipStream_t s) {
+    static bool raised = false;
+    constexpr size_t lds = dma_lds_bytes<BM, BN, BKD, S>();
+    static_assert(lds <= 160 * 1024, "LDS ring exceeds 160 KiB");
+    if (!raised) {  // more than the default dynamic LDS (gfx950: 160 KiB per CU)
+        (void)hipFuncSetAttribute((const void*)gemm_bf16_k<E, BM, BN, BKD, S, WPE>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        raised = true;
+    }
+    const int grid = ((a.Mmax + BM - 1) / BM) * (a.Nout / BN);
+    hipLaunchKernelGGL((gemm_bf16_k<E, BM, BN, BKD, S, WPE>), dim3(grid), dim3(256), lds, s, a);
+}
+
+// Tile configuration per GEMM: the tuning override DV_GEMM_CFG picks another table row.
+int gemm_cfg() {
+    static int v = -1;
+    if (v < 0) {
+        const char* e = getenv("DV_GEMM_CFG");
+        v = e ? atoi(e) : 0;
+    }
+    return v;
+}
+
 template <Epi E>
 void launch_one(bool bf16, const GemmArgs& a, hipStream_t s) {
-    if (bf16) {
-        const int grid = ((a.Mmax + BM - 1) / BM) * (a.Nout / BN);
-        hipLaunchKernelGGL(gemm_bf16_k<E>, dim3(grid), dim3(256), 0, s, a);
-    } else {
+    if (!bf16) {
         const int grid = ((a.Mmax + FBM - 1) / FBM) * (a.Nout / FBN);
         hipLaunchKernelGGL(gemm_f32_k<E>, dim3(grid), dim3(256), 0, s, a);
+        return;
+    }
+    const bool wide = E != Epi::Patch && a.Nout % 256 == 0 && a.Nout / 256 >= 8;
+    (void)wide;
+    switch (gemm_cfg()) {
+        case 1:
+            if (wide) launch_cfg<E, 256, 256, 32, 4, 1>(a, s);
+            else launch_cfg<E, 256, 128, 64, 3, 1>(a, s);
+            break;
+        case 2:
+            if (wide) launch_cfg<E, 256, 256, 64, 2, 1>(a, s);
+            else launch_cfg<E, 256, 128, 32, 3, 2>(a, s);
+            break;
+        case 3:
+            launch_cfg<E, 128, 128, 64, 3, 2>(a, s);
+            break;
+        default:  // 256 x 128 tiles, 3-stage ring of 32-wide k-slices: two blocks per CU
+            launch_cfg<E, 256, 128, 32, 3, 2>(a, s);
+            break;
     }
 }
 

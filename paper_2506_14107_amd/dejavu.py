@@ -60,7 +60,7 @@ def load(path=None):
                                             _P, _P, _P, _P, _P]),
         "dv_compact": (ctypes.c_int, [_P, ctypes.c_int, ctypes.c_int, ctypes.c_int, _P, _P, _P,
                                       _P, _P]),
-        "dv_profile": (ctypes.c_int, [_P, ctypes.c_int]),
+        "dv_profile": (ctypes.c_int, [_P, ctypes.c_uint]),
         "dv_profile_read": (ctypes.c_int, [_P, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_longlong)]),
     }
@@ -131,8 +131,11 @@ def dv_compact(masks, n_frames, n_tokens, group_size, idx, pos, qoff, count, str
                              stream))
 
 
-def dv_profile(handle, enable):
-    _check(load().dv_profile(handle, int(enable)))
+DV_PROFILE_ALL = 0xFFF
+
+
+def dv_profile(handle, stage_mask):
+    _check(load().dv_profile(handle, int(stage_mask)))
 
 
 def dv_profile_read(handle, stage):
@@ -219,8 +222,15 @@ class Encoder:
                              _ptr(masks), _stream(stream))
         return emb, masks, toks
 
-    def profile(self, enable):
-        dv_profile(self.handle, enable)
+    def profile(self, stages=True):
+        """stages: True (all), False (off), or an iterable of stage names."""
+        if stages is True:
+            mask = DV_PROFILE_ALL
+        elif not stages:
+            mask = 0
+        else:
+            mask = sum(1 << STAGES.index(s) for s in stages)
+        dv_profile(self.handle, mask)
 
     def profile_read(self):
         return {name: dv_profile_read(self.handle, i) for i, name in enumerate(STAGES)}

@@ -16,6 +16,11 @@ TINY = synth.get_config("tiny")
 SMALL_BF16 = ModelConfig(64, 16, 2, 128, 2, 256, "bf16")
 # N = 50 tokens in bf16 with three layers
 MID_BF16 = ModelConfig(112, 16, 3, 256, 4, 512, "bf16")
+# ViT-L/14 token counts (257 at 224 px, 577 at 336 px) with a narrow width
+N257_BF16 = ModelConfig(224, 14, 2, 128, 2, 256, "bf16")
+N577_BF16 = ModelConfig(336, 14, 1, 128, 2, 256, "bf16")
+# head dim 80 (the ViT-H/14-class width 1280 / 16 heads)
+DH80_BF16 = ModelConfig(64, 16, 2, 640, 8, 1280, "bf16")
 
 
 def _video(m, n, seed=2000, sigma=0.01, speed=3.0, n_obj=2, size=None, pan=0.0):
@@ -166,8 +171,10 @@ def test_batching_and_determinism_bitwise():
 
 
 @pytest.mark.parametrize("m,n,G", [(TINY.model, 7, 4), (SMALL_BF16, 9, 4), (SMALL_BF16, 1, 4),
-                                   (MID_BF16, 10, 3)],
-                         ids=["tiny-ragged", "small-ragged", "single-frame", "mid-G3"])
+                                   (MID_BF16, 10, 3), (N257_BF16, 6, 4), (N577_BF16, 3, 2),
+                                   (DH80_BF16, 5, 4)],
+                         ids=["tiny-ragged", "small-ragged", "single-frame", "mid-G3", "n257",
+                              "n577", "dh80"])
 def test_injection_mode_parity(m, n, G):
     """Random, non-monotone injected maps; partial last group."""
     torch = require_gpu()
@@ -201,7 +208,8 @@ def test_single_token_injection():
     check_close(t, r["tokens"], "bf16", "tokens")
 
 
-@pytest.mark.parametrize("m", [SMALL_BF16, MID_BF16], ids=["small", "mid"])
+@pytest.mark.parametrize("m", [SMALL_BF16, MID_BF16, N257_BF16, DH80_BF16],
+                         ids=["small", "mid", "n257", "dh80"])
 def test_bf16_gate_mode_parity(m):
     torch = require_gpu()
     blob = synth.make_blob(m, 26)
