@@ -63,6 +63,40 @@ def stage_flops(stage, m, Ml):
     return 0.0
 
 
+def stage_bytes(stage, m, Ml):
+    """Algorithmic HBM bytes of one launch of a GEMM stage at M_l active rows: bf16 operand rows
+    and weights read once, fp32 residual rows read once, outputs written once, row indices."""
+    D, Dm = m.width, m.mlp
+    if stage == "qkv":
+        return Ml * D * 2 + 3 * D * D * 2 + Ml * 3 * D * 2
+    if stage == "oproj":
+        return Ml * D * 2 + D * D * 2 + Ml * D * 4 + Ml * 4 + Ml * D * 4
+    if stage == "fc1":
+        return Ml * D * 2 + Dm * D * 2 + Ml * Dm * 2
+    if stage == "fc2":
+        return Ml * Dm * 2 + D * Dm * 2 + Ml * D * 4 + Ml * 4 + Ml * D * 4
+    return 0.0
+
+
+KERNEL_SOURCE = {"qkv": "gemm.hip", "oproj": "gemm.hip", "fc1": "gemm.hip", "fc2": "gemm.hip",
+                 "attn": "attention.hip"}
+
+
+def measured_traffic(stage):
+    """HBM bytes per launch of `stage` from the committed counter record, if it was taken from
+    the current kernel source; else None."""
+    import hashlib
+    rec = os.path.join(ROOT, "profiles", f"{stage}_hbm_traffic.json")
+    src = KERNEL_SOURCE.get(stage)
+    if not src or not os.path.exists(rec):
+        return None
+    with open(rec) as fh:
+        r = json.load(fh)
+    path = os.path.join(ROOT, "paper_2506_14107_amd", "csrc", src)
+    sha = hashlib.sha256(open(path, "rb").read()).hexdigest()
+    return r["traffic_bytes_per_launch"] if r.get("source_sha256") == sha else None
+
+
 def calibrate(enc, x, G, target, iters=24):
     """Bisection of tau in [-1, 1] so that the batch's reuse rate is within 0.01 of target."""
     import torch
@@ -84,8 +118,8 @@ def calibrate(enc, x, G, target, iters=24):
     return best
 
 
-def cpu_baseline(w, blob, frames, taus, budget_s=20.0):
-    """The CPU oracle (fp64) on whole groups of the same frames, one group per reuse level."""
+def cpu_baseline(w, blob, frames, taus, groups_per_level=2, budget_s=30.0):
+    """The CPU oracle (fp64) on whole groups of the same frames, two groups per reuse level."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -94,16 +128,19 @@ def cpu_baseline(w, blob, frames, taus, budget_s=20.0):
         threads = len(os.sched_getaffinity(0))
     G = w.group_size
     done, t0 = 0, time.time()
+    ngroups = frames.shape[0] // G
     for k, tau in enumerate(taus):
-        g0 = (k % (frames.shape[0] // G)) * G
-        oracle.encode(frames[g0:g0 + G], blob, w.model.as_dict(), G, tau=tau)
-        done += G
+        for gsel in range(groups_per_level):
+            g0 = ((k * groups_per_level + gsel) % ngroups) * G
+            oracle.encode(frames[g0:g0 + G], blob, w.model.as_dict(), G, tau=tau)
+            done += G
         if time.time() - t0 > budget_s:
             break
     dt = time.time() - t0
-    return {"value": done / dt, "unit": "frames/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} frames ({done // G} group(s) of {G}), one group per reuse level, "
-                      f"fp64 NumPy, {dt:.1f} s"}
+    return {"value": round(done / dt, 3), "unit": "frames/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{done} frames ({done // G} groups of {G}: {groups_per_level} per reuse level "
+                      f"at the calibrated thresholds), fp64 NumPy, {dt:.1f} s"}
 
 
 def main():
@@ -113,6 +150,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="vit_l14")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 1 GiB device-to-device copy (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported (this path runs "
@@ -200,10 +239,13 @@ def main():
     if flops > 0:
         achieved = flops / (stage_ms * 1e-3) / 1e12
         peak = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_FP32_TFLOPS
+        algo_b = args.steps * sum(stage_bytes(dominant, m, Ml) for lv in levels for Ml in lv["Ml"])
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": None,
+                "frac": round(achieved / peak, 4), "traffic": measured_traffic(dominant),
                 "kernel": dominant, "launches": launches,
-                "avg_launch_us": round(stage_ms / max(launches, 1) * 1e3, 2)}
+                "avg_launch_us": round(stage_ms / max(launches, 1) * 1e3, 2),
+                "algo_flops_per_launch": round(flops / max(launches, 1)),
+                "algo_bytes_per_launch": round(algo_b / max(launches, 1))}
     else:
         roof = {"bound": "hbm", "achieved": None, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": None, "traffic": None, "kernel": dominant, "launches": launches}
@@ -219,6 +261,14 @@ def main():
         sweep.append({"tau": lv["tau"], "reuse": round(lv["reuse"], 4),
                       "frames_per_s": round(fps, 1), "speedup_vs_dense": round(fps / dense_fps, 3),
                       "ideal_speedup": round(dense / algo, 3)})
+
+    if args.copy_calibration:   # one plain copy kernel of known size for the HBM counters
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] copy calibration: 1 GiB device-to-device copy done")
+        del src, dst
 
     cpu = None
     if not args.no_cpu:

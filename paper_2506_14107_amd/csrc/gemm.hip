@@ -23,6 +23,7 @@
 //
 // fp32 path: a plain LDS-tiled VALU GEMM (small fp32 models).
 #include <cstdlib>
+#include <type_traits>
 
 #include "dv_internal.h"
 
@@ -104,6 +105,90 @@ __device__ inline void epi_store4(const GemmArgs& a, int row, int trow, int col,
     } else {  // Fc2
         v += *(const f32x4*)(a.resid + (size_t)row * Nout + col);
         *(f32x4*)((float*)a.out + (size_t)trow * Nout + col) = v;
+    }
+}
+
+__device__ inline void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Epilogue of one wavefront's (TI*32) x (TJ*32) sub-tile, staged through a wave-private LDS
+// slab so that global traffic is row-contiguous: for each 32-row slab the accumulators (lane l
+// holds row l%32, columns (r/4)*8 + (l/32)*4 + r%4 of each 32-column tile) are written to LDS,
+// then read back row-major -- each lane owns 4 fixed columns, so the bias is loaded once, and a
+// wavefront instruction covers 64/(TJ*8) whole row segments.  Residual rows and row indices are
+// all requested before any is used.  The caller has finished with the LDS ring.
+template <Epi E, int TI, int TJ>
+__device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], float* slab, int row0,
+                                    int col0, int M, int lane) {
+    constexpr int WN = TJ * 32;          // columns of the sub-tile
+    constexpr int LDW = WN + 4;          // padded slab row (floats)
+    constexpr int CPRW = WN / 4;         // 16-byte chunks per row
+    constexpr int RPI = 64 / CPRW;       // rows per wavefront instruction
+    constexpr int NQ = 32 / RPI;         // instructions per 32-row slab
+    const int lr = lane & 31, hl = lane >> 5;
+    const int c = lane % CPRW, rsub = lane / CPRW;
+    const int col = col0 + c * 4;
+    const size_t Nout = a.Nout;
+    const f32x4 bias = *(const f32x4*)(a.bias + col);
+#pragma unroll
+    for (int i = 0; i < TI; ++i) {
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                f32x4 v = {acc[i][j][g * 4 + 0], acc[i][j][g * 4 + 1], acc[i][j][g * 4 + 2],
+                           acc[i][j][g * 4 + 3]};
+                *(f32x4*)(slab + lr * LDW + j * 32 + g * 8 + hl * 4) = v;
+            }
+        wave_lds_sync();
+        int rows[NQ], trows[NQ];
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            rows[q] = row0 + i * 32 + q * RPI + rsub;
+            trows[q] = rows[q];
+        }
+        if constexpr (E == Epi::OProj || E == Epi::Fc2) {
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) trows[q] = rows[q] < M ? a.idx[rows[q]] : 0;
+        }
+        if constexpr (E == Epi::Patch) {
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) trows[q] = (rows[q] / a.P) * a.N + 1 + rows[q] % a.P;
+        }
+        f32x4 extra[NQ];
+        if constexpr (E == Epi::OProj || E == Epi::Fc2 || E == Epi::Patch) {
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                if (rows[q] < M) {
+                    if constexpr (E == Epi::OProj)
+                        extra[q] = *(const f32x4*)(a.resid + (size_t)trows[q] * Nout + col);
+                    else if constexpr (E == Epi::Fc2)
+                        extra[q] = *(const f32x4*)(a.resid + (size_t)rows[q] * Nout + col);
+                    else
+                        extra[q] = *(const f32x4*)(a.pos + (size_t)(1 + rows[q] % a.P) * Nout + col);
+                }
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int r = q * RPI + rsub;
+            if (rows[q] >= M) continue;
+            f32x4 v = *(const f32x4*)(slab + r * LDW + c * 4) + bias;
+            if constexpr (E == Epi::Qkv) {
+                *(u32x2*)((uint16_t*)a.out + (size_t)rows[q] * Nout + col) = pack_bf16x4(v);
+            } else if constexpr (E == Epi::Fc1) {
+                f32x4 gl = {gelu_as(v[0]), gelu_as(v[1]), gelu_as(v[2]), gelu_as(v[3])};
+                *(u32x2*)((uint16_t*)a.out + (size_t)rows[q] * Nout + col) = pack_bf16x4(gl);
+            } else if constexpr (E == Epi::OProj) {
+                *(f32x4*)((float*)a.out + (size_t)rows[q] * Nout + col) = v + extra[q];
+            } else {   // Fc2 and Patch: the output lives in a token row
+                *(f32x4*)((float*)a.out + (size_t)trows[q] * Nout + col) = v + extra[q];
+            }
+        }
+        wave_lds_sync();   // the slab is rewritten by the next 32-row slab
     }
 }
 
@@ -240,23 +325,195 @@ void gemm_bf16_k(GemmArgs a) {
         }
     }
 
+    __syncthreads();   // every wave is done with the LDS ring
+    epilogue_lds<E, TI, TJ>(a, acc, (float*)smem + wave * (32 * (TJ * 32 + 4)), tm * BM + wm * WM,
+                            tn * BN + wn * WN, M, lane);
+}
+
+// ---------------- bf16 MFMA GEMM, fully pipelined 256 x 256 variant ----------------------------
+// One wavefront per SIMD (128 x 128 per wave, 256 accumulator registers), so every latency is
+// hidden inside the wave: the DMA ring keeps S-1 k-slices in flight and the MFMA fragments are
+// always one k-step ahead, across stage boundaries too.  The barrier of stage kt+1 sits just
+// before the first fragment loads of stage kt+1; the DMA of a new stage is issued right after
+// it, into the slot every wave finished reading before that barrier.
+template <Epi E, int BKD, int S>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemm_bf16_pipe_k(GemmArgs a) {
+    constexpr int BM = 256, BN = 256;
+    constexpr int WM = 128, WN = 128, TI = 4, TJ = 4;
+    constexpr int CPR = BKD / 8;
+    constexpr int RPI = 64 / CPR;
+    constexpr int SH = (CPR == 8) ? 1 : 2;
+    constexpr int LA = BM / RPI / 4, LB = BN / RPI / 4;
+    constexpr int L = LA + LB;
+    constexpr int STAGE = (BM + BN) * BKD;
+    constexpr int KS = BKD / 16;
+    static_assert(KS % 2 == 0, "fragment double buffer assumes an even number of k-steps");
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    uint16_t* sm = (uint16_t*)smem;
+
+    const int M = a.Mdev ? *a.Mdev : a.Mconst;
+    const int tilesN = a.Nout / BN;
+    const int mt = (M + BM - 1) / BM;
+    const int active = mt * tilesN;
+    const int bid = blockIdx.x;
+    if (bid >= active) return;
+    int lid = bid;
+    const int per = active / 8;
+    if (bid < per * 8) lid = (bid % 8) * per + bid / 8;
+    constexpr int GM = 8;
+    const int group = lid / (GM * tilesN);
+    const int first_m = group * GM;
+    const int gsize = min(mt - first_m, GM);
+    const int w_in = lid - group * GM * tilesN;
+    const int tm = first_m + w_in % gsize;
+    const int tn = w_in / gsize;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lr = lane & 31, hl = lane >> 5;
+    const int K = a.K;
+
+    const int lrow = lane / CPR, lslot = lane % CPR;
+    const uint16_t* srcA[LA];
+    const uint16_t* srcB[LB];
+#pragma unroll
+    for (int t = 0; t < LA; ++t) {
+        const int r = (wave * LA + t) * RPI + lrow;
+        const int c = lslot ^ ((r >> SH) & (CPR - 1));
+        srcA[t] = (const uint16_t*)a.A + (size_t)(tm * BM + r) * K + c * 8;
+    }
+#pragma unroll
+    for (int t = 0; t < LB; ++t) {
+        const int r = (wave * LB + t) * RPI + lrow;
+        const int c = lslot ^ ((r >> SH) & (CPR - 1));
+        srcB[t] = (const uint16_t*)a.W + (size_t)(tn * BN + r) * K + c * 8;
+    }
+    auto issue = [&](int kt) {
+        uint16_t* st = sm + (kt % S) * STAGE;
+#pragma unroll
+        for (int t = 0; t < LA; ++t)
+            __builtin_amdgcn_global_load_lds((const void*)(srcA[t] + kt * BKD),
+                (__attribute__((address_space(3))) void*)(st + (wave * LA + t) * RPI * BKD), 16, 0, 0);
+#pragma unroll
+        for (int t = 0; t < LB; ++t)
+            __builtin_amdgcn_global_load_lds((const void*)(srcB[t] + kt * BKD),
+                (__attribute__((address_space(3))) void*)(st + BM * BKD + (wave * LB + t) * RPI * BKD), 16, 0, 0);
+    };
+    // per-lane LDS element offsets of the fragments (row part; the chunk is XORed per k-step)
+    int offA[TI], offB[TJ], swA[TI], swB[TJ];
 #pragma unroll
     for (int i = 0; i < TI; ++i) {
-        const int row = tm * BM + wm * WM + i * 32 + lr;
-        if (row >= M) continue;
-        int trow = row;
-        if constexpr (E == Epi::OProj || E == Epi::Fc2) trow = a.idx[row];
-        if constexpr (E == Epi::Patch) trow = (row / a.P) * a.N + 1 + row % a.P;
+        const int r = wm * WM + i * 32 + lr;
+        offA[i] = r * BKD;
+        swA[i] = (r >> SH) & (CPR - 1);
+    }
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+        const int r = wn * WN + j * 32 + lr;
+        offB[j] = BM * BKD + r * BKD;
+        swB[j] = (r >> SH) & (CPR - 1);
+    }
+    auto frag = [&](int kt, int ks, bf16x8 (&xa)[TI], bf16x8 (&xb)[TJ]) {
+        const uint16_t* st = sm + (kt % S) * STAGE;
+        const int c = ks * 2 + hl;
+#pragma unroll
+        for (int i = 0; i < TI; ++i) xa[i] = *(const bf16x8*)(st + offA[i] + (c ^ swA[i]) * 8);
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) xb[j] = *(const bf16x8*)(st + offB[j] + (c ^ swB[j]) * 8);
+    };
+
+    f32x16 acc[TI][TJ];
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int col = tn * BN + wn * WN + j * 32 + g * 8 + hl * 4;
-                f32x4 v = {acc[i][j][g * 4 + 0], acc[i][j][g * 4 + 1], acc[i][j][g * 4 + 2],
-                           acc[i][j][g * 4 + 3]};
-                epi_store4<E>(a, row, trow, col, v);
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    const int nk = K / BKD;
+#pragma unroll
+    for (int p = 0; p < S - 1; ++p)
+        if (p < nk) issue(p);
+    wait_vm<0>();
+    bare_barrier();
+    bf16x8 fa[2][TI], fb[2][TJ];
+    frag(0, 0, fa[0], fb[0]);
+    // one k-slice: MFMAs on the fragments in hand while the next fragments are read.  NEXT:
+    // whether the following slice's first fragments are read at the end (after its barrier);
+    // WAITN: vmcnt that guarantees the following slice has landed.  The three uses below are
+    // separate instantiations, so the steady-state loop body has no branch.
+    auto mfmas = [&](int cur, int from, int to) {
+#pragma unroll
+        for (int q = from; q < to; ++q) {
+            const int i = q / TJ, j = q % TJ;
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i], acc[i][j],
+                                                                0, 0, 0);
+        }
+    };
+    // Interleave for one k-step (in-order issue: a read placed after a run of MFMAs would wait
+    // for the MFMA pipe): reads of the next fragments go between the MFMAs of this k-step.
+    auto slice = [&](int kt, auto next, auto waitn) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int cur = ks & 1;
+            if (ks + 1 < KS) {
+                frag(kt, ks + 1, fa[cur ^ 1], fb[cur ^ 1]);
+                mfmas(cur, 0, TI * TJ);
+#pragma unroll
+                for (int q = 0; q < TI + TJ; ++q) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, TI * TJ - (TI + TJ), 0);
+                __builtin_amdgcn_sched_barrier(0);
+            } else if constexpr (decltype(next)::value) {
+                constexpr int PRE = TI * TJ - (TI + TJ) - 4;   // MFMAs before the barrier
+                mfmas(cur, 0, PRE);
+                __builtin_amdgcn_sched_barrier(0);
+                wait_vm<decltype(waitn)::value>();
+                bare_barrier();
+                frag(kt + 1, 0, fa[cur ^ 1], fb[cur ^ 1]);
+                mfmas(cur, PRE, TI * TJ);
+#pragma unroll
+                for (int q = 0; q < TI + TJ; ++q) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, TI * TJ - PRE - (TI + TJ), 0);
+                __builtin_amdgcn_sched_barrier(0);
+            } else {
+                mfmas(cur, 0, TI * TJ);
             }
+        }
+    };
+    using T_ = std::integral_constant<bool, true>;
+    using F_ = std::integral_constant<bool, false>;
+    int kt = 0;
+    for (; kt + S - 1 < nk; ++kt) {   // steady state: a new slice enters the ring every step
+        issue(kt + S - 1);            // slot of slice kt-1: every wave read it before a barrier
+        slice(kt, T_(), std::integral_constant<int, (S - 2) * L>());
     }
+    for (; kt + 1 < nk; ++kt) slice(kt, T_(), std::integral_constant<int, 0>());   // drain
+    slice(kt, F_(), std::integral_constant<int, 0>());                              // last slice
+
+    __syncthreads();   // every wave is done with the LDS ring
+    epilogue_lds<E, TI, TJ>(a, acc, (float*)smem + wave * (32 * (TJ * 32 + 4)), tm * BM + wm * WM,
+                            tn * BN + wn * WN, M, lane);
+}
+
+template <Epi E, int BKD, int S>
+void launch_pipe(const GemmArgs& a, hipStream_t s) {
+    static bool raised = false;
+    constexpr size_t lds = (size_t)S * 512 * BKD * 2;
+    static_assert(lds <= 160 * 1024, "LDS ring exceeds 160 KiB");
+    if (!raised) {
+        (void)hipFuncSetAttribute((const void*)gemm_bf16_pipe_k<E, BKD, S>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        raised = true;
+    }
+    const int grid = ((a.Mmax + 255) / 256) * (a.Nout / 256);
+    hipLaunchKernelGGL((gemm_bf16_pipe_k<E, BKD, S>), dim3(grid), dim3(256), lds, s, a);
 }
 
 // ---------------- fp32 VALU GEMM: block tile 64 x 64, k-step 16, 4 x 4 outputs per thread ---
@@ -353,6 +610,14 @@ void launch_one(bool bf16, const GemmArgs& a, hipStream_t s) {
             break;
         case 3:
             launch_cfg<E, 128, 128, 64, 3, 2>(a, s);
+            break;
+        case 4:
+            if (a.Nout % 256 == 0 && E != Epi::Patch) launch_pipe<E, 32, 4>(a, s);
+            else launch_cfg<E, 256, 128, 32, 3, 2>(a, s);
+            break;
+        case 5:
+            if (a.Nout % 256 == 0 && E != Epi::Patch) launch_pipe<E, 64, 2>(a, s);
+            else launch_cfg<E, 256, 128, 32, 3, 2>(a, s);
             break;
         default:  // 256 x 128 tiles, 3-stage ring of 32-wide k-slices: two blocks per CU
             launch_cfg<E, 256, 128, 32, 3, 2>(a, s);
