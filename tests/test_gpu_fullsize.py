@@ -1,0 +1,60 @@
+"""Parity at the workloads' full sizes, in the batching the bench and the workloads use.
+
+The GPU encodes whole batches (ViT-B/16: 64 frames; ViT-L/14: 256 frames, the bench's
+configuration; ViT-L/14 at 336 px: 2 batches of 128 frames across a scene cut; ViT-H/14-class:
+a 512-frame batch plus a ragged 8-frame batch).  Sampled whole groups are recomputed by the CPU
+oracle replaying the GPU's reuse maps (teacher-forced decisions, then embeddings and the full
+last-layer token buffers to the bf16 bar: min cosine >= 0.999, per-frame relative error <= 2e-2).
+"""
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+from .gpu_util import check_close, dev, encoder, host, mask_parity, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+# workload, frames encoded, gate threshold, sampled group starts
+CASES = [
+    ("vit_b16", 64, 0.9, [0, 28]),
+    ("vit_l14", 256, 0.906, [0, 128]),
+    ("vit_l14_336", 256, 0.9, [56, 176]),      # groups holding the scene cuts at frames 60, 180
+    ("vit_h14", 520, 0.9, [0, 512]),           # 512 is the ragged second batch
+]
+
+
+@pytest.mark.parametrize("name,n,tau,starts", CASES, ids=[c[0] for c in CASES])
+def test_full_size_parity(name, n, tau, starts):
+    torch = require_gpu()
+    w = synth.get_config(name)
+    m, G = w.model, w.group_size
+    t0 = time.time()
+    blob = synth.make_blob(m, w.weight_seed)
+    fr = synth.render_frames(w.video, m.image_size, 0, n)
+    print(f"[{name}] inputs {time.time() - t0:.1f}s", flush=True)
+    enc = encoder(m, blob, w.batch_frames)
+    x = dev(fr)
+    emb, masks, toks = enc.encode(x, G, float(np.float32(tau)), want_tokens=True)
+    torch.cuda.synchronize()
+    mg = host(masks)
+    rho = oracle.reuse_rate(mg, G)
+    print(f"[{name}] GPU reuse {rho:.3f}", flush=True)
+    assert 0.05 < rho < 0.99, f"threshold gives degenerate reuse {rho}"
+    assert np.all(mg[:, 1:] >= mg[:, :-1]), "gate-mode reuse must be monotone over layers"
+    e_all = host(emb)
+    for g0 in starts:
+        sl = slice(g0, g0 + G)
+        t1 = time.time()
+        r = oracle.encode(fr[sl], blob, m.as_dict(), G, masks=mg[sl])
+        bad, inside = mask_parity(mg[sl], r["cos"], float(np.float32(tau)))
+        c_e, r_e = check_close(e_all[sl], r["emb"], "bf16", f"{name} group {g0} embeddings")
+        c_t, r_t = check_close(host(toks[sl]), r["tokens"], "bf16", f"{name} group {g0} tokens")
+        print(f"[{name}] group {g0}: oracle {time.time() - t1:.1f}s, decisions off {bad}, "
+              f"in band {inside:.2%}, emb cos {c_e:.5f} rel {r_e:.2e}, tok cos {c_t:.5f} "
+              f"rel {r_t:.2e}", flush=True)
+        assert bad == 0, f"{bad} decisions differ outside the 1e-3 band"
+    enc.close()
