@@ -336,11 +336,10 @@ void gemm_bf16_k(GemmArgs a) {
 // always one k-step ahead, across stage boundaries too.  The barrier of stage kt+1 sits just
 // before the first fragment loads of stage kt+1; the DMA of a new stage is issued right after
 // it, into the slot every wave finished reading before that barrier.
-template <Epi E, int BKD, int S>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+template <Epi E, int BM, int BN, int BKD, int S, int WPE>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void gemm_bf16_pipe_k(GemmArgs a) {
-    constexpr int BM = 256, BN = 256;
-    constexpr int WM = 128, WN = 128, TI = 4, TJ = 4;
+    constexpr int WM = BM / 2, WN = BN / 2, TI = WM / 32, TJ = WN / 32;
     constexpr int CPR = BKD / 8;
     constexpr int RPI = 64 / CPR;
     constexpr int SH = (CPR == 8) ? 1 : 2;
@@ -453,37 +452,42 @@ void gemm_bf16_pipe_k(GemmArgs a) {
     };
     // Interleave for one k-step (in-order issue: a read placed after a run of MFMAs would wait
     // for the MFMA pipe): reads of the next fragments go between the MFMAs of this k-step.
+    constexpr int NM = TI * TJ, NR = TI + TJ;      // MFMAs and fragment reads per k-step
+    constexpr int PAIRS = NR < NM ? NR : NM;
+    constexpr int PRE = NM / 4;                    // MFMAs issued before a stage barrier
+    constexpr int PAIRS2 = NR < NM - PRE ? NR : NM - PRE;
     auto slice = [&](int kt, auto next, auto waitn) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             const int cur = ks & 1;
             if (ks + 1 < KS) {
                 frag(kt, ks + 1, fa[cur ^ 1], fb[cur ^ 1]);
-                mfmas(cur, 0, TI * TJ);
+                mfmas(cur, 0, NM);
 #pragma unroll
-                for (int q = 0; q < TI + TJ; ++q) {
+                for (int q = 0; q < PAIRS; ++q) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
                     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
                 }
-                __builtin_amdgcn_sched_group_barrier(0x008, TI * TJ - (TI + TJ), 0);
+                if constexpr (NR > PAIRS) __builtin_amdgcn_sched_group_barrier(0x100, NR - PAIRS, 0);
+                if constexpr (NM > PAIRS) __builtin_amdgcn_sched_group_barrier(0x008, NM - PAIRS, 0);
                 __builtin_amdgcn_sched_barrier(0);
             } else if constexpr (decltype(next)::value) {
-                constexpr int PRE = TI * TJ - (TI + TJ) - 4;   // MFMAs before the barrier
                 mfmas(cur, 0, PRE);
                 __builtin_amdgcn_sched_barrier(0);
                 wait_vm<decltype(waitn)::value>();
                 bare_barrier();
                 frag(kt + 1, 0, fa[cur ^ 1], fb[cur ^ 1]);
-                mfmas(cur, PRE, TI * TJ);
+                mfmas(cur, PRE, NM);
 #pragma unroll
-                for (int q = 0; q < TI + TJ; ++q) {
+                for (int q = 0; q < PAIRS2; ++q) {
                     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                 }
-                __builtin_amdgcn_sched_group_barrier(0x008, TI * TJ - PRE - (TI + TJ), 0);
+                if constexpr (NR > PAIRS2) __builtin_amdgcn_sched_group_barrier(0x100, NR - PAIRS2, 0);
+                if constexpr (NM - PRE > PAIRS2) __builtin_amdgcn_sched_group_barrier(0x008, NM - PRE - PAIRS2, 0);
                 __builtin_amdgcn_sched_barrier(0);
             } else {
-                mfmas(cur, 0, TI * TJ);
+                mfmas(cur, 0, NM);
             }
         }
     };
@@ -502,18 +506,18 @@ void gemm_bf16_pipe_k(GemmArgs a) {
                             tn * BN + wn * WN, M, lane);
 }
 
-template <Epi E, int BKD, int S>
+template <Epi E, int BM, int BN, int BKD, int S, int WPE>
 void launch_pipe(const GemmArgs& a, hipStream_t s) {
     static bool raised = false;
-    constexpr size_t lds = (size_t)S * 512 * BKD * 2;
+    constexpr size_t lds = (size_t)S * (BM + BN) * BKD * 2;
     static_assert(lds <= 160 * 1024, "LDS ring exceeds 160 KiB");
     if (!raised) {
-        (void)hipFuncSetAttribute((const void*)gemm_bf16_pipe_k<E, BKD, S>,
+        (void)hipFuncSetAttribute((const void*)gemm_bf16_pipe_k<E, BM, BN, BKD, S, WPE>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         raised = true;
     }
-    const int grid = ((a.Mmax + 255) / 256) * (a.Nout / 256);
-    hipLaunchKernelGGL((gemm_bf16_pipe_k<E, BKD, S>), dim3(grid), dim3(256), lds, s, a);
+    const int grid = ((a.Mmax + BM - 1) / BM) * (a.Nout / BN);
+    hipLaunchKernelGGL((gemm_bf16_pipe_k<E, BM, BN, BKD, S, WPE>), dim3(grid), dim3(256), lds, s, a);
 }
 
 // ---------------- fp32 VALU GEMM: block tile 64 x 64, k-step 16, 4 x 4 outputs per thread ---
@@ -597,30 +601,17 @@ void launch_one(bool bf16, const GemmArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(gemm_f32_k<E>, dim3(grid), dim3(256), 0, s, a);
         return;
     }
-    const bool wide = E != Epi::Patch && a.Nout % 256 == 0 && a.Nout / 256 >= 8;
-    (void)wide;
+    const bool wide = E != Epi::Patch && a.Nout % 256 == 0;
     switch (gemm_cfg()) {
-        case 1:
-            if (wide) launch_cfg<E, 256, 256, 32, 4, 1>(a, s);
-            else launch_cfg<E, 256, 128, 64, 3, 1>(a, s);
-            break;
-        case 2:
-            if (wide) launch_cfg<E, 256, 256, 64, 2, 1>(a, s);
-            else launch_cfg<E, 256, 128, 32, 3, 2>(a, s);
-            break;
-        case 3:
-            launch_cfg<E, 128, 128, 64, 3, 2>(a, s);
-            break;
-        case 4:
-            if (a.Nout % 256 == 0 && E != Epi::Patch) launch_pipe<E, 32, 4>(a, s);
-            else launch_cfg<E, 256, 128, 32, 3, 2>(a, s);
-            break;
-        case 5:
-            if (a.Nout % 256 == 0 && E != Epi::Patch) launch_pipe<E, 64, 2>(a, s);
-            else launch_cfg<E, 256, 128, 32, 3, 2>(a, s);
-            break;
-        default:  // 256 x 128 tiles, 3-stage ring of 32-wide k-slices: two blocks per CU
+        case 1:   // the simpler loop, same tiles
             launch_cfg<E, 256, 128, 32, 3, 2>(a, s);
+            break;
+        case 2:   // 256 x 256 tiles, one wave per SIMD
+            if (wide) launch_pipe<E, 256, 256, 32, 4, 1>(a, s);
+            else launch_pipe<E, 256, 128, 32, 3, 2>(a, s);
+            break;
+        default:  // 256 x 128 tiles, 3-stage ring of 32-wide k-slices, two blocks per CU
+            launch_pipe<E, 256, 128, 32, 3, 2>(a, s);
             break;
     }
 }
