@@ -118,8 +118,9 @@ __device__ inline void wave_lds_sync() {
 // slab so that global traffic is row-contiguous: for each 32-row slab the accumulators (lane l
 // holds row l%32, columns (r/4)*8 + (l/32)*4 + r%4 of each 32-column tile) are written to LDS,
 // then read back row-major -- each lane owns 4 fixed columns, so the bias is loaded once, and a
-// wavefront instruction covers 64/(TJ*8) whole row segments.  Residual rows and row indices are
-// all requested before any is used.  The caller has finished with the LDS ring.
+// wavefront instruction covers 64/(TJ*8) whole row segments.  Row indices of every slab are
+// requested up front and the residual (or position) rows of slab i+1 are in flight while slab
+// i is combined and stored.  The caller has finished with the LDS ring.
 template <Epi E, int TI, int TJ>
 __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], float* slab, int row0,
                                     int col0, int M, int lane) {
@@ -128,13 +129,44 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
     constexpr int CPRW = WN / 4;         // 16-byte chunks per row
     constexpr int RPI = 64 / CPRW;       // rows per wavefront instruction
     constexpr int NQ = 32 / RPI;         // instructions per 32-row slab
+    constexpr bool LOADS = E == Epi::OProj || E == Epi::Fc2 || E == Epi::Patch;
     const int lr = lane & 31, hl = lane >> 5;
     const int c = lane % CPRW, rsub = lane / CPRW;
     const int col = col0 + c * 4;
     const size_t Nout = a.Nout;
     const f32x4 bias = *(const f32x4*)(a.bias + col);
+
+    auto row_of = [&](int i, int q) { return row0 + i * 32 + q * RPI + rsub; };
+    // residual (or position) rows and output token rows of slab i; one slab ahead
+    f32x4 extra[2][NQ];
+    int trow[2][NQ];
+    auto fetch = [&](int i, f32x4 (&dst)[NQ], int (&tr)[NQ]) {
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int row = row_of(i, q);
+            const int r = row < M ? row : row0;            // a valid row for the tile tail
+            if constexpr (E == Epi::OProj || E == Epi::Fc2) tr[q] = a.idx[r];
+            else if constexpr (E == Epi::Patch) tr[q] = (r / a.P) * a.N + 1 + r % a.P;
+            else tr[q] = r;
+        }
+        if constexpr (LOADS) {
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                const int row = row_of(i, q);
+                const int r = row < M ? row : row0;
+                if constexpr (E == Epi::OProj)
+                    dst[q] = *(const f32x4*)(a.resid + (size_t)tr[q] * Nout + col);
+                else if constexpr (E == Epi::Fc2)
+                    dst[q] = *(const f32x4*)(a.resid + (size_t)r * Nout + col);
+                else
+                    dst[q] = *(const f32x4*)(a.pos + (size_t)(1 + r % a.P) * Nout + col);
+            }
+        }
+    };
+    fetch(0, extra[0], trow[0]);
 #pragma unroll
     for (int i = 0; i < TI; ++i) {
+        if (i + 1 < TI) fetch(i + 1, extra[(i + 1) & 1], trow[(i + 1) & 1]);
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
 #pragma unroll
@@ -144,48 +176,21 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
                 *(f32x4*)(slab + lr * LDW + j * 32 + g * 8 + hl * 4) = v;
             }
         wave_lds_sync();
-        int rows[NQ], trows[NQ];
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            rows[q] = row0 + i * 32 + q * RPI + rsub;
-            trows[q] = rows[q];
-        }
-        if constexpr (E == Epi::OProj || E == Epi::Fc2) {
-#pragma unroll
-            for (int q = 0; q < NQ; ++q) trows[q] = rows[q] < M ? a.idx[rows[q]] : 0;
-        }
-        if constexpr (E == Epi::Patch) {
-#pragma unroll
-            for (int q = 0; q < NQ; ++q) trows[q] = (rows[q] / a.P) * a.N + 1 + rows[q] % a.P;
-        }
-        f32x4 extra[NQ];
-        if constexpr (E == Epi::OProj || E == Epi::Fc2 || E == Epi::Patch) {
-#pragma unroll
-            for (int q = 0; q < NQ; ++q) {
-                if (rows[q] < M) {
-                    if constexpr (E == Epi::OProj)
-                        extra[q] = *(const f32x4*)(a.resid + (size_t)trows[q] * Nout + col);
-                    else if constexpr (E == Epi::Fc2)
-                        extra[q] = *(const f32x4*)(a.resid + (size_t)rows[q] * Nout + col);
-                    else
-                        extra[q] = *(const f32x4*)(a.pos + (size_t)(1 + rows[q] % a.P) * Nout + col);
-                }
-            }
-        }
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int r = q * RPI + rsub;
-            if (rows[q] >= M) continue;
+            const int row = row_of(i, q);
+            if (row >= M) continue;
             f32x4 v = *(const f32x4*)(slab + r * LDW + c * 4) + bias;
             if constexpr (E == Epi::Qkv) {
-                *(u32x2*)((uint16_t*)a.out + (size_t)rows[q] * Nout + col) = pack_bf16x4(v);
+                *(u32x2*)((uint16_t*)a.out + (size_t)row * Nout + col) = pack_bf16x4(v);
             } else if constexpr (E == Epi::Fc1) {
                 f32x4 gl = {gelu_as(v[0]), gelu_as(v[1]), gelu_as(v[2]), gelu_as(v[3])};
-                *(u32x2*)((uint16_t*)a.out + (size_t)rows[q] * Nout + col) = pack_bf16x4(gl);
+                *(u32x2*)((uint16_t*)a.out + (size_t)row * Nout + col) = pack_bf16x4(gl);
             } else if constexpr (E == Epi::OProj) {
-                *(f32x4*)((float*)a.out + (size_t)rows[q] * Nout + col) = v + extra[q];
+                *(f32x4*)((float*)a.out + (size_t)row * Nout + col) = v + extra[i & 1][q];
             } else {   // Fc2 and Patch: the output lives in a token row
-                *(f32x4*)((float*)a.out + (size_t)trows[q] * Nout + col) = v + extra[q];
+                *(f32x4*)((float*)a.out + (size_t)trow[i & 1][q] * Nout + col) = v + extra[i & 1][q];
             }
         }
         wave_lds_sync();   // the slab is rewritten by the next 32-row slab
