@@ -164,7 +164,7 @@ int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size,
 #define DV_STAGE_PATCH 0
 #define DV_STAGE_GATE 1
 #define DV_STAGE_COMPACT 2
-#define DV_STAGE_LN1 3
+#define DV_STAGE_LN1 3   /* LN1 is computed by the gate pass: no launches of its own */
 #define DV_STAGE_QKV 4
 #define DV_STAGE_ATTN 5
 #define DV_STAGE_OPROJ 6

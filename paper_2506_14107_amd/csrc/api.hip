@@ -239,37 +239,32 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         const LayerW& w = h->layers[l];
         uint8_t* cur = h->mask[l & 1];
         uint8_t* prev = l > 0 ? h->mask[(l - 1) & 1] : nullptr;
-        if (dense) {
-            if (om) launch_zero_mask_layer(om, F, L, N, l, s);
-        } else {
-            {
-                Scope sc(h, DV_STAGE_GATE, s);
-                GateArgs ga{};
-                ga.x = h->x;
-                ga.F = F;
-                ga.N = N;
-                ga.D = D;
-                ga.G = G;
-                ga.L = L;
-                ga.layer = l;
-                ga.mode = mode;
-                ga.tau = tau;
-                ga.prev = (mode == GATE_COS) ? prev : nullptr;
-                ga.inj = inj;
-                ga.cur = cur;
-                ga.out_masks = om;
-                ga.cnt = h->cnt;
-                launch_gate(ga, s);
-            }
-            {
-                Scope sc(h, DV_STAGE_COMPACT, s);
-                launch_scan(h->cnt, F, h->qoff, h->M, s);
-                launch_compact(cur, h->qoff, F, N, G, h->idx, h->pos_, nullptr, s);
-            }
+        {   // reuse gate + LN1 of every recomputed token (reuse off: LN1 of every token)
+            Scope sc(h, DV_STAGE_GATE, s);
+            GateArgs ga{};
+            ga.x = h->x;
+            ga.F = F;
+            ga.N = N;
+            ga.D = D;
+            ga.G = G;
+            ga.L = L;
+            ga.layer = l;
+            ga.mode = mode;
+            ga.tau = tau;
+            ga.prev = (mode == GATE_COS) ? prev : nullptr;
+            ga.inj = inj;
+            ga.cur = dense ? nullptr : cur;
+            ga.out_masks = om;
+            ga.cnt = dense ? nullptr : h->cnt;
+            ga.ln_g = w.ln1_g;
+            ga.ln_b = w.ln1_b;
+            ga.ln_out = h->A;   // token-indexed LN1 rows; the QKV GEMM gathers them through idx
+            launch_gate(bf, ga, s);
         }
-        {
-            Scope sc(h, DV_STAGE_LN1, s);
-            launch_ln_rows(bf, h->x, idx, Mdev, T, D, w.ln1_g, w.ln1_b, h->A, s);
+        if (!dense) {
+            Scope sc(h, DV_STAGE_COMPACT, s);
+            launch_scan(h->cnt, gate_chunks(N), F, h->qoff, h->M, s);
+            launch_compact(cur, h->qoff, F, N, G, h->idx, h->pos_, nullptr, s);
         }
         GemmArgs g{};
         g.Mdev = Mdev;
@@ -279,6 +274,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         {
             Scope sc(h, DV_STAGE_QKV, s);
             g.A = h->A;
+            g.a_idx = idx;   // packed row m is token row idx[m] of the LN1 buffer
             g.W = w.W_qkv;
             g.bias = w.b_qkv;
             g.K = D;
@@ -287,6 +283,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             launch_gemm(Epi::Qkv, bf, g, s);
         }
         {
+            g.a_idx = nullptr;
             Scope sc(h, DV_STAGE_ATTN, s);
             AttnArgs at{};
             at.qkv = h->qkv;
@@ -550,7 +547,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
         sz(T * 4);
         sz((d.B + 1) * 4);
     }
-    sz(d.B * 4);
+    sz((size_t)d.B * gate_chunks(d.N) * 4);
     sz(4 * 4);
     {
         hipError_t e = hipMalloc(&h->ws, need);
@@ -579,7 +576,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     h->idx_id = carve<int>(p, T);
     h->pos_id = carve<int>(p, T);
     h->qoff_id = carve<int>(p, d.B + 1);
-    h->cnt = carve<int>(p, d.B);
+    h->cnt = carve<int>(p, (size_t)d.B * gate_chunks(d.N));
     h->M = carve<int>(p, 4);
     *out = h;
     return DV_OK;
@@ -634,7 +631,7 @@ int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size,
     if ((long long)n_frames * n_tokens > (1ll << 30)) return fail(DV_EINVAL, "too many tokens");
     // per-frame counts land in qoff[0..n) and are turned into the prefix in place by one block
     launch_count(masks, n_frames, n_tokens, group_size, qoff, stream);
-    launch_scan(qoff, n_frames, qoff, count, stream);
+    launch_scan(qoff, 1, n_frames, qoff, count, stream);
     launch_compact(masks, qoff, n_frames, n_tokens, group_size, idx, pos, nullptr, stream);
     HIP_TRY(hipGetLastError());
     return DV_OK;

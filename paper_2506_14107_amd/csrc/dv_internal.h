@@ -37,6 +37,7 @@ struct GemmArgs {
     void* out;
     const float* resid;  // OProj: x rows; Fc2: z rows
     const int* idx;      // packed row -> token row
+    const int* a_idx;    // A row gather: packed row m reads A row a_idx[m] (nullptr: row m)
     const float* pos;    // Patch: position table [N, D]
     int P, N;            // Patch: patches and tokens per frame
 };
@@ -69,14 +70,22 @@ struct GateArgs {
     float tau;
     const uint8_t* prev;  // previous layer's map (gate mode, monotone shortcut) or nullptr
     const uint8_t* inj;   // injected maps [F, L, N] (batch base) or nullptr
-    uint8_t* cur;         // [F*N] this layer's map
+    uint8_t* cur;         // [F*N] this layer's map (or nullptr)
     uint8_t* out_masks;   // [F, L, N] (batch base) or nullptr
-    int* cnt;             // [F] recomputed tokens per frame
+    int* cnt;             // [F] recomputed tokens per frame (or nullptr)
+    const float* ln_g;    // LN1 gain / shift
+    const float* ln_b;
+    void* ln_out;         // [F*N, D] elem: LN1 rows of recomputed tokens (token-indexed) or nullptr
 };
-void launch_gate(const GateArgs& a, hipStream_t s);
+// Mode GATE_NONE marks every token recomputed (reuse off) and only writes LN1 rows.
+// The gate runs in blocks of GATE_TOK tokens; counts are per block: cnt[f * gate_chunks(N) + c].
+constexpr int GATE_TOK = 16;
+inline int gate_chunks(int N) { return (N + GATE_TOK - 1) / GATE_TOK; }
+void launch_gate(bool bf16, const GateArgs& a, hipStream_t s);
 void launch_count(const uint8_t* m, int F, int N, int G, int* cnt, hipStream_t s);
-// qoff[0..F] = exclusive prefix of cnt[0..F), *M = qoff[F]
-void launch_scan(const int* cnt, int F, int* qoff, int* M, hipStream_t s);
+// qoff[0..F] = exclusive prefix of the per-frame counts (sum of `per` consecutive entries of
+// cnt per frame), *M = qoff[F]
+void launch_scan(const int* cnt, int per, int F, int* qoff, int* M, hipStream_t s);
 // idx/pos from a per-layer map and its qoff (cur == nullptr: every token recomputed, identity
 // lists, qoff_in ignored and qoff_out written)
 void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,

@@ -264,7 +264,9 @@ void gemm_bf16_k(GemmArgs a) {
     for (int t = 0; t < LA; ++t) {
         const int r = (wave * LA + t) * RPI + lrow;
         const int c = lslot ^ ((r >> SH) & (CPR - 1));
-        srcA[t] = (const uint16_t*)a.A + (size_t)(tm * BM + r) * K + c * 8;
+        const int grow = tm * BM + r;
+        const int arow = a.a_idx ? (grow < M ? a.a_idx[grow] : 0) : grow;   // gathered A rows
+        srcA[t] = (const uint16_t*)a.A + (size_t)arow * K + c * 8;
     }
 #pragma unroll
     for (int t = 0; t < LB; ++t) {
@@ -385,7 +387,9 @@ void gemm_bf16_pipe_k(GemmArgs a) {
     for (int t = 0; t < LA; ++t) {
         const int r = (wave * LA + t) * RPI + lrow;
         const int c = lslot ^ ((r >> SH) & (CPR - 1));
-        srcA[t] = (const uint16_t*)a.A + (size_t)(tm * BM + r) * K + c * 8;
+        const int grow = tm * BM + r;
+        const int arow = a.a_idx ? (grow < M ? a.a_idx[grow] : 0) : grow;   // gathered A rows
+        srcA[t] = (const uint16_t*)a.A + (size_t)arow * K + c * 8;
     }
 #pragma unroll
     for (int t = 0; t < LB; ++t) {
@@ -547,7 +551,9 @@ __global__ __launch_bounds__(256) void gemm_f32_k(GemmArgs a) {
         for (int t = 0; t < 4; ++t) {
             const int e = tid + 256 * t;
             const int rr = e / FBK, kk = e % FBK;
-            sA[kk][rr] = A[(size_t)(tm * FBM + rr) * K + k0 + kk];
+            const int grow = tm * FBM + rr;
+            const int arow = a.a_idx ? (grow < M ? a.a_idx[grow] : 0) : grow;
+            sA[kk][rr] = A[(size_t)arow * K + k0 + kk];
             sB[kk][rr] = W[(size_t)(tn * FBN + rr) * K + k0 + kk];
         }
         __syncthreads();

@@ -45,40 +45,57 @@ __global__ void cls_init_k(float* x, const float* cls, const float* pos, int F, 
     }
 }
 
-// --- reuse gate: one block per frame, one wavefront per token --------------------------------
-// cnt[f] = number of recomputed tokens of frame f.
-__global__ __launch_bounds__(1024) void gate_k(GateArgs a) {
-    const int f = blockIdx.x;
+// --- reuse gate + LN1: blocks of GATE_TOK tokens of one frame, one wavefront per token --------
+// Decides reuse for each token and, for each token that is recomputed, writes LN1 of its row
+// (already in registers for the cosine) to the token-indexed buffer `ln_out`.
+// cnt[f * chunks + block-in-frame] = number of recomputed tokens of that block.
+template <bool BF>
+__global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     const int N = a.N, D = a.D;
+    const int chunks = (N + GATE_TOK - 1) / GATE_TOK;
+    const int f = blockIdx.x / chunks, ch = blockIdx.x % chunks;
     const int r = (f / a.G) * a.G;
     const int lane = threadIdx.x & (WAVE - 1), wave = threadIdx.x / WAVE;
     const int nwaves = blockDim.x / WAVE;
+    const int nchunk = D / 4;
     __shared__ int wcount[16];
     uint8_t* om = a.out_masks ? a.out_masks + ((size_t)f * a.L + a.layer) * N : nullptr;
+    const float4* g4 = (const float4*)a.ln_g;
+    const float4* b4 = (const float4*)a.ln_b;
     int active = 0;
-    for (int i = wave; i < N; i += nwaves) {
+    const int i_end = min(N, (ch + 1) * GATE_TOK);
+    for (int i = ch * GATE_TOK + wave; i < i_end; i += nwaves) {
+        const size_t row = (size_t)f * N + i;
+        const float4* xf = (const float4*)(a.x + row * D);
         int reuse = 0;
+        bool loaded = false;
+        float4 v[MAX_CHUNKS];
         if (f != r && i != 0) {
             if (a.mode == GATE_INJECT) {
                 reuse = a.inj[((size_t)f * a.L + a.layer) * N + i] != 0;
             } else if (a.mode == GATE_ALL) {
                 reuse = 1;
             } else if (a.mode == GATE_COS) {
-                if (a.prev && a.prev[(size_t)f * N + i]) {
+                if (a.prev && a.prev[row]) {
                     // a reused token holds a copy of the reference's row: cosine exactly 1
                     reuse = a.tau <= 1.0f;
                 } else {
-                    const float4* xf = (const float4*)(a.x + ((size_t)f * N + i) * D);
                     const float4* xr = (const float4*)(a.x + ((size_t)r * N + i) * D);
                     float dot = 0.f, na = 0.f, nb = 0.f;
                     int eq = 1;
-                    for (int c = lane; c < D / 4; c += WAVE) {
-                        const float4 u = xf[c], v = xr[c];
-                        dot += u.x * v.x + u.y * v.y + u.z * v.z + u.w * v.w;
-                        na += u.x * u.x + u.y * u.y + u.z * u.z + u.w * u.w;
-                        nb += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-                        eq &= (u.x == v.x) & (u.y == v.y) & (u.z == v.z) & (u.w == v.w);
+#pragma unroll
+                    for (int k = 0; k < MAX_CHUNKS; ++k) {
+                        const int c = lane + k * WAVE;
+                        if (c < nchunk) {
+                            const float4 u = xf[c], w = xr[c];
+                            v[k] = u;
+                            dot += u.x * w.x + u.y * w.y + u.z * w.z + u.w * w.w;
+                            na += u.x * u.x + u.y * u.y + u.z * u.z + u.w * u.w;
+                            nb += w.x * w.x + w.y * w.y + w.z * w.z + w.w * w.w;
+                            eq &= (u.x == w.x) & (u.y == w.y) & (u.z == w.z) & (u.w == w.w);
+                        }
                     }
+                    loaded = true;
                     dot = wave_sum(dot);
                     na = wave_sum(na);
                     nb = wave_sum(nb);
@@ -90,18 +107,62 @@ __global__ __launch_bounds__(1024) void gate_k(GateArgs a) {
                 }
             }
         }
+        if (!reuse && a.ln_out) {   // recomputed: LN1 of the row into the token-indexed buffer
+            if (!loaded) {
+#pragma unroll
+                for (int k = 0; k < MAX_CHUNKS; ++k) {
+                    const int c = lane + k * WAVE;
+                    if (c < nchunk) v[k] = xf[c];
+                }
+            }
+            float sum = 0.f;
+#pragma unroll
+            for (int k = 0; k < MAX_CHUNKS; ++k)
+                if (lane + k * WAVE < nchunk) sum += (v[k].x + v[k].y) + (v[k].z + v[k].w);
+            const float mean = wave_sum(sum) / (float)D;
+            float sq = 0.f;
+#pragma unroll
+            for (int k = 0; k < MAX_CHUNKS; ++k) {
+                if (lane + k * WAVE < nchunk) {
+                    const float a0 = v[k].x - mean, a1 = v[k].y - mean, a2 = v[k].z - mean,
+                                a3 = v[k].w - mean;
+                    sq += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+                }
+            }
+            const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + 1e-5f);
+#pragma unroll
+            for (int k = 0; k < MAX_CHUNKS; ++k) {
+                const int c = lane + k * WAVE;
+                if (c < nchunk) {
+                    const float4 gg = g4[c], bb = b4[c];
+                    float4 o;
+                    o.x = (v[k].x - mean) * rstd * gg.x + bb.x;
+                    o.y = (v[k].y - mean) * rstd * gg.y + bb.y;
+                    o.z = (v[k].z - mean) * rstd * gg.z + bb.z;
+                    o.w = (v[k].w - mean) * rstd * gg.w + bb.w;
+                    if (BF) {
+                        uint2 pk;
+                        pk.x = (uint32_t)f32_to_bf16(o.x) | ((uint32_t)f32_to_bf16(o.y) << 16);
+                        pk.y = (uint32_t)f32_to_bf16(o.z) | ((uint32_t)f32_to_bf16(o.w) << 16);
+                        ((uint2*)a.ln_out)[row * nchunk + c] = pk;
+                    } else {
+                        ((float4*)a.ln_out)[row * nchunk + c] = o;
+                    }
+                }
+            }
+        }
         if (lane == 0) {
-            a.cur[(size_t)f * N + i] = (uint8_t)reuse;
+            if (a.cur) a.cur[row] = (uint8_t)reuse;
             if (om) om[i] = (uint8_t)reuse;
             active += !reuse;
         }
     }
     if (lane == 0) wcount[wave] = active;
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (threadIdx.x == 0 && a.cnt) {
         int s = 0;
         for (int w = 0; w < nwaves; ++w) s += wcount[w];
-        a.cnt[f] = s;
+        a.cnt[blockIdx.x] = s;
     }
 }
 
@@ -120,9 +181,10 @@ __global__ __launch_bounds__(256) void count_k(const uint8_t* m, int F, int N, i
     if (threadIdx.x == 0) cnt[f] = red[0];
 }
 
-// --- exclusive prefix over frames: qoff[f] = sum_{g<f} cnt[g], qoff[F] = *M = total ---------
-// one block; qoff may equal cnt (each thread reads its entry before any write to it)
-__global__ __launch_bounds__(1024) void scan_k(const int* cnt, int F, int* qoff, int* M) {
+// --- exclusive prefix over frames: qoff[f] = sum_{g<f} count(g), qoff[F] = *M = total ---------
+// count(g) = cnt[g*per] + ... + cnt[g*per + per-1]; one block; qoff may equal cnt when per == 1
+// (each thread reads its entries before any write to them)
+__global__ __launch_bounds__(1024) void scan_k(const int* cnt, int per, int F, int* qoff, int* M) {
     __shared__ int part[1024];
     __shared__ int carry_s;
     const int tid = threadIdx.x;
@@ -130,7 +192,9 @@ __global__ __launch_bounds__(1024) void scan_k(const int* cnt, int F, int* qoff,
     __syncthreads();
     for (int base = 0; base < F; base += 1024) {
         const int f = base + tid;
-        const int v = f < F ? cnt[f] : 0;
+        int v = 0;
+        if (f < F)
+            for (int k = 0; k < per; ++k) v += cnt[(size_t)f * per + k];
         part[tid] = v;
         __syncthreads();
         for (int o = 1; o < 1024; o <<= 1) {  // Hillis-Steele inclusive scan
@@ -326,16 +390,18 @@ void launch_cls_init(float* x, const float* cls, const float* pos, int F, int N,
                        pos, F, N, D);
 }
 
-void launch_gate(const GateArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(gate_k, dim3(a.F), dim3(1024), 0, s, a);
+void launch_gate(bool bf16, const GateArgs& a, hipStream_t s) {
+    const int grid = a.F * gate_chunks(a.N);
+    if (bf16) hipLaunchKernelGGL(gate_k<true>, dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(gate_k<false>, dim3(grid), dim3(256), 0, s, a);
 }
 
 void launch_count(const uint8_t* m, int F, int N, int G, int* cnt, hipStream_t s) {
     hipLaunchKernelGGL(count_k, dim3(F), dim3(256), 0, s, m, F, N, G, cnt);
 }
 
-void launch_scan(const int* cnt, int F, int* qoff, int* M, hipStream_t s) {
-    hipLaunchKernelGGL(scan_k, dim3(1), dim3(1024), 0, s, cnt, F, qoff, M);
+void launch_scan(const int* cnt, int per, int F, int* qoff, int* M, hipStream_t s) {
+    hipLaunchKernelGGL(scan_k, dim3(1), dim3(1024), 0, s, cnt, per, F, qoff, M);
 }
 
 void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,
@@ -346,7 +412,7 @@ void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G,
 
 void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* Mdev, int Mmax,
                     int D, const float* g, const float* b, void* dst, hipStream_t s) {
-    const int grid = grid_for((size_t)Mmax, 4, 4096);
+    const int grid = grid_for((size_t)Mmax, 4, 65536);
     if (bf16)
         hipLaunchKernelGGL(ln_rows_k<true>, dim3(grid), dim3(256), 0, s, src, gather, Mdev, Mmax,
                            D, g, b, dst);
