@@ -121,6 +121,7 @@ struct Stage {
 struct dv_handle {
     Dims d;
     int device = 0;
+    int cus = 0;   // compute units of the device
     void* wmem = nullptr;   // weights
     void* ws = nullptr;     // workspace
     size_t ws_bytes = 0;
@@ -223,6 +224,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         g.Mdev = nullptr;
         g.Mconst = F * d.P;
         g.Mmax = F * d.P;
+        g.cus = h->cus;
         g.out = h->x;
         g.pos = h->pos;
         g.P = d.P;
@@ -270,6 +272,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         g.Mdev = Mdev;
         g.Mconst = T;
         g.Mmax = T;
+        g.cus = h->cus;
         g.idx = idx;
         {
             Scope sc(h, DV_STAGE_QKV, s);
@@ -495,6 +498,9 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
         return code;
     };
     if (hipGetDevice(&h->device) != hipSuccess) return cleanup(fail(DV_EHIP, "hipGetDevice failed"));
+    if (hipDeviceGetAttribute(&h->cus, hipDeviceAttributeMultiprocessorCount, h->device) !=
+        hipSuccess)
+        h->cus = 0;   // the GEMMs then keep one tiling for all rows
     {
         hipError_t e = hipMalloc(&h->wmem, wbytes);
         if (e != hipSuccess) {

@@ -40,7 +40,25 @@ struct GemmArgs {
     const int* a_idx;    // A row gather: packed row m reads A row a_idx[m] (nullptr: row m)
     const float* pos;    // Patch: position table [N, D]
     int P, N;            // Patch: patches and tokens per frame
+    int cus;             // compute units of the device (0: no split of the last round)
+    // set by the launcher: blocks below head_grid run large tiles over the rows [0, head),
+    // the others small tiles over [head, M), head = gemm_head_rows(M, Nout, BM, BN, slots);
+    // slots = 0: one tiling for all rows
+    int slots, head_grid;
 };
+
+// Rows that large tiles take when the M rows are split between large tiles (hbm x hbn, `slots`
+// resident blocks) and small ones: the tile rows that fill whole rounds of the large-tile grid.
+// A remainder of more than a quarter of a round, or none, keeps every row in large tiles.  Each
+// output is the same dot product in the same k order in either tiling, so the split does not
+// change results.
+__host__ __device__ inline int gemm_head_rows(int M, int Nout, int hbm, int hbn, int slots) {
+    const int tn = Nout / hbn;
+    const int mt = (M + hbm - 1) / hbm;
+    const int mA = (mt * tn / slots) * slots / tn;   // whole tile rows inside the full rounds
+    if (mA == mt || (mt - mA) * tn * 4 > slots) return M;
+    return mA * hbm;
+}
 
 void launch_gemm(Epi e, bool bf16, const GemmArgs& a, hipStream_t s);
 
@@ -72,7 +90,7 @@ struct GateArgs {
     const uint8_t* inj;   // injected maps [F, L, N] (batch base) or nullptr
     uint8_t* cur;         // [F*N] this layer's map (or nullptr)
     uint8_t* out_masks;   // [F, L, N] (batch base) or nullptr
-    int* cnt;             // [F] recomputed tokens per frame (or nullptr)
+    int* cnt;             // [F * gate_chunks(N)] recomputed tokens per block (or nullptr)
     const float* ln_g;    // LN1 gain / shift
     const float* ln_b;
     void* ln_out;         // [F*N, D] elem: LN1 rows of recomputed tokens (token-indexed) or nullptr

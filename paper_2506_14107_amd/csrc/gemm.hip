@@ -22,6 +22,7 @@
 //     an XCD's L2 sees few distinct A and W tiles.
 //
 // fp32 path: a plain LDS-tiled VALU GEMM (small fp32 models).
+#include <algorithm>
 #include <cstdlib>
 #include <type_traits>
 
@@ -144,7 +145,7 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int row = row_of(i, q);
-            const int r = row < M ? row : row0;            // a valid row for the tile tail
+            const int r = row < M ? row : M - 1;           // a valid row for the tile tail
             if constexpr (E == Epi::OProj || E == Epi::Fc2) tr[q] = a.idx[r];
             else if constexpr (E == Epi::Patch) tr[q] = (r / a.P) * a.N + 1 + r % a.P;
             else tr[q] = r;
@@ -153,7 +154,7 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
                 const int row = row_of(i, q);
-                const int r = row < M ? row : row0;
+                const int r = row < M ? row : M - 1;
                 if constexpr (E == Epi::OProj)
                     dst[q] = *(const f32x4*)(a.resid + (size_t)tr[q] * Nout + col);
                 else if constexpr (E == Epi::Fc2)
@@ -215,154 +216,31 @@ __device__ __forceinline__ void bare_barrier() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-template <int BM, int BN, int BKD, int S>
-constexpr size_t dma_lds_bytes() { return (size_t)S * (BM + BN) * BKD * 2; }
-
-template <Epi E, int BM, int BN, int BKD, int S, int WPE>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
-void gemm_bf16_k(GemmArgs a) {
-    constexpr int WM = BM / 2, WN = BN / 2, TI = WM / 32, TJ = WN / 32;
-    constexpr int CPR = BKD / 8;                 // 16-byte chunks per LDS row
-    constexpr int RPI = 64 / CPR;                // rows one wavefront instruction fills
-    constexpr int SH = (CPR == 8) ? 1 : 2;       // slot = chunk ^ ((row >> SH) & (CPR - 1))
-    constexpr int LA = BM / RPI / 4, LB = BN / RPI / 4;   // load instructions per wave per stage
-    constexpr int L = LA + LB;
-    constexpr int STAGE = (BM + BN) * BKD;       // elements per stage
-    constexpr int KS = BKD / 16;
-    static_assert(CPR == 4 || CPR == 8, "BK must be 32 or 64");
-    static_assert(LA >= 1 && LB >= 1, "tile too small for 4 wavefronts");
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    uint16_t* sm = (uint16_t*)smem;
-
-    const int M = a.Mdev ? *a.Mdev : a.Mconst;
-    const int tilesN = a.Nout / BN;
-    const int mt = (M + BM - 1) / BM;
-    const int active = mt * tilesN;
-    const int bid = blockIdx.x;
-    if (bid >= active) return;
-    int lid = bid;
-    const int per = active / 8;
-    if (bid < per * 8) lid = (bid % 8) * per + bid / 8;
-    constexpr int GM = 8;
-    const int group = lid / (GM * tilesN);
-    const int first_m = group * GM;
-    const int gsize = min(mt - first_m, GM);
-    const int w_in = lid - group * GM * tilesN;
-    const int tm = first_m + w_in % gsize;
-    const int tn = w_in / gsize;
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int lr = lane & 31, hl = lane >> 5;
-    const int K = a.K;
-
-    // this lane's global source for each of its load instructions (k offset added per stage)
-    const int lrow = lane / CPR, lslot = lane % CPR;
-    const uint16_t* srcA[LA];
-    const uint16_t* srcB[LB];
-#pragma unroll
-    for (int t = 0; t < LA; ++t) {
-        const int r = (wave * LA + t) * RPI + lrow;
-        const int c = lslot ^ ((r >> SH) & (CPR - 1));
-        const int grow = tm * BM + r;
-        const int arow = a.a_idx ? (grow < M ? a.a_idx[grow] : 0) : grow;   // gathered A rows
-        srcA[t] = (const uint16_t*)a.A + (size_t)arow * K + c * 8;
-    }
-#pragma unroll
-    for (int t = 0; t < LB; ++t) {
-        const int r = (wave * LB + t) * RPI + lrow;
-        const int c = lslot ^ ((r >> SH) & (CPR - 1));
-        srcB[t] = (const uint16_t*)a.W + (size_t)(tn * BN + r) * K + c * 8;
-    }
-    auto issue = [&](int kt) {
-        uint16_t* st = sm + (kt % S) * STAGE;
-#pragma unroll
-        for (int t = 0; t < LA; ++t)
-            __builtin_amdgcn_global_load_lds((const void*)(srcA[t] + kt * BKD),
-                (__attribute__((address_space(3))) void*)(st + (wave * LA + t) * RPI * BKD), 16, 0, 0);
-#pragma unroll
-        for (int t = 0; t < LB; ++t)
-            __builtin_amdgcn_global_load_lds((const void*)(srcB[t] + kt * BKD),
-                (__attribute__((address_space(3))) void*)(st + BM * BKD + (wave * LB + t) * RPI * BKD), 16, 0, 0);
-    };
-
-    f32x16 acc[TI][TJ];
-#pragma unroll
-    for (int i = 0; i < TI; ++i)
-#pragma unroll
-        for (int j = 0; j < TJ; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-    const int nk = K / BKD;
-#pragma unroll
-    for (int p = 0; p < S - 1; ++p)
-        if (p < nk) issue(p);
-    for (int kt = 0; kt < nk; ++kt) {
-        // slices kt .. min(kt+S-2, nk-1) are in flight: wait for slice kt only
-        if (kt + S - 2 < nk) wait_vm<(S - 2) * L>();
-        else wait_vm<0>();
-        bare_barrier();
-        if (kt + S - 1 < nk) issue(kt + S - 1);   // reuses the slot consumed at kt-1
-        const uint16_t* st = sm + (kt % S) * STAGE;
-        bf16x8 fa[2][TI], fb[2][TJ];
-        auto frag = [&](int ks, bf16x8 (&xa)[TI], bf16x8 (&xb)[TJ]) {
-            const int c = ks * 2 + hl;
-#pragma unroll
-            for (int i = 0; i < TI; ++i) {
-                const int r = wm * WM + i * 32 + lr;
-                xa[i] = *(const bf16x8*)(st + r * BKD + (c ^ ((r >> SH) & (CPR - 1))) * 8);
-            }
-#pragma unroll
-            for (int j = 0; j < TJ; ++j) {
-                const int r = wn * WN + j * 32 + lr;
-                xb[j] = *(const bf16x8*)(st + BM * BKD + r * BKD + (c ^ ((r >> SH) & (CPR - 1))) * 8);
-            }
-        };
-        frag(0, fa[0], fb[0]);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            if (ks + 1 < KS) frag(ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
-#pragma unroll
-            for (int i = 0; i < TI; ++i)
-#pragma unroll
-                for (int j = 0; j < TJ; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks & 1][j], fa[ks & 1][i],
-                                                                        acc[i][j], 0, 0, 0);
-        }
-    }
-
-    __syncthreads();   // every wave is done with the LDS ring
-    epilogue_lds<E, TI, TJ>(a, acc, (float*)smem + wave * (32 * (TJ * 32 + 4)), tm * BM + wm * WM,
-                            tn * BN + wn * WN, M, lane);
-}
-
-// ---------------- bf16 MFMA GEMM, fully pipelined 256 x 256 variant ----------------------------
-// One wavefront per SIMD (128 x 128 per wave, 256 accumulator registers), so every latency is
-// hidden inside the wave: the DMA ring keeps S-1 k-slices in flight and the MFMA fragments are
-// always one k-step ahead, across stage boundaries too.  The barrier of stage kt+1 sits just
-// before the first fragment loads of stage kt+1; the DMA of a new stage is issued right after
-// it, into the slot every wave finished reading before that barrier.
-template <Epi E, int BM, int BN, int BKD, int S, int WPE>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
-void gemm_bf16_pipe_k(GemmArgs a) {
-    constexpr int WM = BM / 2, WN = BN / 2, TI = WM / 32, TJ = WN / 32;
+// ---------------- bf16 MFMA GEMM, pipelined ----------------------------------------------------
+// One block tile of a wave group: the DMA ring keeps S-1 k-slices in flight and the MFMA
+// fragments are always one k-step ahead, across stage boundaries too.  The barrier of stage
+// kt+1 sits just before the first fragment loads of stage kt+1; the DMA of a new stage is issued
+// right after it, into the slot every wave finished reading before that barrier.  The tile is
+// number `bid` of the rows [m0, M); `sm` is the group's LDS and `wave` its index in the group.
+// Every wavefront of the workgroup passes the same barriers (a group without a tile has left).
+template <Epi E, int BM, int BN, int BKD, int S, int WGM, int WGN>
+__device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int bid, int m0, int M,
+                                          int wave) {
+    constexpr int NW = WGM * WGN;                 // wavefronts, WGM x WGN over the block tile
+    constexpr int WM = BM / WGM, WN = BN / WGN, TI = WM / 32, TJ = WN / 32;
     constexpr int CPR = BKD / 8;
     constexpr int RPI = 64 / CPR;
     constexpr int SH = (CPR == 8) ? 1 : 2;
-    constexpr int LA = BM / RPI / 4, LB = BN / RPI / 4;
+    constexpr int LA = BM / RPI / NW, LB = BN / RPI / NW;
+    static_assert(LA * RPI * NW == BM && LB * RPI * NW == BN, "load split");
     constexpr int L = LA + LB;
     constexpr int STAGE = (BM + BN) * BKD;
     constexpr int KS = BKD / 16;
     static_assert(KS % 2 == 0, "fragment double buffer assumes an even number of k-steps");
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    uint16_t* sm = (uint16_t*)smem;
 
-    const int M = a.Mdev ? *a.Mdev : a.Mconst;
     const int tilesN = a.Nout / BN;
-    const int mt = (M + BM - 1) / BM;
+    const int mt = (M - m0 + BM - 1) / BM;
     const int active = mt * tilesN;
-    const int bid = blockIdx.x;
     if (bid >= active) return;
     int lid = bid;
     const int per = active / 8;
@@ -375,8 +253,8 @@ void gemm_bf16_pipe_k(GemmArgs a) {
     const int tm = first_m + w_in % gsize;
     const int tn = w_in / gsize;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int lane = threadIdx.x & 63;
+    const int wm = wave / WGN, wn = wave % WGN;
     const int lr = lane & 31, hl = lane >> 5;
     const int K = a.K;
 
@@ -387,7 +265,7 @@ void gemm_bf16_pipe_k(GemmArgs a) {
     for (int t = 0; t < LA; ++t) {
         const int r = (wave * LA + t) * RPI + lrow;
         const int c = lslot ^ ((r >> SH) & (CPR - 1));
-        const int grow = tm * BM + r;
+        const int grow = m0 + tm * BM + r;
         const int arow = a.a_idx ? (grow < M ? a.a_idx[grow] : 0) : grow;   // gathered A rows
         srcA[t] = (const uint16_t*)a.A + (size_t)arow * K + c * 8;
     }
@@ -511,22 +389,98 @@ void gemm_bf16_pipe_k(GemmArgs a) {
     slice(kt, F_(), std::integral_constant<int, 0>());                              // last slice
 
     __syncthreads();   // every wave is done with the LDS ring
-    epilogue_lds<E, TI, TJ>(a, acc, (float*)smem + wave * (32 * (TJ * 32 + 4)), tm * BM + wm * WM,
-                            tn * BN + wn * WN, M, lane);
+    epilogue_lds<E, TI, TJ>(a, acc, (float*)sm + wave * (32 * (TJ * 32 + 4)),
+                            m0 + tm * BM + wm * WM, tn * BN + wn * WN, M, lane);
 }
 
-template <Epi E, int BM, int BN, int BKD, int S, int WPE>
-void launch_pipe(const GemmArgs& a, hipStream_t s) {
+// LDS of one block tile: the DMA ring, reused by the epilogue's per-wave slabs
+template <int BM, int BN, int BKD, int S, int WGM, int WGN>
+constexpr size_t pipe_lds_bytes() {
+    constexpr size_t ring = (size_t)S * (BM + BN) * BKD * 2;
+    constexpr size_t slabs = (size_t)WGM * WGN * 32 * (BN / WGN + 4) * 4;
+    return ring > slabs ? ring : slabs;
+}
+
+// Tail tiles of a split launch: 64 x 64, 3-stage ring, one per group of four wavefronts.
+constexpr int TBM = 64, TBN = 64, TS = 3;
+constexpr size_t TAIL_LDS = pipe_lds_bytes<TBM, TBN, 32, TS, 2, 2>();
+
+// Block tiles BM x BN of WGM x WGN wavefronts.  With a.slots set, the launch is split: blocks
+// below a.head_grid take the rows [0, head) that fill whole rounds of the grid
+// (gemm_head_rows), and the blocks after them cut the remaining rows into 64 x 64 tiles, one per
+// group of four wavefronts, so that the last, partial round spreads over many compute units.
+template <Epi E, int BM, int BN, int BKD, int S, int WPE, int WGM, int WGN>
+__global__ __launch_bounds__(WGM * WGN * 64) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
+void gemm_bf16_pipe_k(GemmArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    constexpr int NW = WGM * WGN;
+    const int wave = threadIdx.x >> 6;
+    const int M = a.Mdev ? *a.Mdev : a.Mconst;
+    if (!a.slots) {
+        pipe_tile<E, BM, BN, BKD, S, WGM, WGN>(a, (uint16_t*)smem, blockIdx.x, 0, M, wave);
+        return;
+    }
+    const int head = gemm_head_rows(M, a.Nout, BM, BN, a.slots);
+    if ((int)blockIdx.x < a.head_grid) {
+        pipe_tile<E, BM, BN, BKD, S, WGM, WGN>(a, (uint16_t*)smem, blockIdx.x, 0, head, wave);
+        return;
+    }
+    static_assert(NW % 4 == 0, "tail tiles take groups of four wavefronts");
+    const int grp = wave / 4;
+    const int tb = ((int)blockIdx.x - a.head_grid) * (NW / 4) + grp;
+    pipe_tile<E, TBM, TBN, 32, TS, 2, 2>(a, (uint16_t*)(smem + grp * TAIL_LDS), tb, head, M,
+                                         wave % 4);
+}
+
+template <Epi E, int BM, int BN, int BKD, int S, int WPE, int WGM, int WGN>
+constexpr size_t pipe_kernel_lds() {
+    constexpr size_t t = pipe_lds_bytes<BM, BN, BKD, S, WGM, WGN>();
+    constexpr size_t tail = TAIL_LDS * (WGM * WGN / 4);
+    return t > tail ? t : tail;
+}
+
+// Blocks of this configuration that fit on one compute unit (0 if the query fails).
+template <Epi E, int BM, int BN, int BKD, int S, int WPE, int WGM, int WGN>
+int pipe_blocks_per_cu(const void* k, size_t lds) {
+    static int n = -1;
+    if (n < 0) {
+        int v = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, k, WGM * WGN * 64, lds) != hipSuccess)
+            v = 0;
+        n = v;
+    }
+    return n;
+}
+
+// split: cut the last partial round into 64 x 64 tiles (needs a.cus and Nout % 64 == 0)
+template <Epi E, int BM, int BN, int BKD, int S, int WPE, int WGM = 2, int WGN = 2>
+void launch_pipe(const GemmArgs& a0, hipStream_t s, bool split = true) {
     static bool raised = false;
-    constexpr size_t lds = (size_t)S * (BM + BN) * BKD * 2;
-    static_assert(lds <= 160 * 1024, "LDS ring exceeds 160 KiB");
+    constexpr size_t lds = pipe_kernel_lds<E, BM, BN, BKD, S, WPE, WGM, WGN>();
+    static_assert(lds <= 160 * 1024, "LDS exceeds 160 KiB");
+    auto k = gemm_bf16_pipe_k<E, BM, BN, BKD, S, WPE, WGM, WGN>;
     if (!raised) {
-        (void)hipFuncSetAttribute((const void*)gemm_bf16_pipe_k<E, BM, BN, BKD, S, WPE>,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  (int)lds);
         raised = true;
     }
-    const int grid = ((a.Mmax + BM - 1) / BM) * (a.Nout / BN);
-    hipLaunchKernelGGL((gemm_bf16_pipe_k<E, BM, BN, BKD, S, WPE>), dim3(grid), dim3(256), lds, s, a);
+    GemmArgs a = a0;
+    const int tn = a.Nout / BN;
+    a.head_grid = ((a.Mmax + BM - 1) / BM) * tn;
+    a.slots = 0;
+    int grid = a.head_grid;
+    const int per_cu = split && a.cus > 0 && a.Nout % TBN == 0
+                           ? pipe_blocks_per_cu<E, BM, BN, BKD, S, WPE, WGM, WGN>((const void*)k, lds)
+                           : 0;
+    if (per_cu > 0) {
+        a.slots = a.cus * per_cu;
+        // the tail holds at most a quarter round of large tiles: at most slots/4/tn tile rows
+        const int tail_rows = std::min(a.Mmax, (a.slots / 4 / tn + 1) * BM);
+        const int tail_tiles = ((tail_rows + TBM - 1) / TBM) * (a.Nout / TBN);
+        constexpr int per_block = WGM * WGN / 4;
+        grid += (tail_tiles + per_block - 1) / per_block;
+    }
+    if (grid > 0) hipLaunchKernelGGL(k, dim3(grid), dim3(WGM * WGN * 64), lds, s, a);
 }
 
 // ---------------- fp32 VALU GEMM: block tile 64 x 64, k-step 16, 4 x 4 outputs per thread ---
@@ -581,21 +535,8 @@ __global__ __launch_bounds__(256) void gemm_f32_k(GemmArgs a) {
 }
 
 
-template <Epi E, int BM, int BN, int BKD, int S, int WPE>
-void launch_cfg(const GemmArgs& a, hipStream_t s) {
-    static bool raised = false;
-    constexpr size_t lds = dma_lds_bytes<BM, BN, BKD, S>();
-    static_assert(lds <= 160 * 1024, "LDS ring exceeds 160 KiB");
-    if (!raised) {  // more than the default dynamic LDS (gfx950: 160 KiB per CU)
-        (void)hipFuncSetAttribute((const void*)gemm_bf16_k<E, BM, BN, BKD, S, WPE>,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        raised = true;
-    }
-    const int grid = ((a.Mmax + BM - 1) / BM) * (a.Nout / BN);
-    hipLaunchKernelGGL((gemm_bf16_k<E, BM, BN, BKD, S, WPE>), dim3(grid), dim3(256), lds, s, a);
-}
-
-// Tile configuration per GEMM: the tuning override DV_GEMM_CFG picks another table row.
+// Tile configuration: 0 the table in launch_one; tuning overrides (DV_GEMM_CFG): 1 = 256 x 128
+// everywhere, 2 = 256 x 256 wherever Nout allows, 3 = the table without the split last round.
 int gemm_cfg() {
     static int v = -1;
     if (v < 0) {
@@ -612,19 +553,14 @@ void launch_one(bool bf16, const GemmArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(gemm_f32_k<E>, dim3(grid), dim3(256), 0, s, a);
         return;
     }
-    const bool wide = E != Epi::Patch && a.Nout % 256 == 0;
-    switch (gemm_cfg()) {
-        case 1:   // the simpler loop, same tiles
-            launch_cfg<E, 256, 128, 32, 3, 2>(a, s);
-            break;
-        case 2:   // 256 x 256 tiles, one wave per SIMD
-            if (wide) launch_pipe<E, 256, 256, 32, 4, 1>(a, s);
-            else launch_pipe<E, 256, 128, 32, 3, 2>(a, s);
-            break;
-        default:  // 256 x 128 tiles, 3-stage ring of 32-wide k-slices, two blocks per CU
-            launch_pipe<E, 256, 128, 32, 3, 2>(a, s);
-            break;
-    }
+    // 256 x 256 tiles of eight wavefronts (one block per CU) where Nout allows, except for the
+    // GELU GEMM, whose long epilogue overlaps better with 256 x 128 tiles, two blocks per CU
+    const bool wide = a.Nout % 256 == 0;
+    const int cfg = gemm_cfg();
+    const bool big = cfg == 1 ? false : cfg == 2 ? wide : wide && E != Epi::Fc1 && E != Epi::Patch;
+    const bool split = cfg != 3;
+    if (big) launch_pipe<E, 256, 256, 32, 4, 2, 2, 4>(a, s, split);
+    else launch_pipe<E, 256, 128, 32, 3, 2>(a, s, split);
 }
 
 }  // namespace
