@@ -297,6 +297,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             at.N = N;
             at.D = D;
             at.H = d.H;
+            at.G = dense ? 0 : G;
             launch_attention(bf, at, s);
         }
         {

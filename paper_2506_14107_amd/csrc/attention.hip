@@ -98,7 +98,19 @@ void attn_mfma_k(AttnArgs a) {
     constexpr int CH = DH / 8;           // 16-byte chunks per row
     constexpr int NT = AW * 64;
     extern __shared__ __attribute__((aligned(16))) char smem[];
-    const int f = blockIdx.x, h = blockIdx.y;
+    // with reuse (G > 0) the blocks (f, h) of a group's frames share one XCD, whose L2 then
+    // serves the reference rows all of them read; without, frames vary fastest
+    int f, h;
+    if (a.G > 0) {
+        int u, j;
+        xcd_unit(blockIdx.x, a.G, u, j);
+        h = u % a.H;
+        f = u / a.H * a.G + j;
+        if (f >= a.F) return;   // uniform across the block
+    } else {
+        f = blockIdx.x % a.F;
+        h = blockIdx.x / a.F;
+    }
     const int N = a.N, D = a.D;
     const Geo g(N, DH);
     uint16_t* Ks = (uint16_t*)smem;
@@ -387,7 +399,8 @@ void launch_bf16(const AttnArgs& a, hipStream_t s) {
                                   hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         raised = true;
     }
-    hipLaunchKernelGGL(attn_mfma_k<DH>, dim3(a.F, a.H), dim3(AW * 64), lds, s, a);
+    const int grid = a.G > 0 ? xcd_unit_grid((a.F + a.G - 1) / a.G * a.H, a.G) : a.F * a.H;
+    hipLaunchKernelGGL(attn_mfma_k<DH>, dim3(grid), dim3(AW * 64), lds, s, a);
 }
 
 }  // namespace

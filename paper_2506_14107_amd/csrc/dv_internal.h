@@ -16,6 +16,17 @@ __host__ __device__ inline float bf16_to_f32(uint16_t h) {
     return __builtin_bit_cast(float, (uint32_t)h << 16);
 }
 
+// ---- placement of a group's frames on one XCD -------------------------------------------------
+// Workgroups are dealt to the 8 XCDs round-robin (block b runs on XCD b % 8), and each XCD has
+// its own L2.  A unit of G blocks that read the same reference-frame rows (the G frames of one
+// group) is placed on one XCD: unit u's item j is block (u / 8) * 8G + 8j + u % 8.
+__device__ inline void xcd_unit(int b, int G, int& u, int& j) {
+    const int q = b / 8;
+    u = (q / G) * 8 + b % 8;
+    j = q % G;
+}
+inline int xcd_unit_grid(int units, int G) { return (units + 7) / 8 * 8 * G; }
+
 // ---- GEMM ------------------------------------------------------------------------------------
 // C[M, Nout] = A[M, K] * W[Nout, K]^T with a fused epilogue.  M is read on the device.
 enum class Epi : int {
@@ -69,6 +80,7 @@ struct AttnArgs {
     const int* qoff;   // [F+1] packed query rows of frame f: qoff[f] .. qoff[f+1]
     void* out;         // [M, D] elem
     int F, N, D, H;
+    int G;             // group size, 0 without reuse (block placement only)
 };
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
 size_t attention_lds_bytes(bool bf16, int N, int dh);

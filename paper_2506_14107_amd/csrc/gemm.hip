@@ -553,13 +553,14 @@ void launch_one(bool bf16, const GemmArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(gemm_f32_k<E>, dim3(grid), dim3(256), 0, s, a);
         return;
     }
-    // 256 x 256 tiles of eight wavefronts (one block per CU) where Nout allows, except for the
-    // GELU GEMM, whose long epilogue overlaps better with 256 x 128 tiles, two blocks per CU
+    // 256 x 256 tiles of eight wavefronts with a double-buffered 64-deep k-slice (one block per
+    // CU) where Nout allows, except for the GELU GEMM, whose long epilogue overlaps better with
+    // 256 x 128 tiles, two blocks per CU
     const bool wide = a.Nout % 256 == 0;
     const int cfg = gemm_cfg();
     const bool big = cfg == 1 ? false : cfg == 2 ? wide : wide && E != Epi::Fc1 && E != Epi::Patch;
     const bool split = cfg != 3;
-    if (big) launch_pipe<E, 256, 256, 32, 4, 2, 2, 4>(a, s, split);
+    if (big) launch_pipe<E, 256, 256, 64, 2, 2, 2, 4>(a, s, split);
     else launch_pipe<E, 256, 128, 32, 3, 2>(a, s, split);
 }
 

@@ -162,7 +162,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     if (threadIdx.x == 0 && a.cnt) {
         int s = 0;
         for (int w = 0; w < nwaves; ++w) s += wcount[w];
-        a.cnt[blockIdx.x] = s;
+        a.cnt[f * chunks + ch] = s;
     }
 }
 
