@@ -10,9 +10,23 @@ namespace {
 constexpr int WAVE = 64;
 constexpr int MAX_CHUNKS = 8;  // float4 chunks per lane: D <= 2048
 
+// Sum over the 64 lanes, in every lane: DPP steps within rows of 16 lanes (quad swaps, then the
+// half-row and row mirrors), one LDS shuffle across rows, and the permlane32 swap across the two
+// halves of the wavefront.
+template <int CTRL>
+__device__ inline float dpp_mov(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                                 CTRL, 0xF, 0xF, false));
+}
 __device__ inline float wave_sum(float v) {
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, WAVE);
-    return v;
+    v += dpp_mov<0xB1>(v);    // quad_perm [1,0,3,2]
+    v += dpp_mov<0x4E>(v);    // quad_perm [2,3,0,1]
+    v += dpp_mov<0x141>(v);   // row_half_mirror
+    v += dpp_mov<0x140>(v);   // row_mirror
+    v += __shfl_xor(v, 16, WAVE);
+    const unsigned u = __builtin_bit_cast(unsigned, v);
+    const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return v + __builtin_bit_cast(float, (threadIdx.x & 32) ? r[0] : r[1]);
 }
 
 // --- patch gather: A[f*P + k, e] = frame[f][c][py*p+ky][px*p+kx], e = (c, ky, kx); zero pad to Kp
