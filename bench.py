@@ -78,6 +78,13 @@ def stage_bytes(stage, m, Ml):
     return 0.0
 
 
+def attn_bytes(m, Ml, F):
+    """Algorithmic HBM bytes of one attention launch: the packed query rows read and the output
+    rows written once, and every frame's N keys and values (fresh or the reference's) once."""
+    D, N = m.width, m.n_tokens
+    return Ml * D * 2 * 2 + F * N * 2 * D * 2
+
+
 KERNEL_SOURCE = {"qkv": "gemm.hip", "oproj": "gemm.hip", "fc1": "gemm.hip", "fc2": "gemm.hip",
                  "attn": "attention.hip"}
 
@@ -95,6 +102,65 @@ def measured_traffic(stage):
     path = os.path.join(ROOT, "paper_2506_14107_amd", "csrc", src)
     sha = hashlib.sha256(open(path, "rb").read()).hexdigest()
     return r["traffic_bytes_per_launch"] if r.get("source_sha256") == sha else None
+
+
+STAGE_KERNEL = {"qkv": "Epi)1", "oproj": "Epi)2", "fc1": "Epi)3", "fc2": "Epi)4",
+                "attn": "attn_mfma_k"}
+
+
+def traffic_record(fetch_csv, write_csv, bench_json, cmds):
+    """Turns two rocprofv3 --pmc passes over `bench.py --copy-calibration` (FETCH_SIZE, then
+    WRITE_SIZE; KiB per dispatch) into profiles/<stage>_hbm_traffic.json for each stage.  The
+    counters are scaled by what they read for the 1 GiB copy of the same run; the stage's
+    launches of the timed region are the last ones before that copy."""
+    import csv
+    import hashlib
+    bench = None
+    with open(bench_json) as fh:
+        for line in fh:
+            if line.startswith("{"):
+                bench = json.loads(line)
+    stages = bench["stages"]
+
+    def rows(path, counter):
+        with open(path) as fh:
+            rs = [r for r in csv.DictReader(fh) if r["Counter_Name"] == counter]
+        rs.sort(key=lambda r: int(r["Dispatch_Id"]))
+        copies = [r for r in rs if "copyBuffer" in r["Kernel_Name"] and int(r["Grid_Size"]) >= 131072]
+        return rs, copies[-1]
+
+    fr, fcopy = rows(fetch_csv, "FETCH_SIZE")
+    wr, wcopy = rows(write_csv, "WRITE_SIZE")
+    gib_kib = float(1 << 20)
+    fs, ws = gib_kib / float(fcopy["Counter_Value"]), gib_kib / float(wcopy["Counter_Value"])
+    out = {}
+    for stage, info in stages.items():
+        key, n = STAGE_KERNEL[stage], info["launches"]
+
+        def timed(rs, cut):
+            ks = [r for r in rs if key in r["Kernel_Name"] and int(r["Dispatch_Id"]) < cut]
+            return ks[-n:]
+        fk = timed(fr, int(fcopy["Dispatch_Id"]))
+        wk = timed(wr, int(wcopy["Dispatch_Id"]))
+        f_avg = float(np.mean([float(r["Counter_Value"]) for r in fk]))
+        w_avg = float(np.mean([float(r["Counter_Value"]) for r in wk]))
+        traffic = (f_avg * fs + w_avg * ws) * 1024
+        src = os.path.join("paper_2506_14107_amd", "csrc", KERNEL_SOURCE[stage])
+        sha = hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest()
+        rec = {"kernel": fk[0]["Kernel_Name"], "stage": stage, "source": src, "source_sha256": sha,
+               "launches_averaged": len(fk), "fetch_kib_per_launch": round(f_avg, 1),
+               "write_kib_per_launch": round(w_avg, 1),
+               "copy_1GiB_fetch_kib": float(fcopy["Counter_Value"]),
+               "copy_1GiB_write_kib": float(wcopy["Counter_Value"]),
+               "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
+               "traffic_bytes_per_launch": round(traffic),
+               "algo_bytes_per_launch": info["algo_bytes_per_launch"],
+               "traffic_over_algo": round(traffic / info["algo_bytes_per_launch"], 3),
+               "commands": cmds}
+        with open(os.path.join(ROOT, "profiles", f"{stage}_hbm_traffic.json"), "w") as fh:
+            json.dump(rec, fh, indent=1)
+        out[stage] = rec
+    return out
 
 
 def calibrate(enc, x, G, target, iters=24):
@@ -152,7 +218,19 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device-to-device copy (HBM counter calibration)")
+    ap.add_argument("--traffic-record", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_OUT"),
+                    help="write profiles/<stage>_hbm_traffic.json from two rocprofv3 --pmc passes "
+                         "(FETCH_SIZE, WRITE_SIZE) over bench.py --copy-calibration and that "
+                         "run's output line; no GPU work")
+    ap.add_argument("--command", action="append", default=[],
+                    help="with --traffic-record: the profiling commands, kept in the record")
     args = ap.parse_args()
+    if args.traffic_record:
+        recs = traffic_record(*args.traffic_record, args.command)
+        for st, r in recs.items():
+            print(f"{st}: {r['traffic_bytes_per_launch'] / 1e6:.1f} MB per launch, "
+                  f"{r['traffic_over_algo']}x algorithmic")
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported (this path runs "
               "on a single MI355X; groups are independent, see the sharding notes)", file=sys.stderr)
@@ -270,6 +348,15 @@ def main():
         log("[bench] copy calibration: 1 GiB device-to-device copy done")
         del src, dst
 
+    # per-stage launches and algorithmic bytes per launch in the timed region
+    launches_per_stage = args.steps * len(levels) * m.depth
+    stages = {}
+    for stg in ("qkv", "oproj", "fc1", "fc2", "attn"):
+        tot = sum((attn_bytes(m, Ml, F) if stg == "attn" else stage_bytes(stg, m, Ml))
+                  for lv in levels for Ml in lv["Ml"]) * args.steps
+        stages[stg] = {"launches": launches_per_stage,
+                       "algo_bytes_per_launch": round(tot / launches_per_stage)}
+
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(w, blob, frames, taus)
@@ -288,6 +375,7 @@ def main():
         "sweep": sweep,
         "dense_frames_per_s": round(dense_fps, 1),
         "roofline": roof,
+        "stages": stages,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
