@@ -205,11 +205,10 @@ void attn_mfma_k(AttnArgs a) {
 
     float m = -INFINITY, l = 0.f;   // running max (raw score units) and sum
     f32x16 o[DB];
-    int my_t = -1, my_s = 0;
+    int my_t = -1;
     for (int item = wave; item < ntile * S; item += AW) {
         const int t = item / S, sp = item % S;
         my_t = t;
-        my_s = sp;
         const int myq = q0 + t * 32 + lr;
         const int qrow = myq < q1 ? myq : q1 - 1;   // tail lanes compute on a valid row
         bf16x8 qf[KS];
@@ -302,33 +301,30 @@ void attn_mfma_k(AttnArgs a) {
             }
     }
     __syncthreads();
-    if (my_t >= 0 && my_s == 0) {
-        const int myq = q0 + my_t * 32 + lr;
+    // every thread merges 4 output dims of one query: the S partial states of tile t sit in the
+    // slots of waves t*S .. t*S+S-1
+    constexpr int DC = DH / 4;
+    for (int i = tid; i < ntile * 32 * DC; i += NT) {
+        const int t = i / (32 * DC), rest = i % (32 * DC);
+        const int q = rest % 32, dc = rest / 32;
+        const int myq = q0 + t * 32 + q;
+        if (myq >= q1) continue;
+        const float* pt = part + (size_t)t * S * STRIDE;
         float M = -INFINITY;
-        for (int sp = 0; sp < S; ++sp) M = fmaxf(M, part[(wave + sp) * STRIDE + lr]);
-        float L = 0.f;
-        for (int sp = 0; sp < S; ++sp)
-            L += __builtin_amdgcn_exp2f((part[(wave + sp) * STRIDE + lr] - M) * sl2) *
-                 part[(wave + sp) * STRIDE + 32 + lr];
-        if (myq < q1) {
-            const float inv = 1.0f / L;
-            uint16_t* dst = (uint16_t*)a.out + (size_t)myq * D + h * DH;
-            for (int d0 = hl * 4; d0 < DH; d0 += 8) {
-                float v[4];
+        for (int sp = 0; sp < S; ++sp) M = fmaxf(M, pt[sp * STRIDE + q]);
+        float L = 0.f, v[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int sp = 0; sp < S; ++sp) {
+            const float* ps = pt + sp * STRIDE;
+            const float w = __builtin_amdgcn_exp2f((ps[q] - M) * sl2);
+            L += w * ps[32 + q];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    float acc = 0.f;
-                    for (int sp = 0; sp < S; ++sp)
-                        acc += __builtin_amdgcn_exp2f((part[(wave + sp) * STRIDE + lr] - M) * sl2) *
-                               part[(wave + sp) * STRIDE + (2 + d0 + e) * 32 + lr];
-                    v[e] = acc * inv;
-                }
-                uint2 pk;
-                pk.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
-                pk.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
-                *(uint2*)(dst + d0) = pk;
-            }
+            for (int e = 0; e < 4; ++e) v[e] += w * ps[(2 + dc * 4 + e) * 32 + q];
         }
+        const float inv = 1.0f / L;
+        uint2 pk;
+        pk.x = (uint32_t)f32_to_bf16(v[0] * inv) | ((uint32_t)f32_to_bf16(v[1] * inv) << 16);
+        pk.y = (uint32_t)f32_to_bf16(v[2] * inv) | ((uint32_t)f32_to_bf16(v[3] * inv) << 16);
+        *(uint2*)((uint16_t*)a.out + (size_t)myq * D + h * DH + dc * 4) = pk;
     }
 }
 
