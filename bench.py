@@ -267,13 +267,20 @@ def main():
         mk = mk.cpu().numpy()
         levels.append({"tau": tau, "reuse": reuse_of(mk, G), "Ml": active_rows(mk, G)})
 
-    # the dominant stage: one profiled pass over every level
-    enc.profile(True)
-    for lv in levels:
+    # the dominant stage: one profiled pass over every level (stage times also logged per level)
+    prof = {}
+    for lv in levels + [{"tau": float("-inf"), "reuse": 0.0}]:
+        enc.profile(True)
         enc.encode(x, G, lv["tau"], want_masks=False)
-    torch.cuda.synchronize()
-    prof = enc.profile_read()
-    enc.profile(False)
+        torch.cuda.synchronize()
+        p = enc.profile_read()
+        enc.profile(False)
+        log(f"[bench] stage ms at reuse {lv['reuse']:.2f} (tau {lv['tau']:.4f}): "
+            + ", ".join(f"{k} {v[0]:.2f}" for k, v in p.items() if v[1]))
+        if lv["tau"] != float("-inf"):
+            for k, v in p.items():
+                a = prof.get(k, (0.0, 0))
+                prof[k] = (a[0] + v[0], a[1] + v[1])
     dominant = max(prof, key=lambda s: prof[s][0])
     log("[bench] stage ms per sweep: " + ", ".join(f"{k} {v[0]:.2f}" for k, v in prof.items() if v[1]))
 

@@ -298,6 +298,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             at.D = D;
             at.H = d.H;
             at.G = dense ? 0 : G;
+            at.cus = h->cus;
             launch_attention(bf, at, s);
         }
         {

@@ -38,6 +38,16 @@ __device__ inline void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Workgroup barrier that orders LDS only: this wave's LDS operations are complete and every
+// wave has arrived.  Unlike __syncthreads() it does not wait for global stores in flight, so
+// the output rows of one work item drain while the next item is staged.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 __device__ inline float wmax(float v) {
     for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
     return v;
@@ -91,37 +101,62 @@ constexpr int AW = 8;   // wavefronts per attention block
 // are split S = AW / T ways and the partial softmax states are merged through LDS.  Each
 // softmax step takes two key blocks (two independent MFMA chains, one rescale).
 template <int DH>
+__device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char* smem);
+
+template <int DH>
 __global__ __launch_bounds__(AW * 64) __attribute__((amdgpu_waves_per_eu(DH == 64 ? 4 : 2, DH == 64 ? 4 : 2)))
 void attn_mfma_k(AttnArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    // The grid holds as many blocks as are resident at once (a multiple of 8, one share per
+    // XCD) and each block walks a list of work items (frame f, head h): one item per launch slot
+    // would leave the compute units waiting on workgroup dispatch when items are short, as at
+    // high reuse.  Without reuse the items are striped over the blocks, frames fastest.  With
+    // reuse, a unit (a group's frames, one head) lives on XCD unit % 8, whose L2 then serves
+    // the reference rows all of its frames read; the units of XCD x are dealt to its R blocks
+    // frame-index-major (entry e = unit e % U, frame e / U of the group), so that every block
+    // takes reference and non-reference frames alike.
+    if (a.G > 0) {
+        const int units = (a.F + a.G - 1) / a.G * a.H;
+        const int x = blockIdx.x % 8, R = gridDim.x / 8, r = blockIdx.x / 8;
+        const int U = (units + 7) / 8;
+        for (int e = r; e < U * a.G; e += R) {
+            const int u = x + 8 * (e % U), j = e / U;
+            const int f = u / a.H * a.G + j;
+            if (u < units && f < a.F) attn_item<DH>(a, f, u % a.H, smem);
+            lds_barrier();   // the next item restages K/V over this item's LDS
+        }
+    } else {
+        for (int item = blockIdx.x; item < a.F * a.H; item += gridDim.x) {
+            attn_item<DH>(a, item % a.F, item / a.F, smem);
+            lds_barrier();
+        }
+    }
+}
+
+// One work item: frame f, head h.  Every thread of the block takes the same path.
+template <int DH>
+__device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char* smem) {
     constexpr int KS = DH / 16;          // k-steps of S^T
     constexpr int DB = (DH + 31) / 32;   // 32-row blocks of O^T
     constexpr int CH = DH / 8;           // 16-byte chunks per row
     constexpr int NT = AW * 64;
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    // with reuse (G > 0) the blocks (f, h) of a group's frames share one XCD, whose L2 then
-    // serves the reference rows all of them read; without, frames vary fastest
-    int f, h;
-    if (a.G > 0) {
-        int u, j;
-        xcd_unit(blockIdx.x, a.G, u, j);
-        h = u % a.H;
-        f = u / a.H * a.G + j;
-        if (f >= a.F) return;   // uniform across the block
-    } else {
-        f = blockIdx.x % a.F;
-        h = blockIdx.x / a.F;
-    }
     const int N = a.N, D = a.D;
     const Geo g(N, DH);
     uint16_t* Ks = (uint16_t*)smem;
     uint16_t* Vs = Ks + (size_t)g.npad * g.ldk;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // the thread index passes through an empty asm so that nothing derived from it is hoisted
+    // out of the caller's item loop (that would keep it live, and spilled, across items)
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63, wave = tid >> 6;
     const int hl = lane >> 5, lr = lane & 31;
     const size_t ld3 = 3 * (size_t)D;
     const uint16_t* qkv = (const uint16_t*)a.qkv;
     const int q0 = a.qoff[f], q1 = a.qoff[f + 1];
     const int ntile = (q1 - q0 + 31) / 32;
-    if (ntile == 0) return;   // uniform across the block
+    if (ntile == 0) return;
+
+    const int S = ntile >= AW ? 1 : AW / ntile;   // key-block split per tile
 
     // stage K and V rows (row-major, 16-byte chunks); keys past N repeat key N-1 (finite data
     // whose scores are masked).  Up to four chunks per thread are gathered before any store.
@@ -150,11 +185,10 @@ void attn_mfma_k(AttnArgs a) {
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
 
     const float sl2 = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(dh)
     const int nkb = g.npad / 32;
-    const int S = ntile >= AW ? 1 : AW / ntile;   // key-block split per tile
     const int grp = lane >> 4, gi = lane & 15;    // 16-lane group of the transposing read
     const int tr_key = hl * 4 + (gi >> 2);
     const int tr_dim = (grp & 1) * 16 + (gi & 3) * 4;
@@ -283,7 +317,7 @@ void attn_mfma_k(AttnArgs a) {
     if (S == 1) return;   // uniform across the block: S depends only on the frame
 
     // merge the S partial states of each tile (LDS reused: K/V are no longer read)
-    __syncthreads();
+    lds_barrier();
     float* part = (float*)smem;                       // [AW][2 + DB*32][32] floats
     constexpr int STRIDE = (2 + DB * 32) * 32;
     if (my_t >= 0) {
@@ -300,7 +334,7 @@ void attn_mfma_k(AttnArgs a) {
                 pw[(2 + d) * 32 + lr] = o[b][r];
             }
     }
-    __syncthreads();
+    lds_barrier();
     // every thread merges 4 output dims of one query: the S partial states of tile t sit in the
     // slots of waves t*S .. t*S+S-1
     constexpr int DC = DH / 4;
@@ -395,7 +429,19 @@ void launch_bf16(const AttnArgs& a, hipStream_t s) {
                                   hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         raised = true;
     }
-    const int grid = a.G > 0 ? xcd_unit_grid((a.F + a.G - 1) / a.G * a.H, a.G) : a.F * a.H;
+    // work items: (frame, head) pairs; with reuse, the slots of whole units on each of 8 XCDs
+    const int items = a.G > 0 ? xcd_unit_grid((a.F + a.G - 1) / a.G * a.H, a.G) : a.F * a.H;
+    static int per_cu = -1;
+    if (per_cu < 0) {
+        int v = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, (const void*)attn_mfma_k<DH>, AW * 64,
+                                                         lds) != hipSuccess)
+            v = 0;
+        per_cu = v;
+    }
+    // a multiple of 8 blocks keeps item i on XCD i % 8, as the placement of a group's items assumes
+    int grid = items;
+    if (a.cus > 0 && per_cu > 0) grid = std::min(grid, (a.cus * per_cu + 7) / 8 * 8);
     hipLaunchKernelGGL(attn_mfma_k<DH>, dim3(grid), dim3(AW * 64), lds, s, a);
 }
 

@@ -18,13 +18,9 @@ __host__ __device__ inline float bf16_to_f32(uint16_t h) {
 
 // ---- placement of a group's frames on one XCD -------------------------------------------------
 // Workgroups are dealt to the 8 XCDs round-robin (block b runs on XCD b % 8), and each XCD has
-// its own L2.  A unit of G blocks that read the same reference-frame rows (the G frames of one
-// group) is placed on one XCD: unit u's item j is block (u / 8) * 8G + 8j + u % 8.
-__device__ inline void xcd_unit(int b, int G, int& u, int& j) {
-    const int q = b / 8;
-    u = (q / G) * 8 + b % 8;
-    j = q % G;
-}
+// its own L2.  A unit of G work items that read the same reference-frame rows (the G frames of
+// one group, one head) is placed on one XCD: units u = x, x + 8, ... on XCD x.  Slots for
+// `units` units of G items each, in whole rounds of 8:
 inline int xcd_unit_grid(int units, int G) { return (units + 7) / 8 * 8 * G; }
 
 // ---- GEMM ------------------------------------------------------------------------------------
@@ -81,6 +77,7 @@ struct AttnArgs {
     void* out;         // [M, D] elem
     int F, N, D, H;
     int G;             // group size, 0 without reuse (block placement only)
+    int cus;           // compute units of the device (0: one block per work item)
 };
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
 size_t attention_lds_bytes(bool bf16, int N, int dh);
