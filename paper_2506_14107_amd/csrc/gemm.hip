@@ -383,144 +383,6 @@ __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int b
                             m0 + tm * BM + wm * WM, tn * BN + wn * WN, M, lane);
 }
 
-// ---------------- bf16 MFMA GEMM, ping-pong schedule --------------------------------------------
-// vmcnt(n) for a wave-uniform n in [0, 3*L]: all of this wave's loads but the last n have landed
-template <int L>
-__device__ __forceinline__ void wait_vm_n(int n) {
-    if (n <= 0) wait_vm<0>();
-    else if (n <= L) wait_vm<L>();
-    else if (n <= 2 * L) wait_vm<2 * L>();
-    else wait_vm<3 * L>();
-}
-
-// One 256 x 256 block tile of eight wavefronts in two groups of four.  Group g owns the tile rows
-// g*128 .. +128; wave w % 4 owns 64 of the columns (a 128 x 64 sub-tile of 4 x 2 MFMA tiles, as
-// in pipe_tile).  Waves w and w + 4 share a SIMD, so the two groups take turns on its matrix
-// unit: the tile runs in phases separated by workgroup barriers, and in every phase one group
-// issues the MFMAs of a whole BKD-deep k-slice from registers (high wave priority) while the
-// other group reads its fragments of the next slice from LDS and issues its half of the
-// global -> LDS copies (group 0 the A rows, group 1 the weight rows) of the slice S-1 ahead.
-// Phase 2s + g is group g's read phase for slice s, phase 2s + g + 1 its compute phase.  Slot
-// s % S of the LDS ring is free after phase 2s + 1 (both groups have read slice s), and is
-// refilled with slice s + S from phases 2s + 2 and 2s + 3 on.
-template <Epi E, int BKD, int S>
-__device__ __forceinline__ void pp_tile(const GemmArgs& a, uint16_t* sm, int bid, int M, int wave) {
-    constexpr int BM = 256, BN = 256, TI = 4, TJ = 2;
-    constexpr int CPR = BKD / 8;                  // 16-byte chunks per LDS row
-    constexpr int RPI = 64 / CPR;                 // rows per wavefront DMA instruction
-    constexpr int SH = (CPR == 8) ? 1 : 2;
-    constexpr int L = BM / RPI / 4;               // DMA instructions per wave per slice
-    constexpr int STAGE = (BM + BN) * BKD;
-    constexpr int KS = BKD / 16;
-    static_assert(S >= 3 && S <= 5, "ring depth");
-
-    const int tilesN = a.Nout / BN;
-    const int mt = (M + BM - 1) / BM;
-    const int active = mt * tilesN;
-    if (bid >= active) return;
-    int tm, tn;
-    tile_coords(bid, mt, tilesN, tm, tn);
-
-    const int lane = threadIdx.x & 63;
-    const int g = wave >> 2, wn = wave & 3;
-    const int lr = lane & 31, hl = lane >> 5;
-    const int K = a.K;
-    const int nk = K / BKD;
-
-    // this wave's DMA rows: group 0 copies the A rows of the tile, group 1 the weight rows
-    const int lrow = lane / CPR, lslot = lane % CPR;
-    const uint16_t* src[L];
-#pragma unroll
-    for (int t = 0; t < L; ++t) {
-        const int r = (wn * L + t) * RPI + lrow;
-        const int c = lslot ^ ((r >> SH) & (CPR - 1));
-        if (g == 0) {
-            const int grow = tm * BM + r;
-            const int arow = a.a_idx ? (grow < M ? a.a_idx[grow] : 0) : grow;
-            src[t] = (const uint16_t*)a.A + (size_t)arow * K + c * 8;
-        } else {
-            src[t] = (const uint16_t*)a.W + (size_t)(tn * BN + r) * K + c * 8;
-        }
-    }
-    const int dst0 = g * BM * BKD + wn * L * RPI * BKD;   // element offset inside a stage
-    auto issue = [&](int kt) {
-        uint16_t* st = sm + (kt % S) * STAGE + dst0;
-#pragma unroll
-        for (int t = 0; t < L; ++t)
-            __builtin_amdgcn_global_load_lds((const void*)(src[t] + kt * BKD),
-                (__attribute__((address_space(3))) void*)(st + t * RPI * BKD), 16, 0, 0);
-    };
-    int offA[TI], offB[TJ], swA[TI], swB[TJ];
-#pragma unroll
-    for (int i = 0; i < TI; ++i) {
-        const int r = g * 128 + i * 32 + lr;
-        offA[i] = r * BKD;
-        swA[i] = (r >> SH) & (CPR - 1);
-    }
-#pragma unroll
-    for (int j = 0; j < TJ; ++j) {
-        const int r = wn * 64 + j * 32 + lr;
-        offB[j] = BM * BKD + r * BKD;
-        swB[j] = (r >> SH) & (CPR - 1);
-    }
-    bf16x8 fa[KS][TI], fb[KS][TJ];
-    auto read = [&](int kt) {
-        const uint16_t* st = sm + (kt % S) * STAGE;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const int c = ks * 2 + hl;
-#pragma unroll
-            for (int i = 0; i < TI; ++i) fa[ks][i] = *(const bf16x8*)(st + offA[i] + (c ^ swA[i]) * 8);
-#pragma unroll
-            for (int j = 0; j < TJ; ++j) fb[ks][j] = *(const bf16x8*)(st + offB[j] + (c ^ swB[j]) * 8);
-        }
-    };
-    f32x16 acc[TI][TJ];
-#pragma unroll
-    for (int i = 0; i < TI; ++i)
-#pragma unroll
-        for (int j = 0; j < TJ; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-    auto compute = [&]() {
-        __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-            for (int i = 0; i < TI; ++i)
-#pragma unroll
-                for (int j = 0; j < TJ; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks][j], fa[ks][i], acc[i][j],
-                                                                        0, 0, 0);
-        __builtin_amdgcn_s_setprio(0);
-        __builtin_amdgcn_sched_barrier(0);
-    };
-
-    // prologue: slices 0 .. S-2 in flight, slice 0 landed
-#pragma unroll
-    for (int p = 0; p < S - 1; ++p)
-        if (p < nk) issue(p);
-    wait_vm_n<L>(L * (min(S - 1, nk) - 1));
-    bare_barrier();
-    if (g == 1) bare_barrier();                   // group 1 starts one phase later
-    for (int s = 0; s < nk; ++s) {
-        // read phase: fragments of slice s; copies of slice s + S - 1; slice s + 1 landed
-        read(s);
-        if (s + S - 1 < nk) issue(s + S - 1);
-        wait_vm_n<L>(L * min(S - 2, nk - 2 - s));
-        __builtin_amdgcn_s_waitcnt(0xc07f);       // lgkmcnt(0): the fragments are in registers
-        __builtin_amdgcn_sched_barrier(0);
-        bare_barrier();
-        __builtin_amdgcn_sched_barrier(0);
-        compute();
-        bare_barrier();
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    if (g == 0) bare_barrier();                   // matches group 1's extra first phase
-    epilogue_lds<E, TI, TJ>(a, acc, (float*)sm + wave * (32 * (TJ * 32 + 4)), tm * BM + g * 128,
-                            tn * BN + wn * 64, M, lane);
-}
-
 // LDS of one block tile: the DMA ring, reused by the epilogue's per-wave slabs
 template <int BM, int BN, int BKD, int S, int WGM, int WGN>
 constexpr size_t pipe_lds_bytes() {
@@ -556,38 +418,6 @@ void gemm_bf16_pipe_k(GemmArgs a) {
     static_assert(NW % 4 == 0, "tail tiles take groups of four wavefronts");
     const int grp = wave / 4;
     const int tb = ((int)blockIdx.x - a.head_grid) * (NW / 4) + grp;
-    pipe_tile<E, TBM, TBN, 32, TS, 2, 2>(a, (uint16_t*)(smem + grp * TAIL_LDS), tb, head, M,
-                                         wave % 4);
-}
-
-// Ping-pong block tiles (256 x 256, eight wavefronts); with a.slots set the last partial round is
-// cut into 64 x 64 tiles as in gemm_bf16_pipe_k.
-template <int BKD, int S>
-constexpr size_t pp_lds_bytes() {
-    constexpr size_t ring = (size_t)S * 512 * BKD * 2;
-    constexpr size_t slabs = (size_t)8 * 32 * (64 + 4) * 4;
-    constexpr size_t tail = TAIL_LDS * 2;
-    constexpr size_t m = ring > slabs ? ring : slabs;
-    return m > tail ? m : tail;
-}
-
-template <Epi E, int BKD, int S>
-__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void gemm_bf16_pp_k(GemmArgs a) {
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    const int wave = threadIdx.x >> 6;
-    const int M = a.Mdev ? *a.Mdev : a.Mconst;
-    if (!a.slots) {
-        pp_tile<E, BKD, S>(a, (uint16_t*)smem, blockIdx.x, M, wave);
-        return;
-    }
-    const int head = gemm_head_rows(M, a.Nout, 256, 256, a.slots);
-    if ((int)blockIdx.x < a.head_grid) {
-        pp_tile<E, BKD, S>(a, (uint16_t*)smem, blockIdx.x, head, wave);
-        return;
-    }
-    const int grp = wave / 4;
-    const int tb = ((int)blockIdx.x - a.head_grid) * 2 + grp;
     pipe_tile<E, TBM, TBN, 32, TS, 2, 2>(a, (uint16_t*)(smem + grp * TAIL_LDS), tb, head, M,
                                          wave % 4);
 }
@@ -641,31 +471,6 @@ void launch_pipe(const GemmArgs& a0, hipStream_t s, bool split = true) {
         grid += (tail_tiles + per_block - 1) / per_block;
     }
     if (grid > 0) hipLaunchKernelGGL(k, dim3(grid), dim3(WGM * WGN * 64), lds, s, a);
-}
-
-template <Epi E, int BKD, int S>
-void launch_pp(const GemmArgs& a0, hipStream_t s, bool split = true) {
-    static bool raised = false;
-    constexpr size_t lds = pp_lds_bytes<BKD, S>();
-    static_assert(lds <= 160 * 1024, "LDS exceeds 160 KiB");
-    auto k = gemm_bf16_pp_k<E, BKD, S>;
-    if (!raised) {
-        (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                  (int)lds);
-        raised = true;
-    }
-    GemmArgs a = a0;
-    const int tn = a.Nout / 256;
-    a.head_grid = ((a.Mmax + 255) / 256) * tn;
-    a.slots = 0;
-    int grid = a.head_grid;
-    if (split && a.cus > 0 && a.Nout % TBN == 0) {
-        a.slots = a.cus;   // one block per compute unit
-        const int tail_rows = std::min(a.Mmax, (a.slots / 4 / tn + 1) * 256);
-        const int tail_tiles = ((tail_rows + TBM - 1) / TBM) * (a.Nout / TBN);
-        grid += (tail_tiles + 1) / 2;
-    }
-    if (grid > 0) hipLaunchKernelGGL(k, dim3(grid), dim3(512), lds, s, a);
 }
 
 // ---------------- fp32 VALU GEMM: block tile 64 x 64, k-step 16, 4 x 4 outputs per thread ---
