@@ -86,6 +86,13 @@ struct Geo {
 };
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// four floats to four bf16 (round to nearest even, v_cvt_pk_bf16_f32)
+__device__ inline uint2 pack_bf16x4(float a, float b, float c, float d) {
+    const bf16x4 v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+    return __builtin_bit_cast(uint2, v);
+}
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));   // native vector: stays in VGPRs
 
 // The value a lane's partner in the other half of the wavefront (lane l ^ 32) holds.
@@ -95,11 +102,143 @@ __device__ inline float other_half(float x) {
     return __builtin_bit_cast(float, (threadIdx.x & 32) ? r[0] : r[1]);
 }
 
-constexpr int AW = 8;   // wavefronts per attention block
+constexpr int AW = 8;    // wavefronts of a per-frame attention block
+constexpr int UW = 16;   // wavefronts of a per-unit attention block
 
+// Online-softmax attention of one query tile (fragments qf, one query per lane) against the
+// staged K/V: key blocks kb = sp, sp + S, ... taken two at a time (kb, kb + S) -- two
+// independent MFMA chains and one rescale per step.  krow maps a key to its LDS row.  On
+// return (m, l, o) hold the tile's running max (raw score units), sum and unnormalised output.
+// The arithmetic and its order depend only on the key values, never on where the rows sit.
+template <int DH, class KRow>
+__device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, const uint16_t* Vs,
+                                            int N, int lane, const bf16x8 (&qf)[DH / 16], int sp,
+                                            int S, KRow krow, float& m, float& l,
+                                            f32x16 (&o)[(DH + 31) / 32]) {
+    constexpr int KS = DH / 16;          // k-steps of S^T
+    constexpr int DB = (DH + 31) / 32;   // 32-row blocks of O^T
+    const int hl = lane >> 5, lr = lane & 31;
+    const float sl2 = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(dh)
+    const int nkb = g.npad / 32;
+    const int grp = lane >> 4, gi = lane & 15;    // 16-lane group of the transposing read
+    const int tr_key = hl * 4 + (gi >> 2);
+    const int tr_dim = (grp & 1) * 16 + (gi & 3) * 4;
+
+    // scores of key block kb against the query tile (raw, unscaled)
+    auto scores = [&](int kb) {
+        f32x16 sc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[r] = 0.f;
+        const int row = krow(kb * 32 + lr);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8 kf = *(const bf16x8*)(Ks + g.kofs(row, ks * 2 + hl));
+            sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc, 0, 0, 0);
+        }
+        if ((kb + 1) * 32 > N) {   // ragged last block: keys past N get -inf
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int key = kb * 32 + (r >> 2) * 8 + hl * 4 + (r & 3);
+                sc[r] = key < N ? sc[r] : -INFINITY;
+            }
+        }
+        return sc;
+    };
+    // O^T += V^T(kb) . P^T(kb)
+    auto accumulate = [&](int kb, const bf16x8 (&pf)[2]) {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            // lane (group grp, index gi) names key kb*32 + ks*16 + hl*4 + gi/4 (+8) and dims
+            // b*32 + (grp&1)*16 + 4*(gi%4); it receives dim b*32 + (grp&1)*16 + gi of the 4
+            // keys named by lanes 4e + gi/4 of its group
+            const int key = kb * 32 + ks * 16 + tr_key;
+            const int r0 = krow(key), r1 = krow(key + 8);
+#pragma unroll
+            for (int b = 0; b < DB; ++b) {
+                int d = b * 32 + tr_dim;
+                d = d < DH ? d : DH - 4;   // head dims past DH: any finite row data
+                const uint16_t* p0 = Vs + g.vofs(r0, d >> 3) + (d & 7);
+                const uint16_t* p1 = Vs + g.vofs(r1, d >> 3) + (d & 7);
+                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4*)p0);
+                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4*)p1);
+                const s16x4 both[2] = {lo, hi};
+                const bf16x8 vf = __builtin_bit_cast(bf16x8, both);
+                o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
+            }
+        }
+    };
+
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[b][r] = 0.f;
+    m = -INFINITY;
+    l = 0.f;
+    for (int kb = sp; kb < nkb; kb += 2 * S) {
+        const int kb1 = kb + S;
+        const bool two = kb1 < nkb;
+        const f32x16 s0 = scores(kb);
+        f32x16 s1;
+        if (two) {
+            s1 = scores(kb1);
+        } else {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) s1[r] = -INFINITY;
+        }
+        float bm = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) bm = fmaxf(bm, fmaxf(s0[r], s1[r]));
+        bm = fmaxf(bm, other_half(bm));
+        if (__any(bm > m)) {   // rescale only when some lane's running max moved
+            const float mn = fmaxf(m, bm);
+            const float alpha = __builtin_amdgcn_exp2f((m - mn) * sl2);
+            l *= alpha;
+#pragma unroll
+            for (int b = 0; b < DB; ++b)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) o[b][r] *= alpha;
+            m = mn;
+        }
+        const float nm = -m * sl2;
+        float ps = 0.f;
+        bf16x8 p0[2], p1[2];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], sl2, nm));
+            const float e1 = __builtin_amdgcn_exp2f(fmaf(s1[r], sl2, nm));
+            ps += e0 + e1;
+            p0[r >> 3][r & 7] = (__bf16)e0;
+            p1[r >> 3][r & 7] = (__bf16)e1;
+        }
+        l += ps + other_half(ps);
+        accumulate(kb, p0);
+        if (two) accumulate(kb1, p1);
+    }
+}
+
+// o / l of a lane's query as bf16 to its output row (dims of this lane's register groups)
+template <int DH>
+__device__ __forceinline__ void store_row(uint16_t* dst, int lane, float l,
+                                          const f32x16 (&o)[(DH + 31) / 32]) {
+    constexpr int DB = (DH + 31) / 32;
+    const int hl = lane >> 5;
+    const float inv = 1.0f / l;
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+            const int d = b * 32 + q4 * 8 + hl * 4;
+            if (d < DH)
+                *(uint2*)(dst + d) = pack_bf16x4(o[b][q4 * 4 + 0] * inv, o[b][q4 * 4 + 1] * inv,
+                                                 o[b][q4 * 4 + 2] * inv, o[b][q4 * 4 + 3] * inv);
+        }
+}
+
+// ---- per-frame items ---------------------------------------------------------------------------
 // Work split: T = ceil(q/32) query tiles over AW wavefronts.  With T < AW a tile's key blocks
-// are split S = AW / T ways and the partial softmax states are merged through LDS.  Each
-// softmax step takes two key blocks (two independent MFMA chains, one rescale).
+// are split S = AW / T ways and the partial softmax states are merged through LDS.
 template <int DH>
 __device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char* smem);
 
@@ -109,10 +248,10 @@ void attn_mfma_k(AttnArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     // The grid holds as many blocks as are resident at once (a multiple of 8, one share per
     // XCD) and each block walks a list of work items (frame f, head h): one item per launch slot
-    // would leave the compute units waiting on workgroup dispatch when items are short, as at
-    // high reuse.  Without reuse the items are striped over the blocks, frames fastest.  With
-    // reuse, a unit (a group's frames, one head) lives on XCD unit % 8, whose L2 then serves
-    // the reference rows all of its frames read; the units of XCD x are dealt to its R blocks
+    // would leave the compute units waiting on workgroup dispatch when items are short.
+    // Without reuse the items are striped over the blocks, frames fastest.  With reuse, a unit
+    // (a group's frames, one head) lives on XCD unit % 8, whose L2 then serves the reference
+    // rows all of its frames read; the units of XCD x are dealt to its R blocks
     // frame-index-major (entry e = unit e % U, frame e / U of the group), so that every block
     // takes reference and non-reference frames alike.
     if (a.G > 0) {
@@ -187,56 +326,6 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char*
     }
     lds_barrier();
 
-    const float sl2 = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(dh)
-    const int nkb = g.npad / 32;
-    const int grp = lane >> 4, gi = lane & 15;    // 16-lane group of the transposing read
-    const int tr_key = hl * 4 + (gi >> 2);
-    const int tr_dim = (grp & 1) * 16 + (gi & 3) * 4;
-
-    // scores of key block kb against the query tile (raw, unscaled)
-    auto scores = [&](int kb, const bf16x8 (&qf)[KS]) {
-        f32x16 sc;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sc[r] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const bf16x8 kf = *(const bf16x8*)(Ks + g.kofs(kb * 32 + lr, ks * 2 + hl));
-            sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc, 0, 0, 0);
-        }
-        if ((kb + 1) * 32 > N) {   // ragged last block: keys past N get -inf
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int key = kb * 32 + (r >> 2) * 8 + hl * 4 + (r & 3);
-                sc[r] = key < N ? sc[r] : -INFINITY;
-            }
-        }
-        return sc;
-    };
-    // O^T += V^T(kb) . P^T(kb)
-    auto accumulate = [&](int kb, const bf16x8 (&pf)[2], f32x16 (&o)[DB]) {
-#pragma unroll
-        for (int b = 0; b < DB; ++b) {
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                // lane (group grp, index gi) names key kb*32 + ks*16 + hl*4 + gi/4 (+8) and
-                // dims b*32 + (grp&1)*16 + 4*(gi%4); it receives dim b*32 + (grp&1)*16 + gi
-                // of the 4 keys named by lanes 4e + gi/4 of its group
-                const int key = kb * 32 + ks * 16 + tr_key;
-                int d = b * 32 + tr_dim;
-                d = d < DH ? d : DH - 4;   // head dims past DH: any finite row data
-                const uint16_t* p0 = Vs + g.vofs(key, d >> 3) + (d & 7);
-                const uint16_t* p1 = Vs + g.vofs(key + 8, d >> 3) + (d & 7);
-                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) s16x4*)p0);
-                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) s16x4*)p1);
-                const s16x4 both[2] = {lo, hi};
-                const bf16x8 vf = __builtin_bit_cast(bf16x8, both);
-                o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
-            }
-        }
-    };
-
     float m = -INFINITY, l = 0.f;   // running max (raw score units) and sum
     f32x16 o[DB];
     int my_t = -1;
@@ -249,72 +338,11 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char*
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
             qf[ks] = *(const bf16x8*)(qkv + (size_t)qrow * ld3 + h * DH + ks * 16 + hl * 8);
-#pragma unroll
-        for (int b = 0; b < DB; ++b)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) o[b][r] = 0.f;
-        m = -INFINITY;
-        l = 0.f;
-        for (int kb = sp; kb < nkb; kb += 2 * S) {
-            const int kb1 = kb + S;
-            const bool two = kb1 < nkb;
-            const f32x16 s0 = scores(kb, qf);
-            f32x16 s1;
-            if (two) {
-                s1 = scores(kb1, qf);
-            } else {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) s1[r] = -INFINITY;
-            }
-            float bm = -INFINITY;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) bm = fmaxf(bm, fmaxf(s0[r], s1[r]));
-            bm = fmaxf(bm, other_half(bm));
-            if (__any(bm > m)) {   // rescale only when some lane's running max moved
-                const float mn = fmaxf(m, bm);
-                const float alpha = __builtin_amdgcn_exp2f((m - mn) * sl2);
-                l *= alpha;
-#pragma unroll
-                for (int b = 0; b < DB; ++b)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) o[b][r] *= alpha;
-                m = mn;
-            }
-            const float nm = -m * sl2;
-            float ps = 0.f;
-            bf16x8 p0[2], p1[2];
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], sl2, nm));
-                const float e1 = __builtin_amdgcn_exp2f(fmaf(s1[r], sl2, nm));
-                ps += e0 + e1;
-                p0[r >> 3][r & 7] = (__bf16)e0;
-                p1[r >> 3][r & 7] = (__bf16)e1;
-            }
-            l += ps + other_half(ps);
-            accumulate(kb, p0, o);
-            if (two) accumulate(kb1, p1, o);
-        }
-        if (S == 1 && myq < q1) {
-            const float inv = 1.0f / l;
-            uint16_t* dst = (uint16_t*)a.out + (size_t)myq * D + h * DH;
-#pragma unroll
-            for (int b = 0; b < DB; ++b)
-#pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) {
-                    const int d = b * 32 + q4 * 8 + hl * 4;
-                    if (d < DH) {
-                        uint2 pk;
-                        pk.x = (uint32_t)f32_to_bf16(o[b][q4 * 4 + 0] * inv) |
-                               ((uint32_t)f32_to_bf16(o[b][q4 * 4 + 1] * inv) << 16);
-                        pk.y = (uint32_t)f32_to_bf16(o[b][q4 * 4 + 2] * inv) |
-                               ((uint32_t)f32_to_bf16(o[b][q4 * 4 + 3] * inv) << 16);
-                        *(uint2*)(dst + d) = pk;
-                    }
-                }
-        }
+        attend_tile<DH>(g, Ks, Vs, N, lane, qf, sp, S, [](int k) { return k; }, m, l, o);
+        if (S == 1 && myq < q1) store_row<DH>((uint16_t*)a.out + (size_t)myq * D + h * DH, lane, l, o);
     }
     if (S == 1) return;   // uniform across the block: S depends only on the frame
+    const float sl2 = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(dh)
 
     // merge the S partial states of each tile (LDS reused: K/V are no longer read)
     lds_barrier();
@@ -355,10 +383,144 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char*
             for (int e = 0; e < 4; ++e) v[e] += w * ps[(2 + dc * 4 + e) * 32 + q];
         }
         const float inv = 1.0f / L;
-        uint2 pk;
-        pk.x = (uint32_t)f32_to_bf16(v[0] * inv) | ((uint32_t)f32_to_bf16(v[1] * inv) << 16);
-        pk.y = (uint32_t)f32_to_bf16(v[2] * inv) | ((uint32_t)f32_to_bf16(v[3] * inv) << 16);
-        *(uint2*)((uint16_t*)a.out + (size_t)myq * D + h * DH + dc * 4) = pk;
+        *(uint2*)((uint16_t*)a.out + (size_t)myq * D + h * DH + dc * 4) =
+            pack_bf16x4(v[0] * inv, v[1] * inv, v[2] * inv, v[3] * inv);
+    }
+}
+
+// ---- per-unit items ----------------------------------------------------------------------------
+// A unit is one group of frames and one head.  The reference frame's keys are staged once; a
+// non-reference frame reads each reused key from the reference's row and each recomputed key
+// from its own row, through a per-frame key -> row map.  A frame's own rows, and those of
+// consecutive frames, are consecutive packed rows (stable frame-major compaction; the reference
+// frame is recomputed in full, its token i at packed row qoff[f0] + i), so staging is a copy of
+// contiguous rows.  Every query tile of the unit goes to one wavefront, over all key blocks:
+// no key split and no merge.
+//
+// LDS: K and V arrays of npad reference rows (keys past N repeat key N-1) followed by up to pcap
+// rows of other frames; then one 16-bit key -> row map of npad entries per frame of the group.
+struct UnitGeo {
+    Geo g;
+    int pcap, G;
+    __host__ __device__ UnitGeo(int N, int dh, int G_, int pcap_) : g(N, dh), pcap(pcap_), G(G_) {}
+    __host__ __device__ int rows() const { return g.npad + pcap; }
+    __host__ __device__ size_t vbase() const { return (size_t)rows() * g.ldk; }   // elements
+    __host__ __device__ size_t mbase() const { return vbase() + (size_t)rows() * g.ldv; }
+    __host__ __device__ size_t bytes() const { return (mbase() + (size_t)G * g.npad) * 2; }
+};
+
+// Rows of other frames that fit in `limit` bytes of LDS next to the reference rows and maps.
+inline int unit_pcap(int N, int dh, int G, size_t limit) {
+    const UnitGeo u(N, dh, G, 0);
+    const size_t per = (size_t)(u.g.ldk + u.g.ldv) * 2;
+    return u.bytes() >= limit ? 0 : (int)std::min<size_t>((limit - u.bytes()) / per, 32767);
+}
+
+// LDS rows dst0 .. dst0+count-1 of K and V <- packed rows src0 + min(i, nvalid - 1), head h
+template <int DH, int NT>
+__device__ __forceinline__ void stage_rows(const Geo& g, uint16_t* Ks, uint16_t* Vs,
+                                           const uint16_t* qkv, size_t ld3, int D, int h, int dst0,
+                                           int src0, int count, int nvalid, int tid) {
+    constexpr int CH = DH / 8;
+    const int total = count * CH;
+    for (int c0 = tid; c0 < total; c0 += 4 * NT) {
+        u32x4 kv[4], vv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int c = min(c0 + u * NT, total - 1);
+            const size_t off = (size_t)(src0 + min(c / CH, nvalid - 1)) * ld3 + h * DH + (c % CH) * 8;
+            kv[u] = *(const u32x4*)(qkv + off + D);
+            vv[u] = *(const u32x4*)(qkv + off + 2 * D);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int c = c0 + u * NT;
+            if (c < total) {
+                const int i = dst0 + c / CH, part = c % CH;
+                *(u32x4*)(Ks + g.kofs(i, part)) = kv[u];
+                *(u32x4*)(Vs + g.vofs(i, part)) = vv[u];
+            }
+        }
+    }
+}
+
+template <int DH>
+__global__ __launch_bounds__(UW * 64) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void attn_unit_k(AttnArgs a, int pcap) {
+    constexpr int KS = DH / 16;
+    constexpr int DB = (DH + 31) / 32;
+    constexpr int NT = UW * 64;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int G = a.G, N = a.N, D = a.D, H = a.H;
+    const UnitGeo ug(N, DH, G, pcap);
+    const Geo& g = ug.g;
+    uint16_t* Ks = (uint16_t*)smem;
+    uint16_t* Vs = Ks + ug.vbase();
+    uint16_t* kmap = Ks + ug.mbase();
+    const uint16_t* qkv = (const uint16_t*)a.qkv;
+    const size_t ld3 = 3 * (size_t)D;
+    const int units = (a.F + G - 1) / G * H;
+    const int Tref = (N + 31) / 32;   // query tiles of a reference frame
+    for (int u = blockIdx.x; u < units; u += gridDim.x) {
+        int tid = threadIdx.x;
+        asm volatile("" : "+v"(tid));   // keep lane-derived values inside the unit loop
+        const int lane = tid & 63, wave = tid >> 6, hl = lane >> 5, lr = lane & 31;
+        const int h = u % H, f0 = u / H * G, Gu = min(G, a.F - f0);
+        const int r0 = a.qoff[f0];   // the reference frame's token i sits at packed row r0 + i
+        stage_rows<DH, NT>(g, Ks, Vs, qkv, ld3, D, h, 0, r0, g.npad, N, tid);
+        int Tr = Tref;               // reference tiles not taken yet
+        int j = 1;
+        do {
+            // batch: frames j .. j2-1 of the group whose own rows fit in pcap (every frame's do:
+            // pcap >= N), staged after the reference rows
+            const int p0 = a.qoff[f0 + j];
+            int j2 = j;
+            while (j2 < Gu && a.qoff[f0 + j2 + 1] - p0 <= pcap) ++j2;
+            const int prow = a.qoff[f0 + j2] - p0;
+            if (prow > 0) stage_rows<DH, NT>(g, Ks, Vs, qkv, ld3, D, h, g.npad, p0, prow, prow, tid);
+            for (int e = tid; e < (j2 - j) * g.npad; e += NT) {
+                const int jj = j + e / g.npad, i = e % g.npad;
+                const int p = a.pos[(size_t)(f0 + jj) * N + min(i, N - 1)];
+                kmap[jj * g.npad + i] = (uint16_t)(p < r0 + N ? p - r0 : g.npad + p - p0);
+            }
+            lds_barrier();
+            // the batch's tiles, then reference tiles: as many as fill the last round of
+            // wavefronts, or all that are left after the last batch
+            int Tb = 0;
+            for (int jj = j; jj < j2; ++jj) Tb += (a.qoff[f0 + jj + 1] - a.qoff[f0 + jj] + 31) / 32;
+            const int extra = j2 >= Gu ? Tr : min(Tr, (UW - Tb % UW) % UW);
+            for (int t = wave; t < Tb + extra; t += UW) {
+                int jj = -1, tt = t;   // frame (index in the group; -1: the reference) and tile
+                if (t < Tb) {
+                    jj = j;
+                    for (int nt; tt >= (nt = (a.qoff[f0 + jj + 1] - a.qoff[f0 + jj] + 31) / 32); ++jj)
+                        tt -= nt;
+                } else {
+                    tt = Tref - Tr + (t - Tb);
+                }
+                const int f = jj < 0 ? f0 : f0 + jj;
+                const int q0 = a.qoff[f], q1 = a.qoff[f + 1];
+                const int myq = q0 + tt * 32 + lr;
+                const int qrow = myq < q1 ? myq : q1 - 1;
+                bf16x8 qf[KS];
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    qf[ks] = *(const bf16x8*)(qkv + (size_t)qrow * ld3 + h * DH + ks * 16 + hl * 8);
+                float m, l;
+                f32x16 o[DB];
+                if (jj < 0) {
+                    attend_tile<DH>(g, Ks, Vs, N, lane, qf, 0, 1, [](int k) { return k; }, m, l, o);
+                } else {
+                    const uint16_t* km = kmap + jj * g.npad;
+                    attend_tile<DH>(g, Ks, Vs, N, lane, qf, 0, 1, [=](int k) { return (int)km[k]; },
+                                    m, l, o);
+                }
+                if (myq < q1) store_row<DH>((uint16_t*)a.out + (size_t)myq * D + h * DH, lane, l, o);
+            }
+            Tr -= extra;
+            lds_barrier();   // the next batch (or unit) restages rows and maps
+            j = j2;
+        } while (j < Gu);
     }
 }
 
@@ -422,13 +584,30 @@ size_t f32_lds_bytes(int N, int dh) {
 template <int DH>
 void launch_bf16(const AttnArgs& a, hipStream_t s) {
     static bool raised = false;
-    const size_t merge = (size_t)AW * (2 + (DH + 31) / 32 * 32) * 32 * 4;
-    const size_t lds = std::max(Geo(a.N, DH).bytes(), merge);
     if (!raised) {  // allow more than the default dynamic LDS (gfx950 has 160 KiB per CU)
         (void)hipFuncSetAttribute((const void*)attn_mfma_k<DH>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if constexpr (DH == 64)
+            (void)hipFuncSetAttribute((const void*)attn_unit_k<DH>,
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         raised = true;
     }
+    // groups of several frames (head dim 64): per-unit blocks, one per compute unit, when the
+    // reference rows, the maps and at least one other frame's rows fit in LDS
+    if constexpr (DH == 64) {
+        if (a.G > 1 && a.cus > 0) {
+            const int pcap = unit_pcap(a.N, DH, a.G, 160 * 1024);
+            if (pcap >= a.N) {
+                const size_t lds = UnitGeo(a.N, DH, a.G, pcap).bytes();
+                const int units = (a.F + a.G - 1) / a.G * a.H;
+                hipLaunchKernelGGL(attn_unit_k<DH>, dim3(std::min(units, a.cus)), dim3(UW * 64),
+                                   lds, s, a, pcap);
+                return;
+            }
+        }
+    }
+    const size_t merge = (size_t)AW * (2 + (DH + 31) / 32 * 32) * 32 * 4;
+    const size_t lds = std::max(Geo(a.N, DH).bytes(), merge);
     // work items: (frame, head) pairs; with reuse, the slots of whole units on each of 8 XCDs
     const int items = a.G > 0 ? xcd_unit_grid((a.F + a.G - 1) / a.G * a.H, a.G) : a.F * a.H;
     static int per_cu = -1;
