@@ -40,15 +40,14 @@ typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ inline float gelu_erf(float v) { return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f)); }
 
-// GELU for outputs rounded to bf16: Phi(x) - 1/2 = x P(x^2) for |x| <= 4, P a degree-8
-// least-squares fit to the normal CDF on [0, 4] with 4 P(16) = 1/2 imposed (coefficients from
-// gelu_fit.py), so that past |x| = 4 the clamped evaluation gives x or 0.  |GELU error| <= 1.1e-5
-// for |x| <= 3 and <= 1.3e-4 everywhere (largest near |x| = 4): far below the bf16 step
-// (2^-8 relative) the result is rounded to.  GELU = 0.5 x + |x| (Phi(|x|) - 1/2): 13 VALU
-// operations, no transcendental.
+// GELU for outputs rounded to bf16: with y = x clamped to [-4, 4], Phi(x) = 1/2 + y P(y^2), P a
+// degree-8 least-squares fit to the normal CDF on [0, 4] with 4 P(16) = 1/2 imposed
+// (coefficients from gelu_fit.py), so that past |x| = 4 the result is x or 0.  GELU = x Phi(x):
+// 12 VALU operations, no transcendental.  |GELU error| <= 1.1e-5 for |x| <= 3 and <= 1.3e-4
+// everywhere (largest near |x| = 4): far below the bf16 step (2^-8 relative) of the result.
 __device__ inline float gelu_poly(float x) {
-    const float m = fminf(fabsf(x), 4.0f);
-    const float s = m * m;
+    const float y = __builtin_amdgcn_fmed3f(x, -4.0f, 4.0f);
+    const float s = y * y;
     float p = 9.151786967e-11f;
     p = fmaf(p, s, -7.699238580e-09f);
     p = fmaf(p, s, 2.898779599e-07f);
@@ -58,7 +57,7 @@ __device__ inline float gelu_poly(float x) {
     p = fmaf(p, s, 9.898823686e-03f);
     p = fmaf(p, s, -6.643372774e-02f);
     p = fmaf(p, s, 3.989303410e-01f);
-    return fmaf(fabsf(x), m * p, 0.5f * x);
+    return x * fmaf(y, p, 0.5f);
 }
 
 __device__ inline u32x2 pack_bf16x4(f32x4 v) {
@@ -99,8 +98,8 @@ __device__ inline void wave_lds_sync() {
 // Epilogue of one wavefront's (TI*32) x (TJ*32) sub-tile, staged through a wave-private LDS
 // slab so that global traffic is row-contiguous: for each 32-row slab the accumulators (lane l
 // holds row l%32, columns (r/4)*8 + (l/32)*4 + r%4 of each 32-column tile) are written to LDS,
-// then read back row-major -- each lane owns 4 fixed columns, so the bias is loaded once, and a
-// wavefront instruction covers 64/(TJ*8) whole row segments.  Row indices of every slab are
+// then read back row-major -- each lane owns 4 fixed columns, and a wavefront instruction covers
+// 64/(TJ*8) whole row segments.  The accumulators already hold the bias.  Row indices of every slab are
 // requested up front and the residual (or position) rows of slab i+1 are in flight while slab
 // i is combined and stored.  The caller has finished with the LDS ring.
 template <Epi E, int TI, int TJ>
@@ -116,7 +115,6 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
     const int c = lane % CPRW, rsub = lane / CPRW;
     const int col = col0 + c * 4;
     const size_t Nout = a.Nout;
-    const f32x4 bias = *(const f32x4*)(a.bias + col);
 
     auto row_of = [&](int i, int q) { return row0 + i * 32 + q * RPI + rsub; };
     // residual (or position) rows and output token rows of slab i; one slab ahead
@@ -163,7 +161,7 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
             const int r = q * RPI + rsub;
             const int row = row_of(i, q);
             if (row >= M) continue;
-            f32x4 v = *(const f32x4*)(slab + r * LDW + c * 4) + bias;
+            f32x4 v = *(const f32x4*)(slab + r * LDW + c * 4);   // bias included
             if constexpr (E == Epi::Qkv) {
                 *(u32x2*)((uint16_t*)a.out + (size_t)row * Nout + col) = pack_bf16x4(v);
             } else if constexpr (E == Epi::Fc1) {
@@ -299,13 +297,21 @@ __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int b
         for (int j = 0; j < TJ; ++j) xb[j] = *(const bf16x8*)(st + offB[j] + (c ^ swB[j]) * 8);
     };
 
+    // the accumulators start at the bias of their column (lane l, register r of MFMA tile j:
+    // column (r/4)*8 + (l/32)*4 + r%4 of the tile), so the epilogue does not add it
     f32x16 acc[TI][TJ];
 #pragma unroll
-    for (int i = 0; i < TI; ++i)
+    for (int j = 0; j < TJ; ++j) {
+        f32x16 b;
 #pragma unroll
-        for (int j = 0; j < TJ; ++j)
+        for (int g = 0; g < 4; ++g) {
+            const f32x4 v = *(const f32x4*)(a.bias + tn * BN + wn * WN + j * 32 + g * 8 + hl * 4);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+            for (int e = 0; e < 4; ++e) b[g * 4 + e] = v[e];
+        }
+#pragma unroll
+        for (int i = 0; i < TI; ++i) acc[i][j] = b;
+    }
 
     const int nk = K / BKD;
 #pragma unroll

@@ -23,13 +23,16 @@ def _coefficients():
 
 
 def _gelu_poly(x, coef):
+    """The kernel's operation order in float32: y = clamp(x, -4, 4), p = P(y^2) by Horner,
+    x * (y p + 1/2) (the last step one fused multiply-add, rounded once)."""
     x = np.asarray(x, dtype=np.float32)
-    m = np.minimum(np.abs(x), np.float32(4.0))
-    s = (m * m).astype(np.float32)
+    y = np.clip(x, np.float32(-4.0), np.float32(4.0))
+    s = (y * y).astype(np.float32)
     p = np.full_like(x, coef[0])
     for c in coef[1:]:
-        p = (p * s + c).astype(np.float32)
-    return (np.abs(x) * (m * p).astype(np.float32) + np.float32(0.5) * x).astype(np.float32)
+        p = (p.astype(np.float64) * s + c).astype(np.float32)   # fused: one rounding
+    u = (y.astype(np.float64) * p + 0.5).astype(np.float32)
+    return (x * u).astype(np.float32)
 
 
 def test_gelu_poly_error_bounds():
