@@ -95,13 +95,24 @@ __device__ inline void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Buffer descriptor over `bytes` bytes at p (raw, no stride): a load or store whose 32-bit byte
+// offset falls past `bytes` is dropped by the hardware range check.  Every GEMM operand and
+// output of the bf16 path is below 2^32 bytes (rows, padding included, are checked at handle
+// creation), so offsets are plain 32-bit products and need no 64-bit address arithmetic.
+__device__ inline __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+constexpr uint32_t BUF_ANY = 0xFFFFFFF0u;   // records of a descriptor whose offsets are all valid
+
 // Epilogue of one wavefront's (TI*32) x (TJ*32) sub-tile, staged through a wave-private LDS
 // slab so that global traffic is row-contiguous: for each 32-row slab the accumulators (lane l
 // holds row l%32, columns (r/4)*8 + (l/32)*4 + r%4 of each 32-column tile) are written to LDS,
 // then read back row-major -- each lane owns 4 fixed columns, and a wavefront instruction covers
-// 64/(TJ*8) whole row segments.  The accumulators already hold the bias.  Row indices of every slab are
-// requested up front and the residual (or position) rows of slab i+1 are in flight while slab
-// i is combined and stored.  The caller has finished with the LDS ring.
+// 64/(TJ*8) whole row segments.  The accumulators already hold the bias.  Row indices of every
+// slab are requested up front and the residual (or position) rows of slab i+1 are in flight
+// while slab i is combined and stored.  Stores go through buffer descriptors: rows past M in
+// the tile tail get an offset past the descriptor and are dropped.  The caller has finished
+// with the LDS ring.
 template <Epi E, int TI, int TJ>
 __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], float* slab, int row0,
                                     int col0, int M, int lane) {
@@ -111,42 +122,55 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
     constexpr int RPI = 64 / CPRW;       // rows per wavefront instruction
     constexpr int NQ = 32 / RPI;         // instructions per 32-row slab
     constexpr bool LOADS = E == Epi::OProj || E == Epi::Fc2 || E == Epi::Patch;
+    constexpr bool SCATTER = E == Epi::Fc2 || E == Epi::Patch;   // output rows are token rows
+    constexpr uint32_t ESZ = (E == Epi::Qkv || E == Epi::Fc1) ? 2 : 4;   // output element bytes
     const int lr = lane & 31, hl = lane >> 5;
     const int c = lane % CPRW, rsub = lane / CPRW;
-    const int col = col0 + c * 4;
-    const size_t Nout = a.Nout;
+    const uint32_t col = col0 + c * 4;
+    const uint32_t Nout = a.Nout;
+    // packed-row outputs end at row M; token-row outputs drop tail rows by their offset
+    const auto rout = buf_rsrc(a.out, SCATTER ? BUF_ANY : (uint32_t)M * Nout * ESZ);
+    const auto rres = buf_rsrc(E == Epi::Patch ? (const void*)a.pos : (const void*)a.resid, BUF_ANY);
 
     auto row_of = [&](int i, int q) { return row0 + i * 32 + q * RPI + rsub; };
-    // residual (or position) rows and output token rows of slab i; one slab ahead
+    // residual (or position) rows and output offsets of slab i; one slab ahead
     f32x4 extra[2][NQ];
-    int trow[2][NQ];
-    auto fetch = [&](int i, f32x4 (&dst)[NQ], int (&tr)[NQ]) {
+    uint32_t ooff[2][NQ];
+    auto fetch = [&](int i, f32x4 (&dst)[NQ], uint32_t (&oo)[NQ]) {
+        int tr[NQ];
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int row = row_of(i, q);
             const int r = row < M ? row : M - 1;           // a valid row for the tile tail
             if constexpr (E == Epi::OProj || E == Epi::Fc2) tr[q] = a.idx[r];
             else if constexpr (E == Epi::Patch) tr[q] = (r / a.P) * a.N + 1 + r % a.P;
-            else tr[q] = r;
+            else tr[q] = row;
+        }
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int row = row_of(i, q);
+            if constexpr (SCATTER)
+                oo[q] = row < M ? ((uint32_t)tr[q] * Nout + col) * ESZ : BUF_ANY;
+            else
+                oo[q] = ((uint32_t)row * Nout + col) * ESZ;
         }
         if constexpr (LOADS) {
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
                 const int row = row_of(i, q);
-                const int r = row < M ? row : M - 1;
-                if constexpr (E == Epi::OProj)
-                    dst[q] = *(const f32x4*)(a.resid + (size_t)tr[q] * Nout + col);
-                else if constexpr (E == Epi::Fc2)
-                    dst[q] = *(const f32x4*)(a.resid + (size_t)r * Nout + col);
-                else
-                    dst[q] = *(const f32x4*)(a.pos + (size_t)(1 + r % a.P) * Nout + col);
+                const uint32_t r = row < M ? row : M - 1;
+                uint32_t off;
+                if constexpr (E == Epi::OProj) off = ((uint32_t)tr[q] * Nout + col) * 4;
+                else if constexpr (E == Epi::Fc2) off = (r * Nout + col) * 4;
+                else off = ((1 + r % a.P) * Nout + col) * 4;
+                dst[q] = __builtin_amdgcn_raw_buffer_load_b128(rres, (int)off, 0, 0);
             }
         }
     };
-    fetch(0, extra[0], trow[0]);
+    fetch(0, extra[0], ooff[0]);
 #pragma unroll
     for (int i = 0; i < TI; ++i) {
-        if (i + 1 < TI) fetch(i + 1, extra[(i + 1) & 1], trow[(i + 1) & 1]);
+        if (i + 1 < TI) fetch(i + 1, extra[(i + 1) & 1], ooff[(i + 1) & 1]);
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
 #pragma unroll
@@ -159,18 +183,15 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int r = q * RPI + rsub;
-            const int row = row_of(i, q);
-            if (row >= M) continue;
-            f32x4 v = *(const f32x4*)(slab + r * LDW + c * 4);   // bias included
+            const f32x4 v = *(const f32x4*)(slab + r * LDW + c * 4);   // bias included
+            const int off = (int)ooff[i & 1][q];
             if constexpr (E == Epi::Qkv) {
-                *(u32x2*)((uint16_t*)a.out + (size_t)row * Nout + col) = pack_bf16x4(v);
+                __builtin_amdgcn_raw_buffer_store_b64(pack_bf16x4(v), rout, off, 0, 0);
             } else if constexpr (E == Epi::Fc1) {
-                f32x4 gl = {gelu_poly(v[0]), gelu_poly(v[1]), gelu_poly(v[2]), gelu_poly(v[3])};
-                *(u32x2*)((uint16_t*)a.out + (size_t)row * Nout + col) = pack_bf16x4(gl);
-            } else if constexpr (E == Epi::OProj) {
-                *(f32x4*)((float*)a.out + (size_t)row * Nout + col) = v + extra[i & 1][q];
-            } else {   // Fc2 and Patch: the output lives in a token row
-                *(f32x4*)((float*)a.out + (size_t)trow[i & 1][q] * Nout + col) = v + extra[i & 1][q];
+                const f32x4 gl = {gelu_poly(v[0]), gelu_poly(v[1]), gelu_poly(v[2]), gelu_poly(v[3])};
+                __builtin_amdgcn_raw_buffer_store_b64(pack_bf16x4(gl), rout, off, 0, 0);
+            } else {
+                __builtin_amdgcn_raw_buffer_store_b128(v + extra[i & 1][q], rout, off, 0, 0);
             }
         }
         wave_lds_sync();   // the slab is rewritten by the next 32-row slab
