@@ -104,8 +104,8 @@ def measured_traffic(stage):
     return r["traffic_bytes_per_launch"] if r.get("source_sha256") == sha else None
 
 
-STAGE_KERNEL = {"qkv": "Epi)1", "oproj": "Epi)2", "fc1": "Epi)3", "fc2": "Epi)4",
-                "attn": "attn_mfma_k"}
+STAGE_KERNEL = {"qkv": ("Epi)1",), "oproj": ("Epi)2",), "fc1": ("Epi)3",), "fc2": ("Epi)4",),
+                "attn": ("attn_unit_k", "attn_mfma_k")}   # name fragments of each stage's kernels
 
 
 def traffic_record(fetch_csv, write_csv, bench_json, cmds):
@@ -138,7 +138,8 @@ def traffic_record(fetch_csv, write_csv, bench_json, cmds):
         key, n = STAGE_KERNEL[stage], info["launches"]
 
         def timed(rs, cut):
-            ks = [r for r in rs if key in r["Kernel_Name"] and int(r["Dispatch_Id"]) < cut]
+            ks = [r for r in rs if any(k in r["Kernel_Name"] for k in key)
+                  and int(r["Dispatch_Id"]) < cut]
             return ks[-n:]
         fk = timed(fr, int(fcopy["Dispatch_Id"]))
         wk = timed(wr, int(wcopy["Dispatch_Id"]))
