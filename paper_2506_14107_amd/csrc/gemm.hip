@@ -5,7 +5,7 @@
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16 with fp32 accumulation.
 //   * Block tile BM x BN, 4 wavefronts in 2 x 2, each owning (BM/2) x (BN/2) of 32 x 32 tiles.
-//   * k-slices of BK travel global -> LDS with global_load_lds_dwordx4 (no staging registers)
+//   * k-slices of BK travel global -> LDS with buffer_load_dwordx4 ... lds (no staging registers)
 //     through a ring of S stages: S-1 slices are in flight while one is consumed.  One
 //     wavefront instruction writes 1 KiB of LDS (lane i at base + 16 i).  LDS rows are BK*2
 //     bytes without padding; lane i fetches the global chunk that belongs at its slot: chunk
@@ -267,33 +267,39 @@ __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int b
     const int lr = lane & 31, hl = lane >> 5;
     const int K = a.K;
 
+    // this lane's DMA chunks: 32-bit byte offsets into the A and weight buffers (both below 2^32
+    // bytes); the k-slice advance rides in the scalar offset of buffer_load ... lds
     const int lrow = lane / CPR, lslot = lane % CPR;
-    const uint16_t* srcA[LA];
-    const uint16_t* srcB[LB];
+    uint32_t goffA[LA], goffB[LB];
 #pragma unroll
     for (int t = 0; t < LA; ++t) {
         const int r = (wave * LA + t) * RPI + lrow;
         const int c = lslot ^ ((r >> SH) & (CPR - 1));
         const int grow = m0 + tm * BM + r;
         const int arow = a.a_idx ? (grow < M ? a.a_idx[grow] : 0) : grow;   // gathered A rows
-        srcA[t] = (const uint16_t*)a.A + (size_t)arow * K + c * 8;
+        goffA[t] = ((uint32_t)arow * K + c * 8) * 2;
     }
 #pragma unroll
     for (int t = 0; t < LB; ++t) {
         const int r = (wave * LB + t) * RPI + lrow;
         const int c = lslot ^ ((r >> SH) & (CPR - 1));
-        srcB[t] = (const uint16_t*)a.W + (size_t)(tn * BN + r) * K + c * 8;
+        goffB[t] = ((uint32_t)(tn * BN + r) * K + c * 8) * 2;
     }
+    const auto rA = buf_rsrc(a.A, BUF_ANY);
+    const auto rW = buf_rsrc(a.W, BUF_ANY);
     auto issue = [&](int kt) {
         uint16_t* st = sm + (kt % S) * STAGE;
+        const int soff = kt * BKD * 2;
 #pragma unroll
         for (int t = 0; t < LA; ++t)
-            __builtin_amdgcn_global_load_lds((const void*)(srcA[t] + kt * BKD),
-                (__attribute__((address_space(3))) void*)(st + (wave * LA + t) * RPI * BKD), 16, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rA,
+                (__attribute__((address_space(3))) void*)(st + (wave * LA + t) * RPI * BKD), 16,
+                (int)goffA[t], soff, 0, 0);
 #pragma unroll
         for (int t = 0; t < LB; ++t)
-            __builtin_amdgcn_global_load_lds((const void*)(srcB[t] + kt * BKD),
-                (__attribute__((address_space(3))) void*)(st + BM * BKD + (wave * LB + t) * RPI * BKD), 16, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rW,
+                (__attribute__((address_space(3))) void*)(st + BM * BKD + (wave * LB + t) * RPI * BKD), 16,
+                (int)goffB[t], soff, 0, 0);
     };
     // per-lane LDS element offsets of the fragments (row part; the chunk is XORed per k-step)
     int offA[TI], offB[TJ], swA[TI], swB[TJ];
