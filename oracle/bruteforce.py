@@ -4,7 +4,9 @@ It follows the same definition as the vectorised oracle (Section 3 of the
 paper: decision by the threshold gate on the cosine similarity cue, token
 filtration, recompute of C, reconstruction from the reference for R) but
 walks frames, layers, tokens, heads and keys one at a time with scalar
-softmax arithmetic.  It shares no helper with the vectorised oracle.
+softmax arithmetic.  It shares no helper with the vectorised oracle.  With ``cfg["restore"]``
+a reused token's output adds the restoration MLP of its input difference
+to the reference (hidden 128, GELU; Section 3.3), evaluated row by row.
 """
 import math
 
@@ -32,6 +34,8 @@ def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
         layers.append([nxt(D), nxt(D), nxt(3 * D, D), nxt(3 * D), nxt(D, D), nxt(D),
                        nxt(D), nxt(D), nxt(Dm, D), nxt(Dm), nxt(D, Dm), nxt(D)])
     lnfg, lnfb = nxt(D), nxt(D)
+    restore = bool(cfg.get("restore"))
+    rest = [[nxt(128, D), nxt(128), nxt(D, 128), nxt(D)] for _ in range(L)] if restore else None
 
     def norm(v, gamma, beta):
         mean = sum(v) / len(v)
@@ -88,6 +92,11 @@ def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
             for i in range(N):
                 if reuse[i]:
                     Y[f, i] = Y[ref, i]
+                    if restore:
+                        Wr1, br1, Wr2, br2 = rest[l]
+                        hid = Wr1 @ (X[f, i] - X[ref, i]) + br1
+                        hid = np.array([0.5 * t * (1.0 + math.erf(t / math.sqrt(2.0))) for t in hid])
+                        Y[f, i] = Y[f, i] + (Wr2 @ hid + br2)
                     continue
                 o = np.zeros(D)
                 for h in range(H):

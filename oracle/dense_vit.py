@@ -27,7 +27,9 @@ def _read_layout(blob, cfg):
         cnt = int(np.prod(sh))
         out[nm] = flat[pos:pos + cnt].reshape(sh)
         pos += cnt
-    assert pos == flat.size, "weight blob size does not match the configuration"
+    # a restoration section (cfg["restore"]) may follow; the dense forward has no reused rows
+    extra = L * (128 * D + 128 + D * 128 + D) if cfg.get("restore") else 0
+    assert pos + extra == flat.size, "weight blob size does not match the configuration"
     return out
 
 

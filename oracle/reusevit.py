@@ -25,8 +25,14 @@ What it computes, following the paper's model description (Section 3):
   recomputed query sees all N keys/values of its frame: its own fresh K/V for
   tokens in C and the reference frame's K/V for tokens in R.
 * Token reconstruction (Section 3.3): rows of C take the recomputed output,
-  rows of R copy the reference frame's layer output.  (No restoration MLP:
-  the learned restoration layer needs trained weights.)
+  rows of R copy the reference frame's layer output.
+* Restoration layer (Section 3.3, restoration equations), when the
+  configuration enables it (``cfg["restore"]``): a reused row becomes the
+  reference's layer output plus a two-layer MLP (hidden 128, GELU) of the
+  difference between its own layer input and the reference's,
+  y_f[i] = y_r[i] + W_r2 GELU(W_r1 (x_f[i] - x_r[i]) + b_r1) + b_r2.  The
+  keys and values of reused tokens stay the reference's.  The restored rows
+  are the next layer's input (so a token reused once may be recomputed later).
 
 Modes: gate mode (``tau``) and mask-injection mode (``masks`` given; class
 token and reference-frame entries are forced to 0).  ``tau = -inf`` turns
@@ -42,6 +48,7 @@ from scipy.special import erf
 
 LN_EPS = 1e-5
 COS_EPS = 1e-8
+RESTORE_HIDDEN = 128   # hidden width of the restoration MLP (Section 3.3)
 
 
 def unpack_blob(blob, cfg, dtype=np.float64):
@@ -72,6 +79,11 @@ def unpack_blob(blob, cfg, dtype=np.float64):
         lay["W_2"], lay["b_2"] = take(D, Dm), take(D)
         W["layers"].append(lay)
     W["lnf_g"], W["lnf_b"] = take(D), take(D)
+    if cfg.get("restore"):
+        R = RESTORE_HIDDEN
+        for lay in W["layers"]:
+            lay["W_r1"], lay["b_r1"] = take(R, D), take(R)
+            lay["W_r2"], lay["b_r2"] = take(D, R), take(D)
     if off != blob.size:
         raise ValueError(f"weight blob has {blob.size} floats, layout needs {off}")
     return W
@@ -146,6 +158,11 @@ def qkv_rows(x_rows, P):
     return t[:, :D], t[:, D:2 * D], t[:, 2 * D:]
 
 
+def restore_rows(dx, P):
+    """Restoration MLP (Section 3.3) of the input differences dx [n, D] of reused rows."""
+    return gelu(dx @ P["W_r1"].T + P["b_r1"]) @ P["W_r2"].T + P["b_r2"]
+
+
 def finish_rows(x_rows, o_rows, P):
     """Output projection + residual, then the MLP sub-layer + residual."""
     z = x_rows + o_rows @ P["W_o"].T + P["b_o"]
@@ -201,6 +218,9 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
                 y_c = finish_rows(x[f, C], attention(q_c, k_t, v_t, H), P)
                 y[f] = y[r]                                   # reused rows: reference output
                 y[f, C] = y_c                                 # recomputed rows
+                if cfg.get("restore"):                        # ... calibrated by the restoration MLP
+                    Rr = np.flatnonzero(m)
+                    y[f, Rr] += restore_rows(x[f, Rr] - x[r, Rr], P)
         x = y
         if return_layers:
             hist.append(x.copy())

@@ -10,6 +10,8 @@ scene cuts and Gaussian pixel noise.
 from dataclasses import dataclass, field
 from typing import Optional, Tuple
 
+RESTORE_HIDDEN = 128   # hidden width of the restoration MLP (the paper's two-layer MLP, size 128)
+
 
 @dataclass(frozen=True)
 class ModelConfig:
@@ -20,6 +22,7 @@ class ModelConfig:
     heads: int
     mlp: int
     dtype: str  # "f32" or "bf16": arithmetic type of the GEMM/attention operands
+    restore: bool = False   # per-layer restoration MLP on reused tokens (hidden RESTORE_HIDDEN)
 
     @property
     def n_patches(self) -> int:
@@ -35,7 +38,8 @@ class ModelConfig:
 
     def as_dict(self):
         return dict(image_size=self.image_size, patch=self.patch, depth=self.depth,
-                    width=self.width, heads=self.heads, mlp=self.mlp, dtype=self.dtype)
+                    width=self.width, heads=self.heads, mlp=self.mlp, dtype=self.dtype,
+                    restore=self.restore)
 
 
 @dataclass(frozen=True)

@@ -6,9 +6,12 @@ Blob layout (little-endian float32, tensors back to back, row-major):
         ln1_g [D], ln1_b [D], W_qkv [3D,D], b_qkv [3D], W_o [D,D], b_o [D],
         ln2_g [D], ln2_b [D], W_1 [Dm,D], b_1 [Dm], W_2 [D,Dm], b_2 [D]
     lnf_g [D], lnf_b [D]
+    with the restoration MLP (ModelConfig.restore), then per layer l = 0..L-1:
+        W_r1 [R,D], b_r1 [R], W_r2 [D,R], b_r2 [D]        (R = RESTORE_HIDDEN = 128)
 Rows of W_qkv are Q, then K, then V; within each, heads are contiguous slices
 of D/H rows.  Linear layers map x -> x @ W.T + b.
 
+The restoration section comes last, so the other weights of a seed do not depend on it.
 Matrices, biases, the class token and the position table are drawn from
 N(0, 0.02); LayerNorm gains are 1 and shifts 0 unless ``perturb_ln`` is set,
 in which case gains are 1 + N(0, 0.02) and shifts N(0, 0.02) so that the
@@ -18,7 +21,7 @@ blob holds exactly the weights a bf16 kernel sees.
 """
 import numpy as np
 
-from .configs import ModelConfig
+from .configs import RESTORE_HIDDEN, ModelConfig
 
 
 def weight_layout(m: ModelConfig):
@@ -35,6 +38,11 @@ def weight_layout(m: ModelConfig):
             (f"l{l}.W_2", (D, Dm)), (f"l{l}.b_2", (D,)),
         ]
     out += [("lnf_g", (D,)), ("lnf_b", (D,))]
+    if m.restore:
+        Rh = RESTORE_HIDDEN
+        for l in range(m.depth):
+            out += [(f"l{l}.W_r1", (Rh, D)), (f"l{l}.b_r1", (Rh,)),
+                    (f"l{l}.W_r2", (D, Rh)), (f"l{l}.b_r2", (D,))]
     return out
 
 

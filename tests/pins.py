@@ -23,6 +23,12 @@ What pins what:
   cosine       closed-form cosines; equal rows give exactly 1; tie cos == tau reuses
   partial      a short last group still has its first frame as reference
   rate         reuse-rate denominator: non-reference frames x N tokens x L layers
+  restoration (the restoration MLP on reused rows, when the configuration enables it):
+  restore_zero a zero output layer leaves every row and decision unchanged (bitwise)
+  restore_brute == the per-token loop implementation, gate and injection modes
+  restore_one  one injected reused token: reference output + the MLP (torch Linear/GELU) of its
+               input difference; every other row as without restoration
+  restore_static identical frames at tau=+inf: closed forms at layers 0 and 1
 """
 import numpy as np
 
@@ -37,6 +43,9 @@ from . import torch_ref
 M_A = ModelConfig(32, 16, 2, 8, 2, 16, "f32")       # N=5, D=8, L=2
 M_B = ModelConfig(48, 16, 2, 16, 2, 32, "f32")      # N=10, D=16, L=2
 M_1 = ModelConfig(48, 16, 1, 16, 2, 32, "f32")      # one layer
+M_AR = ModelConfig(32, 16, 2, 8, 2, 16, "f32", restore=True)     # M_A with restoration
+M_BR = ModelConfig(48, 16, 2, 16, 2, 32, "f32", restore=True)    # M_B with restoration
+M_1R = ModelConfig(48, 16, 1, 16, 2, 32, "f32", restore=True)    # M_1 with restoration
 
 
 def weights(m, seed=7, perturb=True):
@@ -280,6 +289,81 @@ def pin_rate(ora):
     assert abs(ora.reuse_rate(mk, 4) - 7 / 40) < 1e-15
 
 
+def _without_restoration(w, m):
+    """The blob of the same weights and the model without the restoration section."""
+    base = ModelConfig(m.image_size, m.patch, m.depth, m.width, m.heads, m.mlp, m.dtype)
+    return base, synth.pack_weights(w, base)
+
+
+def pin_restore_zero(ora):
+    m = M_BR
+    w, _ = weights(m, 21)
+    for l in range(m.depth):
+        w[f"l{l}.W_r2"][...] = 0.0
+        w[f"l{l}.b_r2"][...] = 0.0
+    blob = synth.pack_weights(w, m)
+    base, blob0 = _without_restoration(w, m)
+    fr = mixed_frames(m, 8, 4, seed=21)
+    for tau in (0.5, 0.9, np.inf):
+        a = ora.encode(fr, blob, m.as_dict(), 4, tau=tau)
+        b = ora.encode(fr, blob0, base.as_dict(), 4, tau=tau)
+        assert np.array_equal(a["masks"], b["masks"]), f"masks differ at tau={tau}"
+        assert np.array_equal(a["tokens"], b["tokens"]), f"tokens differ at tau={tau}"
+
+
+def pin_restore_brute(ora):
+    for m, G in ((M_AR, 4), (M_BR, 3)):
+        _, blob = weights(m, 24)
+        fr = mixed_frames(m, 7, G, seed=24)
+        cfg = m.as_dict()
+        for tau in (0.3, 0.8, 0.97, np.inf):
+            r = ora.encode(fr, blob, cfg, G, tau=tau)
+            b = encode_bruteforce(fr, blob, cfg, G, tau=tau)
+            assert np.array_equal(r["masks"], b["masks"]), f"masks differ at tau={tau}"
+            _close(r["tokens"], b["tokens"], 1e-12, f"tokens tau={tau}")
+        mk = (np.random.default_rng(25).random((7, m.depth, m.n_tokens)) < 0.5).astype(np.uint8)
+        r = ora.encode(fr, blob, cfg, G, masks=mk)
+        b = encode_bruteforce(fr, blob, cfg, G, masks=mk)
+        _close(r["tokens"], b["tokens"], 1e-12, "tokens (injected)")
+
+
+def pin_restore_one(ora):
+    m = M_1R
+    w, blob = weights(m, 22)
+    base, blob0 = _without_restoration(w, m)
+    fr = mixed_frames(m, 2, 2, seed=22)
+    j = 4
+    mk = np.zeros((2, 1, m.n_tokens), np.uint8)
+    mk[1, 0, j] = 1
+    r = ora.encode(fr, blob, m.as_dict(), 2, masks=mk, return_layers=True)
+    r0 = ora.encode(fr, blob0, base.as_dict(), 2, masks=mk, return_layers=True)
+    x0 = torch_ref.embed(fr, w, m).numpy()
+    dx = (x0[1, j] - x0[0, j])[None]
+    want = r0["layers"][1][0, j] + torch_ref.restoration(dx, w, 0)[0]
+    _close(r["layers"][1][1, j], want, 1e-12, "restored row")
+    y, y0 = r["layers"][1].copy(), r0["layers"][1].copy()
+    y[1, j] = y0[1, j] = 0.0
+    assert np.array_equal(y, y0), "restoration must touch only the reused row"
+
+
+def pin_restore_static(ora):
+    m = M_BR
+    w, blob = weights(m, 23)
+    fr = np.repeat(mixed_frames(m, 1, 1, seed=23), 3, axis=0)
+    r = ora.encode(fr, blob, m.as_dict(), 3, tau=np.inf, return_layers=True)
+    D = m.width
+    c0 = torch_ref.restoration(np.zeros((1, D)), w, 0)[0]      # layer 0: equal inputs
+    x1, x2 = r["layers"][1], r["layers"][2]
+    for f in (1, 2):
+        _close(x1[f, 1:] - x1[0, 1:], np.broadcast_to(c0, x1[0, 1:].shape), 1e-12,
+               f"layer 0 restored rows, frame {f}")
+        _close(x1[f, 0], x1[0, 0], 1e-12, f"layer 0 class token, frame {f}")
+        d = x1[f, 1:] - x1[0, 1:]                               # layer 1: input difference c0
+        _close(x2[f, 1:] - x2[0, 1:], torch_ref.restoration(d, w, 1), 1e-12,
+               f"layer 1 restored rows, frame {f}")
+
+
 ALL_PINS = [pin_library, pin_dense_vit, pin_bruteforce, pin_copy, pin_ref_dense, pin_monotone,
             pin_static, pin_g1, pin_groups, pin_inject_one, pin_extremes, pin_star, pin_cosine,
-            pin_partial, pin_rate]
+            pin_partial, pin_rate, pin_restore_zero, pin_restore_brute, pin_restore_one,
+            pin_restore_static]

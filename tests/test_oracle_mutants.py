@@ -42,6 +42,12 @@ MUTANTS = [
      "return np.zeros(cos.shape, dtype=bool)"),
     ("rate_counts_references", "nonref = [f for f in range(F) if f % group_size != 0]",
      "nonref = list(range(F))"),
+    ("restore_difference_flipped", "x[f, Rr] - x[r, Rr]", "x[r, Rr] - x[f, Rr]"),
+    ("restore_output_bias_dropped", '@ P["W_r2"].T + P["b_r2"]', '@ P["W_r2"].T'),
+    ("restore_relu", 'gelu(dx @ P["W_r1"].T + P["b_r1"])',
+     'np.maximum(dx @ P["W_r1"].T + P["b_r1"], 0.0)'),
+    ("restore_output_difference", "x[f, Rr] - x[r, Rr]", "y[f, Rr] - y[r, Rr]"),
+    ("restore_all_rows", "Rr = np.flatnonzero(m)", "Rr = np.arange(m.size)"),
 ]
 
 

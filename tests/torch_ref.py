@@ -68,3 +68,17 @@ def layer_with_substituted_kv(x_f, x_ref, j, w, l, m):
         z = xf + a
         y = z + lay.linear2(torch.nn.functional.gelu(lay.linear1(lay.norm2(z))))
     return y[0].numpy()
+
+
+def restoration(dx, w, l):
+    """Restoration MLP of layer l (two torch Linear layers, exact erf GELU) applied to the input
+    differences dx [n, D] (numpy); returns numpy float64."""
+    t = lambda a: torch.tensor(np.asarray(a, dtype=np.float64))  # noqa: E731
+    l1 = torch.nn.Linear(w[f"l{l}.W_r1"].shape[1], w[f"l{l}.W_r1"].shape[0], dtype=torch.float64)
+    l2 = torch.nn.Linear(w[f"l{l}.W_r2"].shape[1], w[f"l{l}.W_r2"].shape[0], dtype=torch.float64)
+    with torch.no_grad():
+        l1.weight.copy_(t(w[f"l{l}.W_r1"]))
+        l1.bias.copy_(t(w[f"l{l}.b_r1"]))
+        l2.weight.copy_(t(w[f"l{l}.W_r2"]))
+        l2.bias.copy_(t(w[f"l{l}.b_r2"]))
+        return l2(torch.nn.functional.gelu(l1(t(dx)), approximate="none")).numpy()
