@@ -25,7 +25,10 @@
  *     for recomputed tokens, the reference's rows for reused ones --, output
  *     projection, MLP) on those rows only.
  *   - Token reconstruction (Section 3.3): reused tokens take the reference's
- *     layer output.  Layers run over the whole batch one at a time
+ *     layer output -- with DV_FLAG_RESTORE calibrated by the restoration
+ *     layer (Section 3.3): plus a two-layer MLP (hidden 128, GELU) of the
+ *     difference between the token's layer input and the reference's; reused
+ *     keys and values stay the reference's.  Layers run over the whole batch one at a time
  *     (layer-wise scheduling, Section 5.1); the reference's per-layer state
  *     lives in the batch buffers for one layer step only (cached memory
  *     compaction, Section 5.2).
@@ -76,8 +79,17 @@ typedef struct dv_config {
     int mlp;               /* Dm: MLP hidden width */
     int dtype;             /* DV_F32 or DV_BF16 */
     int max_batch_frames;  /* frames per internal batch (rounded down to whole groups per call) */
-    unsigned flags;        /* reserved, must be 0 */
+    unsigned flags;        /* 0 or DV_FLAG_RESTORE; other bits reserved (must be 0) */
 } dv_config;
+
+/* Restoration layer on reused tokens (Section 3.3): after each layer, a reused token i of a
+ * non-reference frame f becomes  y_ref[i] + W_r2 GELU(W_r1 (x_f[i] - x_ref[i]) + b_r1) + b_r2,
+ * where x is the layer input and y_ref the reference frame's layer output.  The restored row
+ * is the next layer's input, so a token reused at one layer may be recomputed at a later one
+ * (in gate mode every token is gated at every layer).  Reused keys and values stay the
+ * reference's.  The weights follow the base blob (see dv_weights_floats). */
+#define DV_FLAG_RESTORE 1u
+#define DV_RESTORE_HIDDEN 128   /* hidden width of the restoration MLP */
 
 typedef struct dv_handle dv_handle;
 
@@ -87,6 +99,8 @@ typedef struct dv_handle dv_handle;
  *   per layer: ln1_g [D], ln1_b [D], W_qkv [3D,D], b_qkv [3D], W_o [D,D], b_o [D],
  *              ln2_g [D], ln2_b [D], W_1 [Dm,D], b_1 [Dm], W_2 [D,Dm], b_2 [D]
  *   lnf_g [D], lnf_b [D]
+ *   with DV_FLAG_RESTORE, then per layer: W_r1 [R,D], b_r1 [R], W_r2 [D,R], b_r2 [D]
+ *   (R = DV_RESTORE_HIDDEN)
  * Linear layers map x -> x W^T + b.  W_qkv rows: Q, then K, then V; heads are
  * contiguous slices of D/H rows within each.  LayerNorm eps is 1e-5. */
 size_t dv_weights_floats(const dv_config* cfg);
@@ -96,7 +110,7 @@ size_t dv_weights_floats(const dv_config* cfg);
  * rounds the matrices to bf16 (nearest, ties to even) when dtype is
  * DV_BF16, and allocates the workspace for max_batch_frames frames.
  * Synchronous.  Errors: DV_EINVAL (null pointer, wrong blob size, sizes < 1),
- * DV_EUNSUPPORTED (S % p, D % H, head dim, flags), DV_ENOMEM, DV_EHIP.
+ * DV_EUNSUPPORTED (S % p, D % H, head dim, unknown flag bits), DV_ENOMEM, DV_EHIP.
  * On error *out is set to NULL. */
 int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, dv_handle** out);
 
@@ -173,8 +187,9 @@ int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size,
 #define DV_STAGE_FC2 9
 #define DV_STAGE_MERGE 10
 #define DV_STAGE_FINAL 11
-#define DV_NUM_STAGES 12
-#define DV_PROFILE_ALL 0xFFF
+#define DV_STAGE_RESTORE 12   /* the two restoration GEMMs (DV_FLAG_RESTORE) */
+#define DV_NUM_STAGES 13
+#define DV_PROFILE_ALL 0x1FFF
 int dv_profile(dv_handle* h, unsigned stage_mask);
 /* total_ms: summed event time of the stage's launches; launches: how many. */
 int dv_profile_read(dv_handle* h, int stage, double* total_ms, long long* launches);

@@ -10,6 +10,9 @@
 //     -> out-proj GEMM (+bias, +gathered residual) -> LN2 -> FC1 GEMM (+bias, GELU)
 //     -> FC2 GEMM (+bias, +residual) written straight back into the token rows
 //     [injection mode: copy the reference's new row into every reused row]
+//     [restoration: the gate also writes x_f - x_ref of every reused token, the compaction the
+//      reused-token list; a D -> 128 GEMM (+bias, GELU) on those rows runs before QKV and a
+//      128 -> D GEMM (+bias, + the reference token's new row) after FC2 writes the reused rows]
 //   final LayerNorm of the class tokens.
 // Nothing is read back to the host inside an encode call.
 //
@@ -59,12 +62,17 @@ size_t round_up(size_t v, size_t m) { return (v + m - 1) / m * m; }
 struct LayerW {
     const float *ln1_g, *ln1_b, *b_qkv, *b_o, *ln2_g, *ln2_b, *b_1, *b_2;
     const void *W_qkv, *W_o, *W_1, *W_2;
+    const void *W_r1, *W_r2;      // restoration MLP (DV_FLAG_RESTORE), else null
+    const float *b_r1, *b_r2;
 };
 
 struct Dims {
     int S, p, L, D, H, Dm, N, P, Kp, B;
     bool bf16;
+    bool restore;   // DV_FLAG_RESTORE
 };
+
+constexpr int RH = DV_RESTORE_HIDDEN;
 
 // validates a configuration; fills dims
 int check_config(const dv_config* c, Dims* d) {
@@ -73,7 +81,7 @@ int check_config(const dv_config* c, Dims* d) {
         c->mlp < 1 || c->max_batch_frames < 1)
         return fail(DV_EINVAL, "config sizes must be >= 1");
     if (c->dtype != DV_F32 && c->dtype != DV_BF16) return fail(DV_EINVAL, "unknown dtype %d", c->dtype);
-    if (c->flags != 0) return fail(DV_EUNSUPPORTED, "flags must be 0");
+    if (c->flags & ~DV_FLAG_RESTORE) return fail(DV_EUNSUPPORTED, "unknown flag bits 0x%x", c->flags);
     if (c->image_size % c->patch) return fail(DV_EUNSUPPORTED, "image_size %% patch != 0");
     if (c->width % c->heads) return fail(DV_EUNSUPPORTED, "width %% heads != 0");
     const int dh = c->width / c->heads;
@@ -95,6 +103,7 @@ int check_config(const dv_config* c, Dims* d) {
     d->Kp = (int)round_up((size_t)3 * c->patch * c->patch, 64);
     d->B = c->max_batch_frames;
     d->bf16 = bf;
+    d->restore = (c->flags & DV_FLAG_RESTORE) != 0;
     if (!attention_supported(bf, d->N, dh))
         return fail(DV_EUNSUPPORTED, "attention for N=%d tokens, head dim %d is not supported "
                     "(bf16: head dim 64/80/96/128; keys and values of a head must fit in LDS)", d->N, dh);
@@ -108,7 +117,8 @@ int check_config(const dv_config* c, Dims* d) {
 size_t blob_floats(const Dims& d) {
     const size_t D = d.D, Dm = d.Dm, N = d.N, p = d.p;
     size_t per_layer = 2 * D + 3 * D * D + 3 * D + D * D + D + 2 * D + Dm * D + Dm + D * Dm + D;
-    return D * 3 * p * p + D + D + N * D + (size_t)d.L * per_layer + 2 * D;
+    const size_t restore = d.restore ? (size_t)d.L * (2 * RH * D + RH + D) : 0;
+    return D * 3 * p * p + D + D + N * D + (size_t)d.L * per_layer + 2 * D + restore;
 }
 
 struct Stage {
@@ -137,7 +147,9 @@ struct dv_handle {
     float* Z;         // [Tp, D] fp32: after attention residual
     void* Hb;         // [Tp, Dm] elem: MLP hidden
     uint8_t* mask[2]; // [T] per-layer maps (ping-pong)
-    int *idx, *pos_, *qoff, *cnt, *M;
+    int *idx, *pos_, *qoff, *cnt, *M;   // M[0]: recomputed rows, M[1]: reused tokens
+    int* ridx = nullptr;   // [T] reused tokens (restoration)
+    void* Hr = nullptr;    // [Tp, 128] elem: restoration hidden rows
     int *idx_id, *pos_id, *qoff_id;  // identity lists (reuse off)
     int id_frames = -1;              // frames the identity lists were built for
     // profiling
@@ -207,7 +219,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
 
     // identity row lists for the dense pass (built once per batch size)
     if (dense && h->id_frames != F) {
-        launch_compact(nullptr, nullptr, F, N, 1, h->idx_id, h->pos_id, h->qoff_id, s);
+        launch_compact(nullptr, nullptr, F, N, 1, h->idx_id, h->pos_id, h->qoff_id, nullptr, s);
         h->id_frames = F;
     }
 
@@ -236,6 +248,8 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
     const int* pos = dense ? h->pos_id : h->pos_;
     const int* qoff = dense ? h->qoff_id : h->qoff;
     const int* Mdev = dense ? nullptr : h->M;
+    // restoration of reused rows: on whenever tokens can be reused
+    const bool restore = d.restore && !dense;
 
     for (int l = 0; l < L; ++l) {
         const LayerW& w = h->layers[l];
@@ -253,7 +267,8 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             ga.layer = l;
             ga.mode = mode;
             ga.tau = tau;
-            ga.prev = (mode == GATE_COS) ? prev : nullptr;
+            // restored rows differ from the reference's: no shortcut from the previous map
+            ga.prev = (mode == GATE_COS && !restore) ? prev : nullptr;
             ga.inj = inj;
             ga.cur = dense ? nullptr : cur;
             ga.out_masks = om;
@@ -261,12 +276,30 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             ga.ln_g = w.ln1_g;
             ga.ln_b = w.ln1_b;
             ga.ln_out = h->A;   // token-indexed LN1 rows; the QKV GEMM gathers them through idx
+            ga.d_out = restore ? h->A : nullptr;   // reused tokens' differences, same buffer
             launch_gate(bf, ga, s);
         }
         if (!dense) {
             Scope sc(h, DV_STAGE_COMPACT, s);
-            launch_scan(h->cnt, gate_chunks(N), F, h->qoff, h->M, s);
-            launch_compact(cur, h->qoff, F, N, G, h->idx, h->pos_, nullptr, s);
+            launch_scan(h->cnt, gate_chunks(N), F, restore ? T : 0, h->qoff, h->M, s);
+            launch_compact(cur, h->qoff, F, N, G, h->idx, h->pos_, nullptr,
+                           restore ? h->ridx : nullptr, s);
+        }
+        if (restore) {   // restoration hidden rows: GELU(dx W_r1^T + b_r1), before LN2 reuses A
+            Scope sc(h, DV_STAGE_RESTORE, s);
+            GemmArgs r{};
+            r.A = h->A;
+            r.a_idx = h->ridx;
+            r.W = w.W_r1;
+            r.bias = w.b_r1;
+            r.K = D;
+            r.Nout = RH;
+            r.Mdev = h->M + 1;
+            r.Mconst = T;
+            r.Mmax = T;
+            r.cus = h->cus;
+            r.out = h->Hr;
+            launch_gemm(Epi::Fc1, bf, r, s);
         }
         GemmArgs g{};
         g.Mdev = Mdev;
@@ -338,7 +371,26 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             g.resid = h->Z;
             launch_gemm(Epi::Fc2, bf, g, s);
         }
-        if (mode == GATE_INJECT || mode == GATE_ALL || (mode == GATE_COS && tokens && l == L - 1)) {
+        if (restore) {   // reused rows: the reference token's new row + Hr W_r2^T + b_r2
+            Scope sc(h, DV_STAGE_RESTORE, s);
+            GemmArgs r{};
+            r.A = h->Hr;
+            r.W = w.W_r2;
+            r.bias = w.b_r2;
+            r.K = RH;
+            r.Nout = D;
+            r.Mdev = h->M + 1;
+            r.Mconst = T;
+            r.Mmax = T;
+            r.cus = h->cus;
+            r.idx = h->ridx;
+            r.resid = h->x;
+            r.out = h->x;
+            r.N = N;
+            r.G = G;
+            launch_gemm(Epi::Restore, bf, r, s);
+        } else if (mode == GATE_INJECT || mode == GATE_ALL ||
+                   (mode == GATE_COS && tokens && l == L - 1)) {
             // reused rows take the reference's new row (gate mode: only to hand out tokens)
             Scope sc(h, DV_STAGE_MERGE, s);
             launch_merge(h->x, cur, F, N, D, G, s);
@@ -450,6 +502,14 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
         lo[l].b_2 = reserve(D * 4);
     }
     const size_t o_lnf_g = reserve(D * 4), o_lnf_b = reserve(D * 4);
+    struct RO { size_t W_r1, b_r1, W_r2, b_r2; };
+    std::vector<RO> ro(d.restore ? L : 0);
+    for (auto& r : ro) {
+        r.W_r1 = reserve(RH * D * el);
+        r.b_r1 = reserve(RH * 4);
+        r.W_r2 = reserve(D * RH * el);
+        r.b_r2 = reserve(D * 4);
+    }
     try {
         host.assign(wbytes, 0);
     } catch (const std::bad_alloc&) {
@@ -489,6 +549,12 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     }
     put_vec(o_lnf_g, D);
     put_vec(o_lnf_b, D);
+    for (auto& r : ro) {
+        put_mat(r.W_r1, RH, D, D);
+        put_vec(r.b_r1, RH);
+        put_mat(r.W_r2, D, RH, RH);
+        put_vec(r.b_r2, D);
+    }
 
     dv_handle* h = new (std::nothrow) dv_handle();
     if (!h) return fail(DV_ENOMEM, "handle");
@@ -535,6 +601,14 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
         w.b_1 = (const float*)(wb + lo[l].b_1);
         w.W_2 = wb + lo[l].W_2;
         w.b_2 = (const float*)(wb + lo[l].b_2);
+        w.W_r1 = w.W_r2 = nullptr;
+        w.b_r1 = w.b_r2 = nullptr;
+        if (d.restore) {
+            w.W_r1 = wb + ro[l].W_r1;
+            w.b_r1 = (const float*)(wb + ro[l].b_r1);
+            w.W_r2 = wb + ro[l].W_r2;
+            w.b_r2 = (const float*)(wb + ro[l].b_r2);
+        }
     }
 
     // --- workspace ----------------------------------------------------------------------------
@@ -557,6 +631,10 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     }
     sz((size_t)d.B * gate_chunks(d.N) * 4);
     sz(4 * 4);
+    if (d.restore) {
+        sz(T * 4);             // ridx
+        sz(Tp * RH * el);      // Hr
+    }
     {
         hipError_t e = hipMalloc(&h->ws, need);
         if (e != hipSuccess) {
@@ -586,6 +664,10 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     h->qoff_id = carve<int>(p, d.B + 1);
     h->cnt = carve<int>(p, (size_t)d.B * gate_chunks(d.N));
     h->M = carve<int>(p, 4);
+    if (d.restore) {
+        h->ridx = carve<int>(p, T);
+        h->Hr = carve<char>(p, Tp * RH * el);
+    }
     *out = h;
     return DV_OK;
 }
@@ -639,8 +721,9 @@ int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size,
     if ((long long)n_frames * n_tokens > (1ll << 30)) return fail(DV_EINVAL, "too many tokens");
     // per-frame counts land in qoff[0..n) and are turned into the prefix in place by one block
     launch_count(masks, n_frames, n_tokens, group_size, qoff, stream);
-    launch_scan(qoff, 1, n_frames, qoff, count, stream);
-    launch_compact(masks, qoff, n_frames, n_tokens, group_size, idx, pos, nullptr, stream);
+    launch_scan(qoff, 1, n_frames, 0, qoff, count, stream);
+    launch_compact(masks, qoff, n_frames, n_tokens, group_size, idx, pos, nullptr, nullptr,
+                   stream);
     HIP_TRY(hipGetLastError());
     return DV_OK;
 }

@@ -31,6 +31,8 @@ enum class Epi : int {
     OProj = 2,  // z[r, c] = acc + bias[c] + x[idx[r], c]                              (fp32 out)
     Fc1 = 3,    // h[r, c] = gelu(acc + bias[c])                                       (elem out)
     Fc2 = 4,    // x[idx[r], c] = acc + bias[c] + z[r, c]                              (fp32 out)
+    Restore = 5,  // x[t, c] = acc + bias[c] + x[ref(t), c], t = idx[r]: a reused token's row
+                  // from its reference token's new row (ref(t): same token of frame G*floor(f/G))
 };
 
 struct GemmArgs {
@@ -46,7 +48,8 @@ struct GemmArgs {
     const int* idx;      // packed row -> token row
     const int* a_idx;    // A row gather: packed row m reads A row a_idx[m] (nullptr: row m)
     const float* pos;    // Patch: position table [N, D]
-    int P, N;            // Patch: patches and tokens per frame
+    int P, N;            // Patch: patches and tokens per frame (Restore: N)
+    int G;               // Restore: group size
     int cus;             // compute units of the device (0: no split of the last round)
     // set by the launcher: blocks below head_grid run large tiles over the rows [0, head),
     // the others small tiles over [head, M), head = gemm_head_rows(M, Nout, BM, BN, slots);
@@ -103,6 +106,8 @@ struct GateArgs {
     const float* ln_g;    // LN1 gain / shift
     const float* ln_b;
     void* ln_out;         // [F*N, D] elem: LN1 rows of recomputed tokens (token-indexed) or nullptr
+    void* d_out;          // [F*N, D] elem: x_f - x_ref rows of reused tokens (token-indexed;
+                          // restoration) or nullptr.  May be ln_out: the rows are disjoint.
 };
 // Mode GATE_NONE marks every token recomputed (reuse off) and only writes LN1 rows.
 // The gate runs in blocks of GATE_TOK tokens; counts are per block: cnt[f * gate_chunks(N) + c].
@@ -111,12 +116,14 @@ inline int gate_chunks(int N) { return (N + GATE_TOK - 1) / GATE_TOK; }
 void launch_gate(bool bf16, const GateArgs& a, hipStream_t s);
 void launch_count(const uint8_t* m, int F, int N, int G, int* cnt, hipStream_t s);
 // qoff[0..F] = exclusive prefix of the per-frame counts (sum of `per` consecutive entries of
-// cnt per frame), *M = qoff[F]
-void launch_scan(const int* cnt, int per, int F, int* qoff, int* M, hipStream_t s);
+// cnt per frame), M[0] = qoff[F]; M[1] = tokens - M[0] (the reused tokens) when tokens > 0
+void launch_scan(const int* cnt, int per, int F, int tokens, int* qoff, int* M, hipStream_t s);
 // idx/pos from a per-layer map and its qoff (cur == nullptr: every token recomputed, identity
 // lists, qoff_in ignored and qoff_out written)
+// ridx (or nullptr): the reused tokens f*N+i of non-reference frames in frame-major order, at
+// slot (f*N - qoff[f]) + (reused tokens of frame f before i)
 void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,
-                    int* pos, int* qoff_out, hipStream_t s);
+                    int* pos, int* qoff_out, int* ridx, hipStream_t s);
 
 // LayerNorm of rows (optionally gathered through idx) into elem rows: dst[r] = LN(src[g(r)])
 void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* Mdev, int Mmax,

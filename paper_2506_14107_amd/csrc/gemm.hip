@@ -83,9 +83,14 @@ __device__ inline void epi_store(const GemmArgs& a, int row, int col, float acc)
         v = gelu_erf(v);
         if (BF) ((uint16_t*)a.out)[(size_t)row * a.Nout + col] = f32_to_bf16(v);
         else ((float*)a.out)[(size_t)row * a.Nout + col] = v;
-    } else {  // Fc2
+    } else if constexpr (E == Epi::Fc2) {
         v += a.resid[(size_t)row * a.Nout + col];
         ((float*)a.out)[(size_t)a.idx[row] * a.Nout + col] = v;
+    } else {  // Restore: a reused token's row from its reference token's new row
+        const int t = a.idx[row], f = t / a.N;
+        const int rt = (f / a.G * a.G) * a.N + t % a.N;
+        v += a.resid[(size_t)rt * a.Nout + col];
+        ((float*)a.out)[(size_t)t * a.Nout + col] = v;
     }
 }
 
@@ -121,8 +126,9 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
     constexpr int CPRW = WN / 4;         // 16-byte chunks per row
     constexpr int RPI = 64 / CPRW;       // rows per wavefront instruction
     constexpr int NQ = 32 / RPI;         // instructions per 32-row slab
-    constexpr bool LOADS = E == Epi::OProj || E == Epi::Fc2 || E == Epi::Patch;
-    constexpr bool SCATTER = E == Epi::Fc2 || E == Epi::Patch;   // output rows are token rows
+    constexpr bool LOADS = E == Epi::OProj || E == Epi::Fc2 || E == Epi::Patch || E == Epi::Restore;
+    // output rows are token rows
+    constexpr bool SCATTER = E == Epi::Fc2 || E == Epi::Patch || E == Epi::Restore;
     constexpr uint32_t ESZ = (E == Epi::Qkv || E == Epi::Fc1) ? 2 : 4;   // output element bytes
     const int lr = lane & 31, hl = lane >> 5;
     const int c = lane % CPRW, rsub = lane / CPRW;
@@ -142,7 +148,7 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
         for (int q = 0; q < NQ; ++q) {
             const int row = row_of(i, q);
             const int r = row < M ? row : M - 1;           // a valid row for the tile tail
-            if constexpr (E == Epi::OProj || E == Epi::Fc2) tr[q] = a.idx[r];
+            if constexpr (E == Epi::OProj || E == Epi::Fc2 || E == Epi::Restore) tr[q] = a.idx[r];
             else if constexpr (E == Epi::Patch) tr[q] = (r / a.P) * a.N + 1 + r % a.P;
             else tr[q] = row;
         }
@@ -160,9 +166,16 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
                 const int row = row_of(i, q);
                 const uint32_t r = row < M ? row : M - 1;
                 uint32_t off;
-                if constexpr (E == Epi::OProj) off = ((uint32_t)tr[q] * Nout + col) * 4;
-                else if constexpr (E == Epi::Fc2) off = (r * Nout + col) * 4;
-                else off = ((1 + r % a.P) * Nout + col) * 4;
+                if constexpr (E == Epi::OProj) {
+                    off = ((uint32_t)tr[q] * Nout + col) * 4;
+                } else if constexpr (E == Epi::Fc2) {
+                    off = (r * Nout + col) * 4;
+                } else if constexpr (E == Epi::Restore) {   // the reference token's row
+                    const uint32_t t = tr[q], f = t / a.N;
+                    off = (((f / a.G * a.G) * a.N + t % a.N) * Nout + col) * 4;
+                } else {
+                    off = ((1 + r % a.P) * Nout + col) * 4;
+                }
                 dst[q] = __builtin_amdgcn_raw_buffer_load_b128(rres, (int)off, 0, 0);
             }
         }
@@ -595,6 +608,7 @@ void launch_gemm(Epi e, bool bf16, const GemmArgs& a, hipStream_t s) {
         case Epi::OProj: launch_one<Epi::OProj>(bf16, a, s); break;
         case Epi::Fc1: launch_one<Epi::Fc1>(bf16, a, s); break;
         case Epi::Fc2: launch_one<Epi::Fc2>(bf16, a, s); break;
+        case Epi::Restore: launch_one<Epi::Restore>(bf16, a, s); break;
     }
 }
 

@@ -61,7 +61,8 @@ __global__ void cls_init_k(float* x, const float* cls, const float* pos, int F, 
 
 // --- reuse gate + LN1: blocks of GATE_TOK tokens of one frame, one wavefront per token --------
 // Decides reuse for each token and, for each token that is recomputed, writes LN1 of its row
-// (already in registers for the cosine) to the token-indexed buffer `ln_out`.
+// (already in registers for the cosine) to the token-indexed buffer `ln_out`; with `d_out`
+// (restoration), each reused token's difference to its reference row goes to `d_out`.
 // cnt[f * chunks + block-in-frame] = number of recomputed tokens of that block.
 template <bool BF>
 __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
@@ -118,6 +119,25 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
                     cs = fminf(1.0f, fmaxf(-1.0f, cs));
                     if (same) cs = 1.0f;
                     reuse = cs >= a.tau;
+                }
+            }
+        }
+        if (reuse && a.d_out) {   // reused (restoration): x_f - x_ref into the token-indexed buffer
+            const float4* xr = (const float4*)(a.x + ((size_t)r * N + i) * D);
+#pragma unroll
+            for (int k = 0; k < MAX_CHUNKS; ++k) {
+                const int c = lane + k * WAVE;
+                if (c < nchunk) {
+                    const float4 u = loaded ? v[k] : xf[c], w = xr[c];
+                    const float4 o = {u.x - w.x, u.y - w.y, u.z - w.z, u.w - w.w};
+                    if (BF) {
+                        uint2 pk;
+                        pk.x = (uint32_t)f32_to_bf16(o.x) | ((uint32_t)f32_to_bf16(o.y) << 16);
+                        pk.y = (uint32_t)f32_to_bf16(o.z) | ((uint32_t)f32_to_bf16(o.w) << 16);
+                        ((uint2*)a.d_out)[row * nchunk + c] = pk;
+                    } else {
+                        ((float4*)a.d_out)[row * nchunk + c] = o;
+                    }
                 }
             }
         }
@@ -195,10 +215,11 @@ __global__ __launch_bounds__(256) void count_k(const uint8_t* m, int F, int N, i
     if (threadIdx.x == 0) cnt[f] = red[0];
 }
 
-// --- exclusive prefix over frames: qoff[f] = sum_{g<f} count(g), qoff[F] = *M = total ---------
+// --- exclusive prefix over frames: qoff[f] = sum_{g<f} count(g), qoff[F] = M[0] = total ------
 // count(g) = cnt[g*per] + ... + cnt[g*per + per-1]; one block; qoff may equal cnt when per == 1
 // (each thread reads its entries before any write to them)
-__global__ __launch_bounds__(1024) void scan_k(const int* cnt, int per, int F, int* qoff, int* M) {
+__global__ __launch_bounds__(1024) void scan_k(const int* cnt, int per, int F, int tokens, int* qoff,
+                                              int* M) {
     __shared__ int part[1024];
     __shared__ int carry_s;
     const int tid = threadIdx.x;
@@ -225,7 +246,8 @@ __global__ __launch_bounds__(1024) void scan_k(const int* cnt, int per, int F, i
     }
     if (tid == 0) {
         qoff[F] = carry_s;
-        *M = carry_s;
+        M[0] = carry_s;
+        if (tokens > 0) M[1] = tokens - carry_s;   // reused tokens
     }
 }
 
@@ -234,9 +256,11 @@ __global__ __launch_bounds__(1024) void scan_k(const int* cnt, int per, int F, i
 // inside the frame comes from a wavefront ballot + popcount and a prefix over the block's four
 // wavefronts.  A reused token points at the slot of the same token of its reference frame
 // (reference frames keep all their tokens, in order).  cur == nullptr: every token recomputed,
-// qoff ignored (identity lists).
+// qoff ignored (identity lists).  ridx: the complement list of reused tokens, frame-major (a
+// reused token's rank is i minus the recomputed tokens of its frame before i).
 __global__ __launch_bounds__(256) void compact_k(const uint8_t* cur, const int* qoff_in, int F,
-                                                 int N, int G, int* idx, int* pos, int* qoff_out) {
+                                                 int N, int G, int* idx, int* pos, int* qoff_out,
+                                                 int* ridx) {
     const int f = blockIdx.x;
     const int r = (f / G) * G;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -261,6 +285,8 @@ __global__ __launch_bounds__(256) void compact_k(const uint8_t* cur, const int* 
             pos[(size_t)f * N + i] = off + rank;
         } else if (valid) {
             pos[(size_t)f * N + i] = refoff + i;
+            // rank among reused tokens: those of earlier frames, then the frame's before i
+            if (ridx) ridx[(f * N - off) + i - rank] = f * N + i;
         }
         running += wtot[0] + wtot[1] + wtot[2] + wtot[3];
     }
@@ -414,14 +440,14 @@ void launch_count(const uint8_t* m, int F, int N, int G, int* cnt, hipStream_t s
     hipLaunchKernelGGL(count_k, dim3(F), dim3(256), 0, s, m, F, N, G, cnt);
 }
 
-void launch_scan(const int* cnt, int per, int F, int* qoff, int* M, hipStream_t s) {
-    hipLaunchKernelGGL(scan_k, dim3(1), dim3(1024), 0, s, cnt, per, F, qoff, M);
+void launch_scan(const int* cnt, int per, int F, int tokens, int* qoff, int* M, hipStream_t s) {
+    hipLaunchKernelGGL(scan_k, dim3(1), dim3(1024), 0, s, cnt, per, F, tokens, qoff, M);
 }
 
 void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,
-                    int* pos, int* qoff_out, hipStream_t s) {
+                    int* pos, int* qoff_out, int* ridx, hipStream_t s) {
     hipLaunchKernelGGL(compact_k, dim3(F), dim3(256), 0, s, cur, qoff_in, F, N, G, idx, pos,
-                       qoff_out);
+                       qoff_out, ridx);
 }
 
 void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* Mdev, int Mmax,

@@ -50,6 +50,16 @@ def test_weights_floats_matches_layout():
     assert dj.dv_weights_floats(_cfg(image_size=100)) == 0
 
 
+def test_weights_floats_with_restoration_section():
+    import dataclasses
+    import synth
+    m = dataclasses.replace(synth.get_config("tiny").model, restore=True)
+    cfg = _cfg(flags=dj.DV_FLAG_RESTORE)
+    assert dj.dv_weights_floats(cfg) == synth.weights.blob_floats(m)
+    assert synth.weights.blob_floats(m) - dj.dv_weights_floats(_cfg()) == \
+        m.depth * (2 * 128 * m.width + 128 + m.width)
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(image_size=100), dj.DV_EUNSUPPORTED),       # S % p
     (dict(heads=5), dj.DV_EUNSUPPORTED),              # D % H
@@ -58,6 +68,7 @@ def test_weights_floats_matches_layout():
     (dict(max_batch_frames=0), dj.DV_EINVAL),
     (dict(dtype=7), dj.DV_EINVAL),
     (dict(width=200, heads=2), dj.DV_EUNSUPPORTED),   # width not a tile multiple
+    (dict(flags=2), dj.DV_EUNSUPPORTED),              # unknown flag bit
 ])
 def test_create_rejects_bad_config(kw, code):
     cfg = _cfg(**kw)
