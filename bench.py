@@ -217,6 +217,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="vit_l14")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--restore", action="store_true",
+                    help="with the restoration layer on reused tokens (random restoration weights)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device-to-device copy (HBM counter calibration)")
     ap.add_argument("--traffic-record", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_OUT"),
@@ -242,6 +244,10 @@ def main():
 
     w = synth.get_config(args.workload)
     m = w.model
+    if args.restore:
+        import dataclasses
+        m = dataclasses.replace(m, restore=True)
+        w = dataclasses.replace(w, model=m)
     G, F = w.group_size, w.batch_frames
     t0 = time.time()
     blob = synth.make_blob(m, w.weight_seed)
@@ -377,7 +383,10 @@ def main():
         "dtype": "bf16" if m.dtype == "bf16" else "f32", "data": "synthetic",
         "config": {"workload": f"{w.name}: {m.image_size}px patch {m.patch} ({N} tokens), depth "
                                f"{m.depth}, width {D}, {m.heads} heads, MLP {m.mlp}; {F} frames "
-                               f"per batch, groups of {G}; reuse levels "
+                               f"per batch, groups of {G}; "
+                               + ("restoration MLP (hidden 128) on reused tokens; " if m.restore
+                                  else "")
+                               + "reuse levels "
                                + "/".join(f"{t:.0%}" for t in targets if t is not None),
                    "frames_per_step": F * len(taus), "group_size": G},
         "sweep": sweep,

@@ -6,6 +6,7 @@ a 512-frame batch plus a ragged 8-frame batch).  Sampled whole groups are recomp
 oracle replaying the GPU's reuse maps (teacher-forced decisions, then embeddings and the full
 last-layer token buffers to the bf16 bar: min cosine >= 0.999, per-frame relative error <= 2e-2).
 """
+import dataclasses
 import time
 
 import numpy as np
@@ -56,5 +57,33 @@ def test_full_size_parity(name, n, tau, starts):
         print(f"[{name}] group {g0}: oracle {time.time() - t1:.1f}s, decisions off {bad}, "
               f"in band {inside:.2%}, emb cos {c_e:.5f} rel {r_e:.2e}, tok cos {c_t:.5f} "
               f"rel {r_t:.2e}", flush=True)
+        assert bad == 0, f"{bad} decisions differ outside the 1e-3 band"
+    enc.close()
+
+
+def test_full_size_restoration():
+    """ViT-L/14, 256 frames with the restoration layer on reused rows (random restoration
+    weights): sampled groups against the oracle replaying the GPU's maps."""
+    torch = require_gpu()
+    w = synth.get_config("vit_l14")
+    m, G = dataclasses.replace(w.model, restore=True), w.group_size
+    tau = float(np.float32(0.906))
+    blob = synth.make_blob(m, w.weight_seed)
+    fr = synth.render_frames(w.video, m.image_size, 0, 256)
+    enc = encoder(m, blob, w.batch_frames)
+    emb, masks, toks = enc.encode(dev(fr), G, tau, want_tokens=True)
+    torch.cuda.synchronize()
+    mg = host(masks)
+    rho = oracle.reuse_rate(mg, G)
+    print(f"[vit_l14 restore] GPU reuse {rho:.3f}", flush=True)
+    assert 0.05 < rho < 0.99, f"threshold gives degenerate reuse {rho}"
+    for g0 in (0, 128):
+        sl = slice(g0, g0 + G)
+        r = oracle.encode(fr[sl], blob, m.as_dict(), G, masks=mg[sl])
+        bad, inside = mask_parity(mg[sl], r["cos"], tau)
+        c_e, r_e = check_close(host(emb[sl]), r["emb"], "bf16", f"group {g0} embeddings")
+        c_t, r_t = check_close(host(toks[sl]), r["tokens"], "bf16", f"group {g0} tokens")
+        print(f"[vit_l14 restore] group {g0}: decisions off {bad}, in band {inside:.2%}, emb cos "
+              f"{c_e:.5f} rel {r_e:.2e}, tok cos {c_t:.5f} rel {r_t:.2e}", flush=True)
         assert bad == 0, f"{bad} decisions differ outside the 1e-3 band"
     enc.close()
