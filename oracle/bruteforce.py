@@ -6,7 +6,11 @@ filtration, recompute of C, reconstruction from the reference for R) but
 walks frames, layers, tokens, heads and keys one at a time with scalar
 softmax arithmetic.  It shares no helper with the vectorised oracle.  With ``cfg["restore"]``
 a reused token's output adds the restoration MLP of its input difference
-to the reference (hidden 128, GELU; Section 3.3), evaluated row by row.
+to the reference (hidden 128, GELU; Section 3.3), evaluated row by row.  With
+``cfg["decision"]`` the gate is the decision MLP (Section 3.3): inputs the cosine, the class
+token's attention weight on the token in the frame's previous layer (mean over heads; 1/N at
+the first layer) and the one-hot frame type (P for every non-reference frame); reuse when its
+output exceeds tau.
 """
 import math
 
@@ -36,6 +40,8 @@ def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
     lnfg, lnfb = nxt(D), nxt(D)
     restore = bool(cfg.get("restore"))
     rest = [[nxt(128, D), nxt(128), nxt(D, 128), nxt(D)] for _ in range(L)] if restore else None
+    decide = bool(cfg.get("decision"))
+    dec = [[nxt(64, 6), nxt(64), nxt(1, 64), nxt(1)] for _ in range(L)] if decide else None
 
     def norm(v, gamma, beta):
         mean = sum(v) / len(v)
@@ -61,12 +67,23 @@ def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
                 vec = fr64[f, :, r * p:(r + 1) * p, c * p:(c + 1) * p].reshape(-1)
                 X[f, 1 + r * gs + c] = Wpe @ vec + bpe + pos[1 + r * gs + c]
 
+    def decision(s, t, ftype, Wd1, bd1, Wd2, bd2):
+        v = [s, t, 0.0, 0.0, 0.0, 0.0]
+        v[2 + ftype] = 1.0
+        out = float(bd2[0])
+        for k in range(64):
+            z = float(bd1[k]) + sum(float(Wd1[k, j]) * v[j] for j in range(6))
+            out += float(Wd2[0, k]) * 0.5 * z * (1.0 + math.erf(z / math.sqrt(2.0)))
+        return out
+
     M = np.zeros((F, L, N), dtype=np.uint8)
+    tprev = [[1.0 / N] * N for _ in range(F)]   # class-token attention of the previous layer
     for l in range(L):
         g1, b1, Wqkv, bqkv, Wo, bo, g2, b2, W1, bb1, W2, bb2 = layers[l]
         Y = np.zeros_like(X)
         KEY = np.zeros((F, N, D))
         VAL = np.zeros((F, N, D))
+        tnext = [[0.0] * N for _ in range(F)]
         for f in range(F):                      # frames in order: the reference comes first
             ref = (f // group_size) * group_size
             reuse = [False] * N
@@ -78,6 +95,9 @@ def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
                         reuse[i] = False
                     elif tau == math.inf:
                         reuse[i] = True
+                    elif decide:
+                        dval = decision(cosine(X[f, i], X[ref, i]), tprev[f][i], 1, *dec[l])
+                        reuse[i] = dval > tau
                     else:
                         reuse[i] = cosine(X[f, i], X[ref, i]) >= tau
             Q = {}
@@ -107,10 +127,13 @@ def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
                     tot = sum(ex)
                     for j in range(N):
                         o[lo:hi] += (ex[j] / tot) * VAL[f, j, lo:hi]
+                        if i == 0:
+                            tnext[f][j] += (ex[j] / tot) / H
                 z = X[f, i] + Wo @ o + bo
                 u = W1 @ norm(z, g2, b2) + bb1
                 u = np.array([0.5 * t * (1.0 + math.erf(t / math.sqrt(2.0))) for t in u])
                 Y[f, i] = z + W2 @ u + bb2
         X = Y
+        tprev = tnext
     emb = np.stack([norm(X[f, 0], lnfg, lnfb) for f in range(F)])
     return {"emb": emb, "masks": M, "tokens": X}

@@ -34,6 +34,20 @@ What it computes, following the paper's model description (Section 3):
   keys and values of reused tokens stay the reference's.  The restored rows
   are the next layer's input (so a token reused once may be recomputed later).
 
+* Learned decision layer (Section 3.3, decision-layer equations), when the
+  configuration enables it (``cfg["decision"]``): the threshold is replaced by
+  d_i = MLP(v_i), v_i = (s_i, t_i, r_i) -- s_i the cosine above (one reference,
+  so the max over past and future references of Eq. 1 has a single term),
+  t_i the class token's attention weight on token i (mean over heads) in the
+  frame's previous layer (1/N before the first layer, where no attention has
+  run yet), r_i the one-hot frame type (I, P, B_dist2, B_dist1; with one
+  earlier reference per group every non-reference frame is a P frame); the
+  codec-metadata cue has no input here and is left out.  The MLP is two
+  layers, hidden 64, exact GELU; token i is reused when d_i > tau (tau = 0
+  is the paper's rule).  Such decisions are not monotone over layers, so
+  every token is gated at every layer and a reused row copies the
+  reference's layer output.
+
 Modes: gate mode (``tau``) and mask-injection mode (``masks`` given; class
 token and reference-frame entries are forced to 0).  ``tau = -inf`` turns
 reuse off (dense), ``tau = +inf`` reuses every non-class token of every
@@ -49,6 +63,8 @@ from scipy.special import erf
 LN_EPS = 1e-5
 COS_EPS = 1e-8
 RESTORE_HIDDEN = 128   # hidden width of the restoration MLP (Section 3.3)
+DECISION_HIDDEN = 64   # hidden width of the decision MLP (Section 3.3 gives none)
+FRAME_TYPES = ("I", "P", "B_dist2", "B_dist1")   # reference-type cue r (Section 3.3)
 
 
 def unpack_blob(blob, cfg, dtype=np.float64):
@@ -84,6 +100,11 @@ def unpack_blob(blob, cfg, dtype=np.float64):
         for lay in W["layers"]:
             lay["W_r1"], lay["b_r1"] = take(R, D), take(R)
             lay["W_r2"], lay["b_r2"] = take(D, R), take(D)
+    if cfg.get("decision"):
+        Hd = DECISION_HIDDEN
+        for lay in W["layers"]:
+            lay["W_d1"], lay["b_d1"] = take(Hd, 2 + len(FRAME_TYPES)), take(Hd)
+            lay["W_d2"], lay["b_d2"] = take(1, Hd), take(1)
     if off != blob.size:
         raise ValueError(f"weight blob has {blob.size} floats, layout needs {off}")
     return W
@@ -137,11 +158,14 @@ def gate_decision(cos, tau):
     return cos >= tau
 
 
-def attention(q, k, v, heads):
-    """Multi-head softmax attention: q [n, D] against all keys k, v [N, D]."""
+def attention(q, k, v, heads, first_probs=False):
+    """Multi-head softmax attention: q [n, D] against all keys k, v [N, D].  With
+    ``first_probs`` also returns the attention weights of query 0 over the N keys, averaged
+    over the heads."""
     n, D = q.shape
     dh = D // heads
     out = np.empty_like(q)
+    p0 = np.zeros(k.shape[0], dtype=q.dtype)
     for h in range(heads):
         s = slice(h * dh, (h + 1) * dh)
         logits = (q[:, s] @ k[:, s].T) / np.sqrt(dh)
@@ -149,7 +173,34 @@ def attention(q, k, v, heads):
         pr = np.exp(logits)
         pr /= pr.sum(axis=1, keepdims=True)
         out[:, s] = pr @ v[:, s]
-    return out
+        p0 += pr[0]
+    return (out, p0 / heads) if first_probs else out
+
+
+def frame_type(f, group_size):
+    """Index into FRAME_TYPES: the group's first frame is the I frame, every other frame
+    references it alone, the role of a P frame."""
+    return 0 if f % group_size == 0 else 1
+
+
+def decision_values(s, t, ftype, P):
+    """d_i = MLP_decision(concat(s_i, t_i, r_i)) for one frame's tokens (Section 3.3)."""
+    r = np.zeros((len(s), len(FRAME_TYPES)), dtype=P["W_d1"].dtype)
+    r[:, ftype] = 1.0
+    v = np.concatenate([s[:, None], t[:, None], r], axis=1)
+    return (gelu(v @ P["W_d1"].T + P["b_d1"]) @ P["W_d2"].T + P["b_d2"])[:, 0]
+
+
+def decision_gate(d, tau):
+    """Hard gate of the decision layer: reuse when d_i > tau (the paper's rule is tau = 0);
+    tau = -inf / +inf keep their meanings (reuse off / reuse everything)."""
+    if np.isnan(tau):
+        raise ValueError("tau must not be NaN")
+    if tau == -np.inf:
+        return np.zeros(d.shape, dtype=bool)
+    if tau == np.inf:
+        return np.ones(d.shape, dtype=bool)
+    return d > tau
 
 
 def qkv_rows(x_rows, P):
@@ -178,6 +229,8 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
       emb    [F, D]      final LayerNorm of each frame's class token
       masks  [F, L, N]   uint8, 1 = token reused at that layer
       cos    [F, L, N]   cosine to the reference token (NaN where not evaluated)
+      dec    [F, L, N]   decision-MLP output d_i (only with cfg["decision"]; NaN where not
+                         evaluated)
       tokens [F, N, D]   output of the last layer
       layers (optional)  list of the L+1 token buffers x^0..x^L
     """
@@ -193,40 +246,58 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
     N = x.shape[1]
     out_m = np.zeros((F, L, N), dtype=np.uint8)
     out_c = np.full((F, L, N), np.nan)
+    decide = bool(cfg.get("decision"))
+    out_d = np.full((F, L, N), np.nan) if decide else None
+    t_cls = np.full((F, N), 1.0 / N) if decide else None  # class-token attention, previous layer
     hist = [x.copy()] if return_layers else None
 
     for l in range(L):
         P = W["layers"][l]
         y = np.empty_like(x)
+        t_next = np.empty((F, N)) if decide else None
         for r in range(0, F, G):
             # reference frame: full layer on every token
             q_r, k_r, v_r = qkv_rows(x[r], P)
-            y[r] = finish_rows(x[r], attention(q_r, k_r, v_r, H), P)
+            o_r, p_r = attention(q_r, k_r, v_r, H, first_probs=True)
+            y[r] = finish_rows(x[r], o_r, P)
+            if decide:
+                t_next[r] = p_r
             for f in range(r + 1, min(r + G, F)):
                 c = cosine_rows(x[f, 1:], x[r, 1:])
                 out_c[f, l, 1:] = c
+                if decide:
+                    dv = decision_values(c, t_cls[f, 1:], frame_type(f, G), P)
+                    out_d[f, l, 1:] = dv
                 if masks is not None:
                     reuse = np.asarray(masks[f, l, 1:]) != 0
+                elif decide:
+                    reuse = decision_gate(dv, tau)
                 else:
                     reuse = gate_decision(c, tau)
                 m = np.concatenate([[False], reuse])          # class token never reused
                 out_m[f, l] = m
-                C = np.flatnonzero(~m)                        # recompute tokens
+                C = np.flatnonzero(~m)                        # recompute tokens (C[0] = class)
                 q_c, k_c, v_c = qkv_rows(x[f, C], P)
                 k_t, v_t = k_r.copy(), v_r.copy()             # keys/values: reference ...
                 k_t[C], v_t[C] = k_c, v_c                     # ... overwritten by fresh rows
-                y_c = finish_rows(x[f, C], attention(q_c, k_t, v_t, H), P)
+                o_c, p_c = attention(q_c, k_t, v_t, H, first_probs=True)
+                y_c = finish_rows(x[f, C], o_c, P)
+                if decide:
+                    t_next[f] = p_c
                 y[f] = y[r]                                   # reused rows: reference output
                 y[f, C] = y_c                                 # recomputed rows
                 if cfg.get("restore"):                        # ... calibrated by the restoration MLP
                     Rr = np.flatnonzero(m)
                     y[f, Rr] += restore_rows(x[f, Rr] - x[r, Rr], P)
         x = y
+        t_cls = t_next
         if return_layers:
             hist.append(x.copy())
 
     emb = layer_norm(x[:, 0], W["lnf_g"], W["lnf_b"])
     res = {"emb": emb, "masks": out_m, "cos": out_c, "tokens": x}
+    if decide:
+        res["dec"] = out_d
     if return_layers:
         res["layers"] = hist
     return res

@@ -11,6 +11,8 @@ from dataclasses import dataclass, field
 from typing import Optional, Tuple
 
 RESTORE_HIDDEN = 128   # hidden width of the restoration MLP (the paper's two-layer MLP, size 128)
+DECISION_HIDDEN = 64   # hidden width of the decision MLP (the paper gives none; one per wavefront lane)
+DECISION_FEATURES = 6  # its input: similarity s, class-token attention t, one-hot frame type r (4)
 
 
 @dataclass(frozen=True)
@@ -23,6 +25,7 @@ class ModelConfig:
     mlp: int
     dtype: str  # "f32" or "bf16": arithmetic type of the GEMM/attention operands
     restore: bool = False   # per-layer restoration MLP on reused tokens (hidden RESTORE_HIDDEN)
+    decision: bool = False  # per-layer learned decision MLP as the gate (hidden DECISION_HIDDEN)
 
     @property
     def n_patches(self) -> int:
@@ -39,7 +42,7 @@ class ModelConfig:
     def as_dict(self):
         return dict(image_size=self.image_size, patch=self.patch, depth=self.depth,
                     width=self.width, heads=self.heads, mlp=self.mlp, dtype=self.dtype,
-                    restore=self.restore)
+                    restore=self.restore, decision=self.decision)
 
 
 @dataclass(frozen=True)

@@ -8,20 +8,26 @@ Blob layout (little-endian float32, tensors back to back, row-major):
     lnf_g [D], lnf_b [D]
     with the restoration MLP (ModelConfig.restore), then per layer l = 0..L-1:
         W_r1 [R,D], b_r1 [R], W_r2 [D,R], b_r2 [D]        (R = RESTORE_HIDDEN = 128)
+    with the decision MLP (ModelConfig.decision), then per layer l = 0..L-1:
+        W_d1 [Hd,6], b_d1 [Hd], W_d2 [1,Hd], b_d2 [1]     (Hd = DECISION_HIDDEN = 64)
 Rows of W_qkv are Q, then K, then V; within each, heads are contiguous slices
 of D/H rows.  Linear layers map x -> x @ W.T + b.
 
-The restoration section comes last, so the other weights of a seed do not depend on it.
+The restoration and decision sections come last (in that order), so the other weights of a
+seed do not depend on them.
 Matrices, biases, the class token and the position table are drawn from
 N(0, 0.02); LayerNorm gains are 1 and shifts 0 unless ``perturb_ln`` is set,
 in which case gains are 1 + N(0, 0.02) and shifts N(0, 0.02) so that the
-affine part of every LayerNorm is exercised.  For bf16 models every value is
+affine part of every LayerNorm is exercised.  The decision MLP is drawn at unit scale so
+that its output moves with its inputs: W_d1 and b_d1 ~ N(0, 1) except the column of the
+class-token attention feature, ~ N(0, N) (that feature is about 1/N), W_d2 ~ N(0, 1/Hd),
+b_d2 = 0.  For bf16 models every value is
 rounded to the nearest bf16 (ties to even) and stored back as fp32, so the
 blob holds exactly the weights a bf16 kernel sees.
 """
 import numpy as np
 
-from .configs import RESTORE_HIDDEN, ModelConfig
+from .configs import DECISION_FEATURES, DECISION_HIDDEN, RESTORE_HIDDEN, ModelConfig
 
 
 def weight_layout(m: ModelConfig):
@@ -43,6 +49,11 @@ def weight_layout(m: ModelConfig):
         for l in range(m.depth):
             out += [(f"l{l}.W_r1", (Rh, D)), (f"l{l}.b_r1", (Rh,)),
                     (f"l{l}.W_r2", (D, Rh)), (f"l{l}.b_r2", (D,))]
+    if m.decision:
+        Hd, Fd = DECISION_HIDDEN, DECISION_FEATURES
+        for l in range(m.depth):
+            out += [(f"l{l}.W_d1", (Hd, Fd)), (f"l{l}.b_d1", (Hd,)),
+                    (f"l{l}.W_d2", (1, Hd)), (f"l{l}.b_d2", (1,))]
     return out
 
 
@@ -80,6 +91,14 @@ def make_weights(m: ModelConfig, seed: int, perturb_ln: bool = False, std: float
             v[...] = 0.0
             if perturb_ln:
                 v[...] = np.float32(std) * rng.standard_normal(shape, dtype=np.float32)
+        elif base in ("W_d1", "b_d1", "W_d2"):
+            rng.standard_normal(shape, dtype=np.float32, out=v)
+            if base == "W_d1":
+                v[:, 1] *= np.float32(m.n_tokens)
+            if base == "W_d2":
+                v *= np.float32(1.0 / np.sqrt(shape[1]))
+        elif base == "b_d2":
+            v[...] = 0.0
         else:
             rng.standard_normal(shape, dtype=np.float32, out=v)
             v *= np.float32(std)

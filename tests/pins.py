@@ -29,6 +29,15 @@ What pins what:
   restore_one  one injected reused token: reference output + the MLP (torch Linear/GELU) of its
                input difference; every other row as without restoration
   restore_static identical frames at tau=+inf: closed forms at layers 0 and 1
+  decision layer (the learned gate, when the configuration enables it):
+  decision_threshold an MLP that is a*(s - theta) gives the cosine gate's maps and outputs
+  decision_attention  the class-token attention cue: 1/N before the first layer, then torch
+               MultiheadAttention's head-averaged weights of the class query in the previous
+               layer (also with a reference key/value substituted)
+  decision_type      the frame-type cue is the P entry for every non-reference frame; a tie
+               d == tau recomputes
+  decision_mlp       the MLP itself == torch Linear/GELU/Linear on the features
+  decision_brute     == the per-token loop implementation (with and without restoration)
 """
 import numpy as np
 
@@ -46,6 +55,9 @@ M_1 = ModelConfig(48, 16, 1, 16, 2, 32, "f32")      # one layer
 M_AR = ModelConfig(32, 16, 2, 8, 2, 16, "f32", restore=True)     # M_A with restoration
 M_BR = ModelConfig(48, 16, 2, 16, 2, 32, "f32", restore=True)    # M_B with restoration
 M_1R = ModelConfig(48, 16, 1, 16, 2, 32, "f32", restore=True)    # M_1 with restoration
+M_AD = ModelConfig(32, 16, 2, 8, 2, 16, "f32", decision=True)    # M_A with the decision MLP
+M_BD = ModelConfig(48, 16, 2, 16, 2, 32, "f32", decision=True)   # M_B with the decision MLP
+M_BRD = ModelConfig(48, 16, 2, 16, 2, 32, "f32", restore=True, decision=True)
 
 
 def weights(m, seed=7, perturb=True):
@@ -363,7 +375,131 @@ def pin_restore_static(ora):
                f"layer 1 restored rows, frame {f}")
 
 
+def linear_decision(w, m, col, a, theta, c=40.0):
+    """Make every layer's decision MLP the affine function d = a * (v[col] - theta) of one
+    input feature: hidden unit 0 computes a * v[col] + c, where GELU is the identity to fp64
+    rounding (erf(c / sqrt 2) rounds to 1 for c > 8.4), the other units are switched off.
+    Returns the blob and the threshold the fp32 weights hold (theta after rounding)."""
+    for l in range(m.depth):
+        for k in ("W_d1", "b_d1", "W_d2", "b_d2"):
+            w[f"l{l}.{k}"][...] = 0.0
+        w[f"l{l}.W_d1"][0, col] = a
+        w[f"l{l}.b_d1"][0] = c
+        w[f"l{l}.W_d2"][0, 0] = 1.0
+        w[f"l{l}.b_d2"][0] = -c - a * theta
+    held = (-float(w["l0.b_d2"][0]) - c) / a
+    return synth.pack_weights(w, m), held
+
+
+def _without_decision(w, m):
+    base = ModelConfig(m.image_size, m.patch, m.depth, m.width, m.heads, m.mlp, m.dtype,
+                       restore=m.restore)
+    return base, synth.pack_weights(w, base)
+
+
+def pin_decision_threshold(ora):
+    m = M_BD
+    w, _ = weights(m, 31)
+    base, blob0 = _without_decision(w, m)
+    fr = mixed_frames(m, 8, 4, seed=31)
+    for theta in (0.3, 0.8, 0.95):
+        want = ora.encode(fr, blob0, base.as_dict(), 4, tau=theta)
+        c = want["cos"][~np.isnan(want["cos"])]
+        assert np.min(np.abs(c - theta)) > 1e-9, "threshold too close to a cosine"
+        blob, th = linear_decision(w, m, 0, 5.0, theta)
+        assert np.min(np.abs(c - th)) > 1e-9
+        r = ora.encode(fr, blob, m.as_dict(), 4, tau=0.0)
+        assert np.array_equal(r["masks"], want["masks"]), f"maps differ at theta={theta}"
+        assert np.array_equal(r["tokens"], want["tokens"]), f"tokens differ at theta={theta}"
+        ev = ~np.isnan(r["cos"])
+        _close(r["dec"][ev], 5.0 * (r["cos"][ev] - th), 1e-12, "decision values")
+
+
+def pin_decision_attention(ora):
+    m = M_BD
+    N = m.n_tokens
+    w, _ = weights(m, 32)
+    fr = mixed_frames(m, 4, 4, seed=32)
+    x0 = torch_ref.embed(fr, w, m).numpy()
+    t0 = [torch_ref.cls_attention(x0[f], x0[f], w, 0, m) for f in range(4)]
+    # threshold above the first layer's uniform 1/N: nothing reused at layer 0
+    blob, theta = linear_decision(w, m, 1, 1.0, 1.02 / N)
+    assert min(np.min(np.abs(t[1:] - theta)) for t in t0[1:]) > 1e-9
+    r = ora.encode(fr, blob, m.as_dict(), 4, tau=0.0)
+    assert not r["masks"][:, 0].any(), "t = 1/N at the first layer"
+    _close(r["dec"][1:, 0, 1:], np.full((3, N - 1), 1.0 / N - theta), 1e-12, "layer-0 decisions")
+    for f in (1, 2, 3):   # layer 1: the class token's attention in frame f's (dense) layer 0
+        _close(r["dec"][f, 1, 1:], t0[f][1:] - theta, 1e-12, f"layer-1 decisions, frame {f}")
+        assert np.array_equal(r["masks"][f, 1, 1:] != 0, t0[f][1:] > theta)
+    assert 0 < r["masks"][:, 1].mean() < 0.75, "want a mixed map at layer 1"
+    # an injected reuse at layer 0: the class query of frame 1 sees the reference's key/value
+    j = 3
+    mk = np.zeros((4, m.depth, N), np.uint8)
+    mk[1, 0, j] = 1
+    r = ora.encode(fr, blob, m.as_dict(), 4, masks=mk)
+    xs = x0[1].copy()
+    xs[j] = x0[0, j]
+    t = torch_ref.cls_attention(x0[1], xs, w, 0, m)
+    _close(r["dec"][1, 1, 1:], t[1:] - theta, 1e-12, "layer-1 decisions after an injected reuse")
+    # below 1/N: everything reused at layer 0
+    blob, _ = linear_decision(w, m, 1, 1.0, 0.98 / N)
+    r = ora.encode(fr, blob, m.as_dict(), 4, tau=0.0)
+    assert r["masks"][1:, 0, 1:].all() and not r["masks"][:, :, 0].any()
+
+
+def pin_decision_type(ora):
+    m = M_BD
+    w, _ = weights(m, 33)
+    fr = mixed_frames(m, 6, 3, seed=33)
+    cfg = m.as_dict()
+    cases = ((3, 0.5, np.inf),      # P entry: d = +0.5 for every non-reference token
+             (2, 0.5, -np.inf),     # I entry: d = -0.5
+             (3, 1.0, -np.inf))     # P entry, d == 0 exactly: the tie recomputes
+    for col, theta, same_as in cases:
+        blob, _ = linear_decision(w, m, col, 1.0, theta)
+        r = ora.encode(fr, blob, cfg, 3, tau=0.0)
+        want = ora.encode(fr, blob, cfg, 3, tau=same_as)
+        assert np.array_equal(r["masks"], want["masks"]), f"maps (column {col}, theta {theta})"
+        assert np.array_equal(r["tokens"], want["tokens"]), f"tokens (column {col})"
+    ev = ~np.isnan(r["dec"])
+    assert ev.any() and np.all(r["dec"][ev] == 0.0)
+
+
+def pin_decision_mlp(ora):
+    m = M_BD
+    N = m.n_tokens
+    w, blob = weights(m, 34)
+    fr = mixed_frames(m, 6, 3, seed=34)
+    r = ora.encode(fr, blob, m.as_dict(), 3, tau=0.0)
+    x0 = torch_ref.embed(fr, w, m).numpy()
+    for f in (1, 2, 4, 5):
+        a, b = x0[f, 1:], x0[f - f % 3, 1:]
+        s = np.sum(a * b, 1) / (np.linalg.norm(a, axis=1) * np.linalg.norm(b, axis=1))
+        v = np.zeros((N - 1, 6))
+        v[:, 0], v[:, 1], v[:, 3] = s, 1.0 / N, 1.0
+        _close(r["dec"][f, 0, 1:], torch_ref.decision_mlp(v, w, 0), 1e-12, f"frame {f}")
+    dv = r["dec"][~np.isnan(r["dec"])]
+    assert np.ptp(dv) > 0.1, "decision values should spread"
+
+
+def pin_decision_brute(ora):
+    for m, G in ((M_AD, 4), (M_BD, 3), (M_BRD, 3)):
+        w, blob = weights(m, 35)
+        fr = mixed_frames(m, 7, G, seed=35)
+        cfg = m.as_dict()
+        r0 = ora.encode(fr, blob, cfg, G, tau=0.0)
+        dv = r0["dec"][~np.isnan(r0["dec"])]
+        for tau in (np.quantile(dv, 0.3), np.quantile(dv, 0.7), np.inf, -np.inf):
+            tau = float(tau)
+            r = ora.encode(fr, blob, cfg, G, tau=tau)
+            b = encode_bruteforce(fr, blob, cfg, G, tau=tau)
+            assert np.array_equal(r["masks"], b["masks"]), f"masks differ at tau={tau}"
+            _close(r["tokens"], b["tokens"], 1e-12, f"tokens tau={tau}")
+            _close(r["emb"], b["emb"], 1e-12, f"emb tau={tau}")
+
+
 ALL_PINS = [pin_library, pin_dense_vit, pin_bruteforce, pin_copy, pin_ref_dense, pin_monotone,
             pin_static, pin_g1, pin_groups, pin_inject_one, pin_extremes, pin_star, pin_cosine,
             pin_partial, pin_rate, pin_restore_zero, pin_restore_brute, pin_restore_one,
-            pin_restore_static]
+            pin_restore_static, pin_decision_threshold, pin_decision_attention, pin_decision_type,
+            pin_decision_mlp, pin_decision_brute]

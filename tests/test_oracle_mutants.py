@@ -48,6 +48,17 @@ MUTANTS = [
      'np.maximum(dx @ P["W_r1"].T + P["b_r1"], 0.0)'),
     ("restore_output_difference", "x[f, Rr] - x[r, Rr]", "y[f, Rr] - y[r, Rr]"),
     ("restore_all_rows", "Rr = np.flatnonzero(m)", "Rr = np.arange(m.size)"),
+    ("decision_features_swapped", "v = np.concatenate([s[:, None], t[:, None], r], axis=1)",
+     "v = np.concatenate([t[:, None], s[:, None], r], axis=1)"),
+    ("decision_type_b_dist2", "r[:, ftype] = 1.0", "r[:, ftype + 1] = 1.0"),
+    ("decision_relu", 'gelu(v @ P["W_d1"].T + P["b_d1"])', 'np.maximum(v @ P["W_d1"].T + P["b_d1"], 0)'),
+    ("decision_output_bias_dropped", '@ P["W_d2"].T + P["b_d2"])', '@ P["W_d2"].T)'),
+    ("decision_tie_reuses", "return d > tau", "return d >= tau"),
+    ("decision_attention_not_advanced", "        t_cls = t_next\n", "\n"),
+    ("decision_attention_summed_over_heads", "(out, p0 / heads)", "(out, p0)"),
+    ("decision_attention_from_reference", "t_next[f] = p_c", "t_next[f] = p_r"),
+    ("decision_attention_starts_at_zero", "np.full((F, N), 1.0 / N)", "np.zeros((F, N))"),
+    ("decision_attention_of_last_query", "p0 += pr[0]", "p0 += pr[-1]"),
 ]
 
 

@@ -82,3 +82,29 @@ def restoration(dx, w, l):
         l2.weight.copy_(t(w[f"l{l}.W_r2"]))
         l2.bias.copy_(t(w[f"l{l}.b_r2"]))
         return l2(torch.nn.functional.gelu(l1(t(dx)), approximate="none")).numpy()
+
+
+def cls_attention(x_q, x_kv, w, l, m):
+    """Attention weights of query 0 (the class token) over all keys in layer l, averaged over
+    the heads, from torch's MultiheadAttention: queries from LN1 of the rows x_q [N, D], keys
+    and values from LN1 of the rows x_kv [N, D] (numpy); returns numpy float64 [N]."""
+    lay = encoder_layer(w, l, m)
+    with torch.no_grad():
+        hq = lay.norm1(torch.tensor(np.asarray(x_q, dtype=np.float64))[None])
+        hk = lay.norm1(torch.tensor(np.asarray(x_kv, dtype=np.float64))[None])
+        a = lay.self_attn(hq, hk, hk, need_weights=True, average_attn_weights=True)[1]
+    return a[0, 0].numpy()
+
+
+def decision_mlp(v, w, l):
+    """Decision MLP of layer l (torch Linear -> exact GELU -> Linear) on features v [n, 6]
+    (numpy); returns numpy float64 [n]."""
+    t = lambda a: torch.tensor(np.asarray(a, dtype=np.float64))  # noqa: E731
+    l1 = torch.nn.Linear(w[f"l{l}.W_d1"].shape[1], w[f"l{l}.W_d1"].shape[0], dtype=torch.float64)
+    l2 = torch.nn.Linear(w[f"l{l}.W_d2"].shape[1], 1, dtype=torch.float64)
+    with torch.no_grad():
+        l1.weight.copy_(t(w[f"l{l}.W_d1"]))
+        l1.bias.copy_(t(w[f"l{l}.b_d1"]))
+        l2.weight.copy_(t(w[f"l{l}.W_d2"]))
+        l2.bias.copy_(t(w[f"l{l}.b_d2"]))
+        return l2(torch.nn.functional.gelu(l1(t(v)), approximate="none"))[:, 0].numpy()
