@@ -164,10 +164,11 @@ def traffic_record(fetch_csv, write_csv, bench_json, cmds):
     return out
 
 
-def calibrate(enc, x, G, target, iters=24):
-    """Bisection of tau in [-1, 1] so that the batch's reuse rate is within 0.01 of target."""
+def calibrate(enc, x, G, target, iters=24, lo=-1.0, hi=1.0):
+    """Bisection of tau in [lo, hi] so that the batch's reuse rate is within 0.01 of target
+    (the cosine gate's tau lies in [-1, 1]; the decision MLP's threshold on d is wider)."""
     import torch
-    lo, hi = -1.0, 1.0            # reuse(lo) high, reuse(hi) low
+    # reuse(lo) high, reuse(hi) low
     best = None
     for _ in range(iters):
         mid = 0.5 * (lo + hi)
@@ -219,6 +220,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--restore", action="store_true",
                     help="with the restoration layer on reused tokens (random restoration weights)")
+    ap.add_argument("--decision", action="store_true",
+                    help="gate with the learned decision MLP (random decision weights; the "
+                         "threshold on its output is calibrated like tau)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device-to-device copy (HBM counter calibration)")
     ap.add_argument("--traffic-record", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_OUT"),
@@ -248,6 +252,10 @@ def main():
         import dataclasses
         m = dataclasses.replace(m, restore=True)
         w = dataclasses.replace(w, model=m)
+    if args.decision:
+        import dataclasses
+        m = dataclasses.replace(m, decision=True)
+        w = dataclasses.replace(w, model=m)
     G, F = w.group_size, w.batch_frames
     t0 = time.time()
     blob = synth.make_blob(m, w.weight_seed)
@@ -261,7 +269,8 @@ def main():
         if tgt is None:
             tau, rho = float(np.float32(w.tau)), None
         else:
-            tau, rho = calibrate(enc, x, G, tgt)
+            bracket = {"lo": -16.0, "hi": 16.0} if m.decision else {}
+            tau, rho = calibrate(enc, x, G, tgt, **bracket)
         taus.append(float(np.float32(tau)))
         rhos.append(rho)
         log(f"[bench] target reuse {tgt}: tau {tau:.6f} -> reuse {rho}")
@@ -385,6 +394,8 @@ def main():
                                f"{m.depth}, width {D}, {m.heads} heads, MLP {m.mlp}; {F} frames "
                                f"per batch, groups of {G}; "
                                + ("restoration MLP (hidden 128) on reused tokens; " if m.restore
+                                  else "")
+                               + ("learned decision MLP gate (hidden 64); " if m.decision
                                   else "")
                                + "reuse levels "
                                + "/".join(f"{t:.0%}" for t in targets if t is not None),

@@ -17,7 +17,8 @@
  *     Eq. 1 with one reference and the hard gate M_i = [d_i > 0]) with the
  *     learned decision MLP replaced by a threshold: token i of a
  *     non-reference frame is reused when cos(x_f[i], x_ref[i]) >= tau, on the
- *     layer input x (residual stream).  The class token is never reused.
+ *     layer input x (residual stream) -- or, with DV_FLAG_DECISION, by the
+ *     decision MLP itself.  The class token is never reused.
  *   - Token filtration (Section 3.3): recompute tokens are stream-compacted
  *     across all frames of the batch into dense rows (sparse computation
  *     compaction, Section 5.3) and run the whole encoder layer (QKV
@@ -79,7 +80,7 @@ typedef struct dv_config {
     int mlp;               /* Dm: MLP hidden width */
     int dtype;             /* DV_F32 or DV_BF16 */
     int max_batch_frames;  /* frames per internal batch (rounded down to whole groups per call) */
-    unsigned flags;        /* 0 or DV_FLAG_RESTORE; other bits reserved (must be 0) */
+    unsigned flags;        /* DV_FLAG_RESTORE | DV_FLAG_DECISION or 0; other bits must be 0 */
 } dv_config;
 
 /* Restoration layer on reused tokens (Section 3.3): after each layer, a reused token i of a
@@ -91,6 +92,23 @@ typedef struct dv_config {
 #define DV_FLAG_RESTORE 1u
 #define DV_RESTORE_HIDDEN 128   /* hidden width of the restoration MLP */
 
+/* Learned decision layer as the gate (Section 3.3, decision-layer equations).  In gate mode
+ * token i of a non-reference frame f is reused at layer l when d_i > tau, where
+ *   d_i = w_2 . GELU(W_1 v_i + b_1) + b_2,   v_i = (s_i, t_i, r_I, r_P, r_B2, r_B1),
+ *   s_i  cosine of x_f[i] and x_ref[i] (the convention below),
+ *   t_i  the class token's attention weight on token i in frame f's layer l-1, averaged over
+ *        the heads (1/N at layer 0),
+ *   r    one-hot frame type: every non-reference frame references its group's first frame
+ *        alone, the role of a P frame, so r = (0, 1, 0, 0);
+ * the codec-metadata cue has no input.  tau = 0 is the paper's rule; other finite values move
+ * the operating point; -INFINITY and +INFINITY keep their meanings.  GELU is the exact erf
+ * form; d is computed in fp32.  The decision is not monotone over layers: every token is gated
+ * at every layer, and a reused token's row is the reference's layer output (restored with
+ * DV_FLAG_RESTORE).  The weights follow the base blob and the restoration section. */
+#define DV_FLAG_DECISION 2u
+#define DV_DECISION_HIDDEN 64     /* hidden width of the decision MLP */
+#define DV_DECISION_FEATURES 6    /* its input width: s, t and the four frame types */
+
 typedef struct dv_handle dv_handle;
 
 /* Number of floats the weight blob of `cfg` must hold (0 if cfg is NULL or invalid).
@@ -101,6 +119,8 @@ typedef struct dv_handle dv_handle;
  *   lnf_g [D], lnf_b [D]
  *   with DV_FLAG_RESTORE, then per layer: W_r1 [R,D], b_r1 [R], W_r2 [D,R], b_r2 [D]
  *   (R = DV_RESTORE_HIDDEN)
+ *   with DV_FLAG_DECISION, then per layer: W_d1 [Hd,6], b_d1 [Hd], W_d2 [1,Hd], b_d2 [1]
+ *   (Hd = DV_DECISION_HIDDEN; kept in fp32 for every dtype)
  * Linear layers map x -> x W^T + b.  W_qkv rows: Q, then K, then V; heads are
  * contiguous slices of D/H rows within each.  LayerNorm eps is 1e-5. */
 size_t dv_weights_floats(const dv_config* cfg);
@@ -133,7 +153,8 @@ int dv_workspace_bytes(const dv_handle* h, size_t* bytes);
  * max_batch_frames.  tau = -INFINITY turns reuse off (the same kernels run
  * densely, masks all 0); tau = +INFINITY reuses every non-class token of
  * every non-reference frame; a finite tau applies the rule above
- * (tau > 1 reuses nothing, tau <= -1 everything).  NaN tau -> DV_EINVAL.
+ * (tau > 1 reuses nothing, tau <= -1 everything) or, with DV_FLAG_DECISION,
+ * the decision MLP's rule d_i > tau.  NaN tau -> DV_EINVAL.
  * Enqueued on `stream`, asynchronous, no host synchronisation.
  * Errors: DV_EINVAL (null handle/frames/embeddings, n_frames < 1,
  * group_size < 1 or > max_batch_frames, NaN tau), DV_EHIP. */
@@ -188,8 +209,9 @@ int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size,
 #define DV_STAGE_MERGE 10
 #define DV_STAGE_FINAL 11
 #define DV_STAGE_RESTORE 12   /* the two restoration GEMMs (DV_FLAG_RESTORE) */
-#define DV_NUM_STAGES 13
-#define DV_PROFILE_ALL 0x1FFF
+#define DV_STAGE_CLS 13       /* class-token attention weights for the decision MLP */
+#define DV_NUM_STAGES 14
+#define DV_PROFILE_ALL 0x3FFF
 int dv_profile(dv_handle* h, unsigned stage_mask);
 /* total_ms: summed event time of the stage's launches; launches: how many. */
 int dv_profile_read(dv_handle* h, int stage, double* total_ms, long long* launches);

@@ -231,6 +231,7 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
       cos    [F, L, N]   cosine to the reference token (NaN where not evaluated)
       dec    [F, L, N]   decision-MLP output d_i (only with cfg["decision"]; NaN where not
                          evaluated)
+      t      [F, L, N]   its class-token attention input t_i (same conditions)
       tokens [F, N, D]   output of the last layer
       layers (optional)  list of the L+1 token buffers x^0..x^L
     """
@@ -248,6 +249,7 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
     out_c = np.full((F, L, N), np.nan)
     decide = bool(cfg.get("decision"))
     out_d = np.full((F, L, N), np.nan) if decide else None
+    out_t = np.full((F, L, N), np.nan) if decide else None
     t_cls = np.full((F, N), 1.0 / N) if decide else None  # class-token attention, previous layer
     hist = [x.copy()] if return_layers else None
 
@@ -268,6 +270,7 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
                 if decide:
                     dv = decision_values(c, t_cls[f, 1:], frame_type(f, G), P)
                     out_d[f, l, 1:] = dv
+                    out_t[f, l, 1:] = t_cls[f, 1:]
                 if masks is not None:
                     reuse = np.asarray(masks[f, l, 1:]) != 0
                 elif decide:
@@ -298,6 +301,7 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
     res = {"emb": emb, "masks": out_m, "cos": out_c, "tokens": x}
     if decide:
         res["dec"] = out_d
+        res["t"] = out_t
     if return_layers:
         res["layers"] = hist
     return res

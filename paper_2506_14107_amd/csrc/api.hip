@@ -13,13 +13,19 @@
 //     [restoration: the gate also writes x_f - x_ref of every reused token, the compaction the
 //      reused-token list; a D -> 128 GEMM (+bias, GELU) on those rows runs before QKV and a
 //      128 -> D GEMM (+bias, + the reference token's new row) after FC2 writes the reused rows]
+//     [decision MLP: the gate evaluates it on (cosine, class-token attention of the previous
+//      layer, frame type); after attention the class-token weights of every frame are
+//      computed for the next layer]
 //   final LayerNorm of the class tokens.
 // Nothing is read back to the host inside an encode call.
 //
 // Gate mode needs no merge pass: once a token is reused its row would be a copy of the
 // reference's, whose cosine is exactly 1, so it stays reused in every later layer; the gate
 // answers such tokens from the previous layer's map and nobody reads their rows again.  Only
-// when the caller asks for the full token buffer are those rows filled in at the end.
+// when the caller asks for the full token buffer are those rows filled in at the end.  Under
+// the decision MLP a reused token may be recomputed later (its other cues change): its cosine
+// is still exactly 1, and when the MLP recomputes it the gate first copies the reference's
+// row into it.
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -64,12 +70,14 @@ struct LayerW {
     const void *W_qkv, *W_o, *W_1, *W_2;
     const void *W_r1, *W_r2;      // restoration MLP (DV_FLAG_RESTORE), else null
     const float *b_r1, *b_r2;
+    const float* dec;             // decision MLP (DV_FLAG_DECISION): DEC_FLOATS fp32, else null
 };
 
 struct Dims {
     int S, p, L, D, H, Dm, N, P, Kp, B;
     bool bf16;
     bool restore;   // DV_FLAG_RESTORE
+    bool decision;  // DV_FLAG_DECISION
 };
 
 constexpr int RH = DV_RESTORE_HIDDEN;
@@ -81,7 +89,8 @@ int check_config(const dv_config* c, Dims* d) {
         c->mlp < 1 || c->max_batch_frames < 1)
         return fail(DV_EINVAL, "config sizes must be >= 1");
     if (c->dtype != DV_F32 && c->dtype != DV_BF16) return fail(DV_EINVAL, "unknown dtype %d", c->dtype);
-    if (c->flags & ~DV_FLAG_RESTORE) return fail(DV_EUNSUPPORTED, "unknown flag bits 0x%x", c->flags);
+    if (c->flags & ~(DV_FLAG_RESTORE | DV_FLAG_DECISION))
+        return fail(DV_EUNSUPPORTED, "unknown flag bits 0x%x", c->flags);
     if (c->image_size % c->patch) return fail(DV_EUNSUPPORTED, "image_size %% patch != 0");
     if (c->width % c->heads) return fail(DV_EUNSUPPORTED, "width %% heads != 0");
     const int dh = c->width / c->heads;
@@ -104,6 +113,7 @@ int check_config(const dv_config* c, Dims* d) {
     d->B = c->max_batch_frames;
     d->bf16 = bf;
     d->restore = (c->flags & DV_FLAG_RESTORE) != 0;
+    d->decision = (c->flags & DV_FLAG_DECISION) != 0;
     if (!attention_supported(bf, d->N, dh))
         return fail(DV_EUNSUPPORTED, "attention for N=%d tokens, head dim %d is not supported "
                     "(bf16: head dim 64/80/96/128; keys and values of a head must fit in LDS)", d->N, dh);
@@ -118,7 +128,8 @@ size_t blob_floats(const Dims& d) {
     const size_t D = d.D, Dm = d.Dm, N = d.N, p = d.p;
     size_t per_layer = 2 * D + 3 * D * D + 3 * D + D * D + D + 2 * D + Dm * D + Dm + D * Dm + D;
     const size_t restore = d.restore ? (size_t)d.L * (2 * RH * D + RH + D) : 0;
-    return D * 3 * p * p + D + D + N * D + (size_t)d.L * per_layer + 2 * D + restore;
+    const size_t decision = d.decision ? (size_t)d.L * DEC_FLOATS : 0;
+    return D * 3 * p * p + D + D + N * D + (size_t)d.L * per_layer + 2 * D + restore + decision;
 }
 
 struct Stage {
@@ -149,6 +160,8 @@ struct dv_handle {
     uint8_t* mask[2]; // [T] per-layer maps (ping-pong)
     int *idx, *pos_, *qoff, *cnt, *M;   // M[0]: recomputed rows, M[1]: reused tokens
     int* ridx = nullptr;   // [T] reused tokens (restoration)
+    float* tcls = nullptr; // [B, H, N] class-token attention weights of the last layer, per head
+                           // (decision MLP)
     void* Hr = nullptr;    // [Tp, 128] elem: restoration hidden rows
     int *idx_id, *pos_id, *qoff_id;  // identity lists (reuse off)
     int id_frames = -1;              // frames the identity lists were built for
@@ -250,6 +263,8 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
     const int* Mdev = dense ? nullptr : h->M;
     // restoration of reused rows: on whenever tokens can be reused
     const bool restore = d.restore && !dense;
+    // learned decision gate: gate mode only (injected maps and the sentinels bypass it)
+    const bool decide = d.decision && mode == GATE_COS;
 
     for (int l = 0; l < L; ++l) {
         const LayerW& w = h->layers[l];
@@ -277,6 +292,9 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             ga.ln_b = w.ln1_b;
             ga.ln_out = h->A;   // token-indexed LN1 rows; the QKV GEMM gathers them through idx
             ga.d_out = restore ? h->A : nullptr;   // reused tokens' differences, same buffer
+            ga.dec = decide ? w.dec : nullptr;
+            ga.tcls = (decide && l > 0) ? h->tcls : nullptr;
+            ga.H = d.H;
             launch_gate(bf, ga, s);
         }
         if (!dense) {
@@ -318,21 +336,25 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             g.out = h->qkv;
             launch_gemm(Epi::Qkv, bf, g, s);
         }
+        g.a_idx = nullptr;
+        AttnArgs at{};
+        at.qkv = h->qkv;
+        at.pos = pos;
+        at.qoff = qoff;
+        at.out = h->O;
+        at.F = F;
+        at.N = N;
+        at.D = D;
+        at.H = d.H;
+        at.G = dense ? 0 : G;
+        at.cus = h->cus;
         {
-            g.a_idx = nullptr;
             Scope sc(h, DV_STAGE_ATTN, s);
-            AttnArgs at{};
-            at.qkv = h->qkv;
-            at.pos = pos;
-            at.qoff = qoff;
-            at.out = h->O;
-            at.F = F;
-            at.N = N;
-            at.D = D;
-            at.H = d.H;
-            at.G = dense ? 0 : G;
-            at.cus = h->cus;
             launch_attention(bf, at, s);
+        }
+        if (decide && l + 1 < L) {   // the next layer's importance cue
+            Scope sc(h, DV_STAGE_CLS, s);
+            launch_cls_attention(bf, at, h->tcls, s);
         }
         {
             Scope sc(h, DV_STAGE_OPROJ, s);
@@ -510,6 +532,8 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
         r.W_r2 = reserve(D * RH * el);
         r.b_r2 = reserve(D * 4);
     }
+    std::vector<size_t> dco(d.decision ? L : 0);
+    for (auto& o : dco) o = reserve(DEC_FLOATS * 4);
     try {
         host.assign(wbytes, 0);
     } catch (const std::bad_alloc&) {
@@ -555,6 +579,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
         put_mat(r.W_r2, D, RH, RH);
         put_vec(r.b_r2, D);
     }
+    for (auto o : dco) put_vec(o, DEC_FLOATS);   // W_d1, b_d1, W_d2, b_d2 as the kernel reads them
 
     dv_handle* h = new (std::nothrow) dv_handle();
     if (!h) return fail(DV_ENOMEM, "handle");
@@ -609,6 +634,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
             w.W_r2 = wb + ro[l].W_r2;
             w.b_r2 = (const float*)(wb + ro[l].b_r2);
         }
+        w.dec = d.decision ? (const float*)(wb + dco[l]) : nullptr;
     }
 
     // --- workspace ----------------------------------------------------------------------------
@@ -635,6 +661,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
         sz(T * 4);             // ridx
         sz(Tp * RH * el);      // Hr
     }
+    if (d.decision) sz(T * d.H * 4);   // tcls
     {
         hipError_t e = hipMalloc(&h->ws, need);
         if (e != hipSuccess) {
@@ -668,6 +695,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
         h->ridx = carve<int>(p, T);
         h->Hr = carve<char>(p, Tp * RH * el);
     }
+    if (d.decision) h->tcls = carve<float>(p, T * d.H);
     *out = h;
     return DV_OK;
 }

@@ -14,12 +14,15 @@
 //                      ds_read_b64_tr_b16; B = the probabilities as they sit in the S^T
 //                      accumulators; the contraction runs over the 32 keys in the order the
 //                      accumulator layout gives (the same order on both operands)
-// so a lane rescales and normalises its own query's output without any shuffle.  When a frame
-// has fewer query tiles than wavefronts, the key blocks of a tile are split across wavefronts
-// and their partial (max, sum, output) states are merged through LDS.
+// so a lane rescales and normalises its own query's output without any shuffle.  A query tile is
+// always taken by one wavefront over all key blocks in order, whatever kernel runs it and however
+// many other queries its frame has, so a row's result depends only on its query and the frame's
+// keys and values (no split of the keys across wavefronts, whose merge would round the
+// probabilities against partial maxima).
 //
 // fp32 path: scalar scores, softmax and P.V (small fp32 models).
 #include <algorithm>
+#include <type_traits>
 
 #include "dv_internal.h"
 
@@ -106,14 +109,14 @@ constexpr int AW = 8;    // wavefronts of a per-frame attention block
 constexpr int UW = 16;   // wavefronts of a per-unit attention block
 
 // Online-softmax attention of one query tile (fragments qf, one query per lane) against the
-// staged K/V: key blocks kb = sp, sp + S, ... taken two at a time (kb, kb + S) -- two
-// independent MFMA chains and one rescale per step.  krow maps a key to its LDS row.  On
+// staged K/V: key blocks taken two at a time in order (kb, kb + 1) -- two independent MFMA
+// chains and one rescale per step.  krow maps a key to its LDS row.  On
 // return (m, l, o) hold the tile's running max (raw score units), sum and unnormalised output.
 // The arithmetic and its order depend only on the key values, never on where the rows sit.
 template <int DH, class KRow>
 __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, const uint16_t* Vs,
-                                            int N, int lane, const bf16x8 (&qf)[DH / 16], int sp,
-                                            int S, KRow krow, float& m, float& l,
+                                            int N, int lane, const bf16x8 (&qf)[DH / 16],
+                                            KRow krow, float& m, float& l,
                                             f32x16 (&o)[(DH + 31) / 32]) {
     constexpr int KS = DH / 16;          // k-steps of S^T
     constexpr int DB = (DH + 31) / 32;   // 32-row blocks of O^T
@@ -176,8 +179,8 @@ __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, co
         for (int r = 0; r < 16; ++r) o[b][r] = 0.f;
     m = -INFINITY;
     l = 0.f;
-    for (int kb = sp; kb < nkb; kb += 2 * S) {
-        const int kb1 = kb + S;
+    for (int kb = 0; kb < nkb; kb += 2) {
+        const int kb1 = kb + 1;
         const bool two = kb1 < nkb;
         const f32x16 s0 = scores(kb);
         f32x16 s1;
@@ -237,8 +240,7 @@ __device__ __forceinline__ void store_row(uint16_t* dst, int lane, float l,
 }
 
 // ---- per-frame items ---------------------------------------------------------------------------
-// Work split: T = ceil(q/32) query tiles over AW wavefronts.  With T < AW a tile's key blocks
-// are split S = AW / T ways and the partial softmax states are merged through LDS.
+// Work split: T = ceil(q/32) query tiles over AW wavefronts, each tile over all key blocks.
 template <int DH>
 __device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char* smem);
 
@@ -295,8 +297,6 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char*
     const int ntile = (q1 - q0 + 31) / 32;
     if (ntile == 0) return;
 
-    const int S = ntile >= AW ? 1 : AW / ntile;   // key-block split per tile
-
     // stage K and V rows (row-major, 16-byte chunks); keys past N repeat key N-1 (finite data
     // whose scores are masked).  Up to four chunks per thread are gathered before any store.
     const int total = g.npad * CH;
@@ -326,65 +326,17 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char*
     }
     lds_barrier();
 
-    float m = -INFINITY, l = 0.f;   // running max (raw score units) and sum
+    float m, l;   // running max (raw score units) and sum
     f32x16 o[DB];
-    int my_t = -1;
-    for (int item = wave; item < ntile * S; item += AW) {
-        const int t = item / S, sp = item % S;
-        my_t = t;
+    for (int t = wave; t < ntile; t += AW) {
         const int myq = q0 + t * 32 + lr;
         const int qrow = myq < q1 ? myq : q1 - 1;   // tail lanes compute on a valid row
         bf16x8 qf[KS];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
             qf[ks] = *(const bf16x8*)(qkv + (size_t)qrow * ld3 + h * DH + ks * 16 + hl * 8);
-        attend_tile<DH>(g, Ks, Vs, N, lane, qf, sp, S, [](int k) { return k; }, m, l, o);
-        if (S == 1 && myq < q1) store_row<DH>((uint16_t*)a.out + (size_t)myq * D + h * DH, lane, l, o);
-    }
-    if (S == 1) return;   // uniform across the block: S depends only on the frame
-    const float sl2 = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(dh)
-
-    // merge the S partial states of each tile (LDS reused: K/V are no longer read)
-    lds_barrier();
-    float* part = (float*)smem;                       // [AW][2 + DB*32][32] floats
-    constexpr int STRIDE = (2 + DB * 32) * 32;
-    if (my_t >= 0) {
-        float* pw = part + wave * STRIDE;
-        if (hl == 0) {
-            pw[lr] = m;
-            pw[32 + lr] = l;
-        }
-#pragma unroll
-        for (int b = 0; b < DB; ++b)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int d = b * 32 + (r >> 2) * 8 + hl * 4 + (r & 3);
-                pw[(2 + d) * 32 + lr] = o[b][r];
-            }
-    }
-    lds_barrier();
-    // every thread merges 4 output dims of one query: the S partial states of tile t sit in the
-    // slots of waves t*S .. t*S+S-1
-    constexpr int DC = DH / 4;
-    for (int i = tid; i < ntile * 32 * DC; i += NT) {
-        const int t = i / (32 * DC), rest = i % (32 * DC);
-        const int q = rest % 32, dc = rest / 32;
-        const int myq = q0 + t * 32 + q;
-        if (myq >= q1) continue;
-        const float* pt = part + (size_t)t * S * STRIDE;
-        float M = -INFINITY;
-        for (int sp = 0; sp < S; ++sp) M = fmaxf(M, pt[sp * STRIDE + q]);
-        float L = 0.f, v[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int sp = 0; sp < S; ++sp) {
-            const float* ps = pt + sp * STRIDE;
-            const float w = __builtin_amdgcn_exp2f((ps[q] - M) * sl2);
-            L += w * ps[32 + q];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] += w * ps[(2 + dc * 4 + e) * 32 + q];
-        }
-        const float inv = 1.0f / L;
-        *(uint2*)((uint16_t*)a.out + (size_t)myq * D + h * DH + dc * 4) =
-            pack_bf16x4(v[0] * inv, v[1] * inv, v[2] * inv, v[3] * inv);
+        attend_tile<DH>(g, Ks, Vs, N, lane, qf, [](int k) { return k; }, m, l, o);
+        if (myq < q1) store_row<DH>((uint16_t*)a.out + (size_t)myq * D + h * DH, lane, l, o);
     }
 }
 
@@ -509,10 +461,10 @@ void attn_unit_k(AttnArgs a, int pcap) {
                 float m, l;
                 f32x16 o[DB];
                 if (jj < 0) {
-                    attend_tile<DH>(g, Ks, Vs, N, lane, qf, 0, 1, [](int k) { return k; }, m, l, o);
+                    attend_tile<DH>(g, Ks, Vs, N, lane, qf, [](int k) { return k; }, m, l, o);
                 } else {
                     const uint16_t* km = kmap + jj * g.npad;
-                    attend_tile<DH>(g, Ks, Vs, N, lane, qf, 0, 1, [=](int k) { return (int)km[k]; },
+                    attend_tile<DH>(g, Ks, Vs, N, lane, qf, [=](int k) { return (int)km[k]; },
                                     m, l, o);
                 }
                 if (myq < q1) store_row<DH>((uint16_t*)a.out + (size_t)myq * D + h * DH, lane, l, o);
@@ -577,6 +529,106 @@ __global__ __launch_bounds__(256) void attn_f32_k(AttnArgs a) {
     }
 }
 
+// ---- class-token attention weights (the decision MLP's importance cue) ------------------------
+// One wavefront per (non-reference frame, head): the class query's scores against the frame's N
+// keys (read through pos), then their softmax.  Eight lanes share a key: each multiplies one or
+// more 16-byte chunks of the key row with the matching chunks of the query (held in registers),
+// so a wavefront reads eight key rows per step in whole 128-byte segments; the eight partial
+// sums meet in three shuffles.  Four heads per block, no block barriers (each wavefront has its
+// own LDS slice).
+template <bool BF>
+__device__ inline float elem_at(const void* p, size_t i) {
+    if constexpr (BF) return bf16_to_f32(((const uint16_t*)p)[i]);
+    else return ((const float*)p)[i];
+}
+
+template <bool BF>
+__global__ __launch_bounds__(256) void cls_attn_k(AttnArgs a, float* __restrict__ out) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    constexpr int CE = BF ? 8 : 4;            // elements per 16-byte chunk
+    constexpr int U = 128 / CE / 8;           // chunks per lane for a head dim of up to 128
+    constexpr int KB = 4;                     // steps of eight keys whose loads are in flight together
+    const int f = blockIdx.x;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int h = blockIdx.y * 4 + wave;
+    if ((a.G > 0 && f % a.G == 0) || h >= a.H) return;   // reference frames are never gated
+    const int N = a.N, D = a.D, dh = D / a.H, nch = dh / CE;
+    const int sub = lane & 7, kq = lane >> 3;
+    float* sc = (float*)smem + (size_t)wave * N;   // scores, then exponentials
+    const size_t ld3 = 3 * (size_t)D;
+    const size_t qrow = (size_t)a.qoff[f] * ld3 + (size_t)h * dh;   // the frame's first row
+    float q[U][CE];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int e = 0; e < CE; ++e) {
+            const int c = sub + 8 * u;
+            q[u][e] = c < nch ? elem_at<BF>(a.qkv, qrow + (size_t)c * CE + e) : 0.f;
+        }
+    const float scale = 1.0f / sqrtf((float)dh);
+    typedef typename std::conditional<BF, uint4, float4>::type chunk_t;
+    for (int j0 = 0; j0 < N; j0 += 8 * KB) {
+        // KB steps of eight keys at once: every row offset, then every chunk, then the sums
+        size_t kr[KB];
+#pragma unroll
+        for (int t = 0; t < KB; ++t) {
+            const int j = j0 + 8 * t + kq;
+            kr[t] = j < N ? (size_t)a.pos[(size_t)f * N + j] * ld3 + D + (size_t)h * dh : 0;
+        }
+        chunk_t kv[KB][U];
+#pragma unroll
+        for (int t = 0; t < KB; ++t)
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int c = sub + 8 * u, j = j0 + 8 * t + kq;
+                if (j < N && c < nch) {
+                    kv[t][u] = *(const chunk_t*)((const char*)a.qkv +
+                                                 (kr[t] + (size_t)c * CE) * (BF ? 2 : 4));
+                } else {
+                    kv[t][u] = chunk_t{0, 0, 0, 0};
+                }
+            }
+#pragma unroll
+        for (int t = 0; t < KB; ++t) {
+            float s = 0.f;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if constexpr (BF) {
+                    const uint32_t w[4] = {kv[t][u].x, kv[t][u].y, kv[t][u].z, kv[t][u].w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        s = fmaf(q[u][2 * e], bf16_to_f32((uint16_t)(w[e] & 0xFFFFu)), s);
+                        s = fmaf(q[u][2 * e + 1], bf16_to_f32((uint16_t)(w[e] >> 16)), s);
+                    }
+                } else {
+                    s = fmaf(q[u][0], kv[t][u].x, s);
+                    s = fmaf(q[u][1], kv[t][u].y, s);
+                    s = fmaf(q[u][2], kv[t][u].z, s);
+                    s = fmaf(q[u][3], kv[t][u].w, s);
+                }
+            }
+            s += __shfl_xor(s, 1, 64);
+            s += __shfl_xor(s, 2, 64);
+            s += __shfl_xor(s, 4, 64);
+            const int j = j0 + 8 * t + kq;
+            if (sub == 0 && j < N) sc[j] = s * scale;
+        }
+    }
+    wave_lds_sync();
+    float mx = -INFINITY;
+    for (int j = lane; j < N; j += 64) mx = fmaxf(mx, sc[j]);
+    mx = wmax(mx);
+    float sum = 0.f;
+    for (int j = lane; j < N; j += 64) {
+        const float e = expf(sc[j] - mx);
+        sc[j] = e;
+        sum += e;
+    }
+    const float inv = 1.0f / wsum(sum);
+    float* o = out + ((size_t)f * a.H + h) * N;
+    for (int j = lane; j < N; j += 64) o[j] = sc[j] * inv;
+}
+
 size_t f32_lds_bytes(int N, int dh) {
     return ((size_t)N * (dh + 1) + (size_t)N * dh + (size_t)NWAVE * dh + (size_t)NWAVE * N) * 4;
 }
@@ -606,8 +658,7 @@ void launch_bf16(const AttnArgs& a, hipStream_t s) {
             }
         }
     }
-    const size_t merge = (size_t)AW * (2 + (DH + 31) / 32 * 32) * 32 * 4;
-    const size_t lds = std::max(Geo(a.N, DH).bytes(), merge);
+    const size_t lds = Geo(a.N, DH).bytes();
     // work items: (frame, head) pairs; with reuse, the slots of whole units on each of 8 XCDs
     const int items = a.G > 0 ? xcd_unit_grid((a.F + a.G - 1) / a.G * a.H, a.G) : a.F * a.H;
     static int per_cu = -1;
@@ -632,13 +683,15 @@ size_t attention_lds_bytes(bool bf16, int N, int dh) {
 
 bool attention_supported(bool bf16, int N, int dh) {
     if (attention_lds_bytes(bf16, N, dh) > 160 * 1024) return false;
-    if (bf16) {
-        // the merge of split partial states reuses the K/V area
-        const size_t merge = (size_t)AW * (2 + (dh + 31) / 32 * 32) * 32 * 4;
-        return (dh == 64 || dh == 80 || dh == 96 || dh == 128) &&
-               std::max(attention_lds_bytes(true, N, dh), merge) <= 160 * 1024;
-    }
+    if (bf16) return dh == 64 || dh == 80 || dh == 96 || dh == 128;
     return dh % 16 == 0;
+}
+
+void launch_cls_attention(bool bf16, const AttnArgs& a, float* probs, hipStream_t s) {
+    const size_t lds = 4 * (size_t)a.N * sizeof(float);
+    const dim3 grid(a.F, (a.H + 3) / 4);
+    if (bf16) hipLaunchKernelGGL(cls_attn_k<true>, grid, dim3(256), lds, s, a, probs);
+    else hipLaunchKernelGGL(cls_attn_k<false>, grid, dim3(256), lds, s, a, probs);
 }
 
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s) {

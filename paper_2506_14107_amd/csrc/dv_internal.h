@@ -83,6 +83,10 @@ struct AttnArgs {
     int cus;           // compute units of the device (0: one block per work item)
 };
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
+// Class-token attention weights of every non-reference frame (G > 0: frames f % G == 0 are
+// skipped), per head: probs[(f*H + h)*N + j] = softmax_j(q_h . k_h,j / sqrt(dh)) with q the
+// frame's class-token query (its first packed row, qoff[f]) and k_j its key row through pos.
+void launch_cls_attention(bool bf16, const AttnArgs& a, float* probs, hipStream_t s);
 size_t attention_lds_bytes(bool bf16, int N, int dh);
 bool attention_supported(bool bf16, int N, int dh);
 
@@ -94,7 +98,7 @@ void launch_cls_init(float* x, const float* cls, const float* pos, int F, int N,
 
 enum GateMode : int { GATE_COS = 0, GATE_INJECT = 1, GATE_ALL = 2, GATE_NONE = 3 };
 struct GateArgs {
-    const float* x;       // [F*N, D]
+    float* x;             // [F*N, D] (written only to give a recomputed alias its row)
     int F, N, D, G, L, layer;
     int mode;
     float tau;
@@ -108,7 +112,15 @@ struct GateArgs {
     void* ln_out;         // [F*N, D] elem: LN1 rows of recomputed tokens (token-indexed) or nullptr
     void* d_out;          // [F*N, D] elem: x_f - x_ref rows of reused tokens (token-indexed;
                           // restoration) or nullptr.  May be ln_out: the rows are disjoint.
+    const float* dec;     // GATE_COS with the decision MLP: the layer's W_d1 [64,6], b_d1 [64],
+                          // W_d2 [64], b_d2 [1] (fp32, back to back), else nullptr
+    const float* tcls;    // [F, H, N] class-token attention weights of the previous layer, per
+                          // head (nullptr: 1/N); the cue is their mean over the H heads
+    int H;
 };
+constexpr int DEC_HIDDEN = 64;   // decision MLP hidden units: one per lane of a wavefront
+constexpr int DEC_FEAT = 6;      // its features: s, t, one-hot type (I, P, B_dist2, B_dist1)
+constexpr int DEC_FLOATS = DEC_HIDDEN * DEC_FEAT + 2 * DEC_HIDDEN + 1;
 // Mode GATE_NONE marks every token recomputed (reuse off) and only writes LN1 rows.
 // The gate runs in blocks of GATE_TOK tokens; counts are per block: cnt[f * gate_chunks(N) + c].
 constexpr int GATE_TOK = 16;

@@ -64,7 +64,10 @@ __global__ void cls_init_k(float* x, const float* cls, const float* pos, int F, 
 // (already in registers for the cosine) to the token-indexed buffer `ln_out`; with `d_out`
 // (restoration), each reused token's difference to its reference row goes to `d_out`.
 // cnt[f * chunks + block-in-frame] = number of recomputed tokens of that block.
-template <bool BF>
+// With `prev`, a token reused at the previous layer holds no row of its own (it is the
+// reference's row): its cosine is exactly 1.  Under the decision MLP such a token may be
+// recomputed; the gate then writes the reference's row into the token's row first.
+template <bool BF, bool DEC>
 __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     const int N = a.N, D = a.D;
     const int chunks = (N + GATE_TOK - 1) / GATE_TOK;
@@ -77,11 +80,38 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     uint8_t* om = a.out_masks ? a.out_masks + ((size_t)f * a.L + a.layer) * N : nullptr;
     const float4* g4 = (const float4*)a.ln_g;
     const float4* b4 = (const float4*)a.ln_b;
+    // decision MLP (Section 3.3): lane k holds hidden unit k -- its input weights for s and t,
+    // its bias plus the weight of the P entry of the one-hot frame type (every non-reference
+    // frame references its group's first frame alone), and its output weight
+    static_assert(DEC_HIDDEN == WAVE, "one hidden unit per lane");
+    float dw_s = 0.f, dw_t = 0.f, dw_b = 0.f, dw_o = 0.f, db_o = 0.f;
+    if constexpr (DEC) {
+        const float* w1 = a.dec + lane * DEC_FEAT;
+        dw_s = w1[0];
+        dw_t = w1[1];
+        dw_b = a.dec[DEC_HIDDEN * DEC_FEAT + lane] + w1[2 + 1];
+        dw_o = a.dec[DEC_HIDDEN * DEC_FEAT + DEC_HIDDEN + lane];
+        db_o = a.dec[DEC_HIDDEN * DEC_FEAT + 2 * DEC_HIDDEN];
+    }
+    // d = w_2 . GELU(W_1 (s, t, r) + b_1) + b_2 for token i of this frame; t is the mean over
+    // the heads of the class token's attention weight on i in the previous layer (1/N at the
+    // first).  Every lane returns the same d.
+    auto decision = [&](float cs, int i) {
+        float t = 1.0f / (float)N;
+        if (a.tcls) {
+            float p = 0.f;
+            for (int h = lane; h < a.H; h += WAVE) p += a.tcls[((size_t)f * a.H + h) * N + i];
+            t = wave_sum(p) / (float)a.H;
+        }
+        const float z = fmaf(dw_t, t, fmaf(dw_s, cs, dw_b));
+        const float g = 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
+        return wave_sum(dw_o * g) + db_o;
+    };
     int active = 0;
     const int i_end = min(N, (ch + 1) * GATE_TOK);
     for (int i = ch * GATE_TOK + wave; i < i_end; i += nwaves) {
         const size_t row = (size_t)f * N + i;
-        const float4* xf = (const float4*)(a.x + row * D);
+        float4* xf = (float4*)(a.x + row * D);
         int reuse = 0;
         bool loaded = false;
         float4 v[MAX_CHUNKS];
@@ -92,8 +122,24 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
                 reuse = 1;
             } else if (a.mode == GATE_COS) {
                 if (a.prev && a.prev[row]) {
-                    // a reused token holds a copy of the reference's row: cosine exactly 1
-                    reuse = a.tau <= 1.0f;
+                    // a reused token stands for the reference's row: cosine exactly 1
+                    if constexpr (DEC) {
+                        reuse = decision(1.0f, i) > a.tau;
+                        if (!reuse) {   // recomputed again: its row becomes the reference's
+                            const float4* xr = (const float4*)(a.x + ((size_t)r * N + i) * D);
+#pragma unroll
+                            for (int k = 0; k < MAX_CHUNKS; ++k) {
+                                const int c = lane + k * WAVE;
+                                if (c < nchunk) {
+                                    v[k] = xr[c];
+                                    xf[c] = v[k];
+                                }
+                            }
+                            loaded = true;
+                        }
+                    } else {
+                        reuse = a.tau <= 1.0f;
+                    }
                 } else {
                     const float4* xr = (const float4*)(a.x + ((size_t)r * N + i) * D);
                     float dot = 0.f, na = 0.f, nb = 0.f;
@@ -118,7 +164,11 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
                     float cs = dot / fmaxf(sqrtf(na) * sqrtf(nb), 1e-8f);
                     cs = fminf(1.0f, fmaxf(-1.0f, cs));
                     if (same) cs = 1.0f;
-                    reuse = cs >= a.tau;
+                    if constexpr (DEC) {
+                        reuse = decision(cs, i) > a.tau;
+                    } else {
+                        reuse = cs >= a.tau;
+                    }
                 }
             }
         }
@@ -432,8 +482,14 @@ void launch_cls_init(float* x, const float* cls, const float* pos, int F, int N,
 
 void launch_gate(bool bf16, const GateArgs& a, hipStream_t s) {
     const int grid = a.F * gate_chunks(a.N);
-    if (bf16) hipLaunchKernelGGL(gate_k<true>, dim3(grid), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(gate_k<false>, dim3(grid), dim3(256), 0, s, a);
+    const bool dec = a.dec != nullptr && a.mode == GATE_COS;
+    if (bf16) {
+        if (dec) hipLaunchKernelGGL((gate_k<true, true>), dim3(grid), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((gate_k<true, false>), dim3(grid), dim3(256), 0, s, a);
+    } else {
+        if (dec) hipLaunchKernelGGL((gate_k<false, true>), dim3(grid), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((gate_k<false, false>), dim3(grid), dim3(256), 0, s, a);
+    }
 }
 
 void launch_count(const uint8_t* m, int F, int N, int G, int* cnt, hipStream_t s) {

@@ -17,8 +17,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "lib
 DV_OK, DV_EINVAL, DV_ENOMEM, DV_EHIP, DV_EUNSUPPORTED = 0, -1, -2, -3, -4
 DV_F32, DV_BF16 = 0, 1
 STAGES = ["patch", "gate", "compact", "ln1", "qkv", "attn", "oproj", "ln2", "fc1", "fc2",
-          "merge", "final", "restore"]
+          "merge", "final", "restore", "cls"]
 DV_FLAG_RESTORE = 1
+DV_FLAG_DECISION = 2
 
 
 class DejaVuError(RuntimeError):
@@ -132,7 +133,7 @@ def dv_compact(masks, n_frames, n_tokens, group_size, idx, pos, qoff, count, str
                              stream))
 
 
-DV_PROFILE_ALL = 0x1FFF
+DV_PROFILE_ALL = 0x3FFF
 
 
 def dv_profile(handle, stage_mask):
@@ -161,7 +162,8 @@ class Encoder:
     def __init__(self, model, weights, max_batch_frames):
         m = model
         self.model = m
-        flags = DV_FLAG_RESTORE if getattr(m, "restore", False) else 0
+        flags = (DV_FLAG_RESTORE if getattr(m, "restore", False) else 0) | \
+            (DV_FLAG_DECISION if getattr(m, "decision", False) else 0)
         self.cfg = make_config(m.image_size, m.patch, m.depth, m.width, m.heads, m.mlp, m.dtype,
                                max_batch_frames, flags)
         self.handle = dv_create(self.cfg, weights)

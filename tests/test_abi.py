@@ -60,6 +60,19 @@ def test_weights_floats_with_restoration_section():
         m.depth * (2 * 128 * m.width + 128 + m.width)
 
 
+def test_weights_floats_with_decision_section():
+    import dataclasses
+    import synth
+    tiny = synth.get_config("tiny").model
+    for restore in (False, True):
+        m = dataclasses.replace(tiny, restore=restore, decision=True)
+        flags = dj.DV_FLAG_DECISION | (dj.DV_FLAG_RESTORE if restore else 0)
+        assert dj.dv_weights_floats(_cfg(flags=flags)) == synth.weights.blob_floats(m)
+        without = dataclasses.replace(m, decision=False)
+        assert synth.weights.blob_floats(m) - synth.weights.blob_floats(without) == \
+            m.depth * (64 * 6 + 64 + 64 + 1)
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(image_size=100), dj.DV_EUNSUPPORTED),       # S % p
     (dict(heads=5), dj.DV_EUNSUPPORTED),              # D % H
@@ -68,7 +81,7 @@ def test_weights_floats_with_restoration_section():
     (dict(max_batch_frames=0), dj.DV_EINVAL),
     (dict(dtype=7), dj.DV_EINVAL),
     (dict(width=200, heads=2), dj.DV_EUNSUPPORTED),   # width not a tile multiple
-    (dict(flags=2), dj.DV_EUNSUPPORTED),              # unknown flag bit
+    (dict(flags=4), dj.DV_EUNSUPPORTED),              # unknown flag bit
 ])
 def test_create_rejects_bad_config(kw, code):
     cfg = _cfg(**kw)

@@ -21,6 +21,8 @@ N257_BF16 = ModelConfig(224, 14, 2, 128, 2, 256, "bf16")
 N577_BF16 = ModelConfig(336, 14, 1, 128, 2, 256, "bf16")
 # head dim 80 (the ViT-H/14-class width 1280 / 16 heads)
 DH80_BF16 = ModelConfig(64, 16, 2, 640, 8, 1280, "bf16")
+# head dim 80 with two key blocks per frame (N = 50): the per-frame attention kernel
+DH80_N50 = ModelConfig(112, 16, 2, 640, 8, 1280, "bf16")
 
 
 def _video(m, n, seed=2000, sigma=0.01, speed=3.0, n_obj=2, size=None, pan=0.0):
@@ -107,7 +109,8 @@ def test_tiny_dense_matches_oracle():
     check_close(host(toks), r[1], "f32", "tokens")
 
 
-@pytest.mark.parametrize("m", [TINY.model, SMALL_BF16, MID_BF16], ids=["tiny", "small", "mid"])
+@pytest.mark.parametrize("m", [TINY.model, SMALL_BF16, MID_BF16, DH80_N50],
+                         ids=["tiny", "small", "mid", "dh80"])
 def test_copy_at_plus_inf_is_bitwise(m):
     torch = require_gpu()
     blob = synth.make_blob(m, 21)
@@ -129,7 +132,8 @@ def test_copy_at_plus_inf_is_bitwise(m):
     assert np.array_equal(host(toks2), t) and np.array_equal(host(emb2), e)
 
 
-@pytest.mark.parametrize("m", [TINY.model, SMALL_BF16], ids=["tiny", "small"])
+@pytest.mark.parametrize("m", [TINY.model, SMALL_BF16, MID_BF16, DH80_N50],
+                         ids=["tiny", "small", "mid", "dh80"])
 def test_reuse_off_equivalences_bitwise(m):
     """tau=2 (gate runs, reuses nothing) == tau=-inf; G=1 == dense; reference frames of a
     reuse run == the same frames run densely (rows are independent of their packed slot)."""
