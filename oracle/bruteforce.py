@@ -10,7 +10,10 @@ to the reference (hidden 128, GELU; Section 3.3), evaluated row by row.  With
 ``cfg["decision"]`` the gate is the decision MLP (Section 3.3): inputs the cosine, the class
 token's attention weight on the token in the frame's previous layer (mean over heads; 1/N at
 the first layer) and the one-hot frame type (P for every non-reference frame); reuse when its
-output exceeds tau.
+output exceeds tau.  With ``cfg["reorder"]`` frames reference their I/P/B anchors (Section
+3.1): a token compares itself with each reference, takes the larger cosine, and when reused
+copies that reference (the earlier-listed, past one on a tie); a frame is computed after its
+references.
 """
 import math
 
@@ -76,6 +79,22 @@ def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
             out += float(Wd2[0, k]) * 0.5 * z * (1.0 + math.erf(z / math.sqrt(2.0)))
         return out
 
+    reorder = bool(cfg.get("reorder"))
+
+    def refs_of(f):
+        """(type: 0 I, 1 P, 2 B_dist2, 3 B_dist1; references, past first)"""
+        pos_in = f % group_size
+        if not reorder:
+            return (0, []) if pos_in == 0 else (1, [f - pos_in])
+        if pos_in == 0:
+            return 0, []
+        if pos_in % 4 == 0:
+            return 1, [f - 4]
+        d = pos_in % 4
+        base = f - d
+        a, b = {1: (base, base + 2), 2: (base, base + 4), 3: (base + 2, base + 4)}[d]
+        return (2 if d == 2 else 3), [a] + ([b] if b < F else [])
+
     M = np.zeros((F, L, N), dtype=np.uint8)
     tprev = [[1.0 / N] * N for _ in range(F)]   # class-token attention of the previous layer
     for l in range(L):
@@ -84,11 +103,27 @@ def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
         KEY = np.zeros((F, N, D))
         VAL = np.zeros((F, N, D))
         tnext = [[0.0] * N for _ in range(F)]
-        for f in range(F):                      # frames in order: the reference comes first
-            ref = (f // group_size) * group_size
+        done = set()
+
+        def compute(f):
+            ftype, refs = refs_of(f)
+            for r in refs:                      # a frame's references are computed before it
+                if r not in done:
+                    compute(r)
+            layer_frame(f, ftype, refs)
+            done.add(f)
+
+        def layer_frame(f, ftype, refs):
             reuse = [False] * N
-            if f != ref:
+            src = [f] * N
+            if refs:
                 for i in range(1, N):
+                    sims = [cosine(X[f, i], X[r, i]) for r in refs]
+                    best = 0
+                    for k in range(1, len(sims)):
+                        if sims[k] > sims[best]:
+                            best = k
+                    src[i] = refs[best]
                     if masks is not None:
                         reuse[i] = bool(masks[f][l][i])
                     elif tau == -math.inf:
@@ -96,25 +131,25 @@ def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
                     elif tau == math.inf:
                         reuse[i] = True
                     elif decide:
-                        dval = decision(cosine(X[f, i], X[ref, i]), tprev[f][i], 1, *dec[l])
+                        dval = decision(sims[best], tprev[f][i], ftype, *dec[l])
                         reuse[i] = dval > tau
                     else:
-                        reuse[i] = cosine(X[f, i], X[ref, i]) >= tau
+                        reuse[i] = sims[best] >= tau
             Q = {}
             for i in range(N):
                 if reuse[i]:
-                    KEY[f, i] = KEY[ref, i]
-                    VAL[f, i] = VAL[ref, i]
+                    KEY[f, i] = KEY[src[i], i]
+                    VAL[f, i] = VAL[src[i], i]
                     M[f, l, i] = 1
                 else:
                     t = Wqkv @ norm(X[f, i], g1, b1) + bqkv
                     Q[i], KEY[f, i], VAL[f, i] = t[:D], t[D:2 * D], t[2 * D:]
             for i in range(N):
                 if reuse[i]:
-                    Y[f, i] = Y[ref, i]
+                    Y[f, i] = Y[src[i], i]
                     if restore:
                         Wr1, br1, Wr2, br2 = rest[l]
-                        hid = Wr1 @ (X[f, i] - X[ref, i]) + br1
+                        hid = Wr1 @ (X[f, i] - X[src[i], i]) + br1
                         hid = np.array([0.5 * t * (1.0 + math.erf(t / math.sqrt(2.0))) for t in hid])
                         Y[f, i] = Y[f, i] + (Wr2 @ hid + br2)
                     continue
@@ -133,6 +168,10 @@ def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
                 u = W1 @ norm(z, g2, b2) + bb1
                 u = np.array([0.5 * t * (1.0 + math.erf(t / math.sqrt(2.0))) for t in u])
                 Y[f, i] = z + W2 @ u + bb2
+
+        for f in range(F):
+            if f not in done:
+                compute(f)
         X = Y
         tprev = tnext
     emb = np.stack([norm(X[f, 0], lnfg, lnfb) for f in range(F)])

@@ -48,6 +48,21 @@ What it computes, following the paper's model description (Section 3):
   every token is gated at every layer and a reused row copies the
   reference's layer output.
 
+* Reordered referencing (Section 3.1, frame-reordering figure; Eq. 1 with two
+  references), when the configuration enables it (``cfg["reorder"]``, group
+  size a multiple of 4): within a group the first frame is the I frame
+  (computed in full); every fourth frame after it is a P frame referencing
+  the anchor four frames back; between two anchors a0 and a0 + 4 (the next
+  group's I frame closing the group's last block) the middle frame is
+  B_dist2, referencing both anchors, and the other two are B_dist1,
+  referencing their two neighbours among a0, a0 + 2, a0 + 4.  A reference
+  past the end of the call is dropped.  Frames of a layer are processed in
+  the paper's order I -> (P -> B_dist2 -> B_dist1 -> B_dist1) -> ..., each
+  after its references.  The similarity is the larger of the two cosines and
+  a reused token takes its keys, values and layer output from the reference
+  that gave it (the past one on a tie); the decision MLP's type cue is the
+  frame's own type.
+
 Modes: gate mode (``tau``) and mask-injection mode (``masks`` given; class
 token and reference-frame entries are forced to 0).  ``tau = -inf`` turns
 reuse off (dense), ``tau = +inf`` reuses every non-class token of every
@@ -177,6 +192,47 @@ def attention(q, k, v, heads, first_probs=False):
     return (out, p0 / heads) if first_probs else out
 
 
+def reference_frames(f, group_size, n_frames):
+    """(type index into FRAME_TYPES, past reference, future reference or None) of frame f under
+    the reordered referencing (module docstring)."""
+    G = group_size
+    p = f % G
+    if p == 0:
+        return 0, None, None
+    if p % 4 == 0:
+        return 1, f - 4, None
+    a0 = f - p % 4
+    if p % 4 == 2:
+        t, past, fut = 2, a0, a0 + 4
+    elif p % 4 == 1:
+        t, past, fut = 3, a0, a0 + 2
+    else:
+        t, past, fut = 3, a0 + 2, a0 + 4
+    return t, past, (fut if fut < n_frames else None)
+
+
+def processing_order(n_frames, group_size):
+    """Frames of a layer in the paper's order: each group's I frame, then block by block the
+    closing anchor (a P frame, or the next group's I frame), the B_dist2 frame, the two B_dist1
+    frames."""
+    G = group_size
+    order, seen = [], set()
+
+    def put(f):
+        if f < n_frames and f not in seen:
+            order.append(f)
+            seen.add(f)
+
+    for g0 in range(0, n_frames, G):
+        put(g0)
+        for a0 in range(g0, g0 + G, 4):
+            put(a0 + 4)
+            for q in (a0 + 2, a0 + 1, a0 + 3):
+                if q < g0 + G:
+                    put(q)
+    return order
+
+
 def frame_type(f, group_size):
     """Index into FRAME_TYPES: the group's first frame is the I frame, every other frame
     references it alone, the role of a P frame."""
@@ -221,6 +277,58 @@ def finish_rows(x_rows, o_rows, P):
     return z + h @ P["W_2"].T + P["b_2"]
 
 
+def reordered_layer(x, P, cfg, G, l, tau, masks, t_cls, rec):
+    """One layer over all frames with the reordered referencing; returns the layer output and
+    the class-token attention weights of every frame (for the next layer's decision cue).
+    rec: the per-(frame, layer, token) records (masks, cos, src, dec, t) to fill."""
+    F, N, D = x.shape
+    H = cfg["heads"]
+    decide = bool(cfg.get("decision"))
+    y = np.empty_like(x)
+    k_eff, v_eff = np.empty_like(x), np.empty_like(x)   # the keys/values each frame attends to
+    t_next = np.empty((F, N))
+    for f in processing_order(F, G):
+        ftype, past, fut = reference_frames(f, G, F)
+        if ftype == 0:   # I frame: the whole layer on every token
+            q, k, v = qkv_rows(x[f], P)
+            o, t_next[f] = attention(q, k, v, H, first_probs=True)
+            y[f] = finish_rows(x[f], o, P)
+            k_eff[f], v_eff[f] = k, v
+            continue
+        c_past = cosine_rows(x[f, 1:], x[past, 1:])
+        c_fut = cosine_rows(x[f, 1:], x[fut, 1:]) if fut is not None else np.full(N - 1, -np.inf)
+        s = np.maximum(c_past, c_fut)                       # similarity cue: the better reference
+        from_fut = c_fut > c_past                           # a tie takes the past reference
+        rec["cos"][f, l, 1:] = s
+        rec["src"][f, l, 1:] = from_fut
+        if decide:
+            dv = decision_values(s, t_cls[f, 1:], ftype, P)
+            rec["dec"][f, l, 1:] = dv
+            rec["t"][f, l, 1:] = t_cls[f, 1:]
+        if masks is not None:
+            reuse = np.asarray(masks[f, l, 1:]) != 0
+        elif decide:
+            reuse = decision_gate(dv, tau)
+        else:
+            reuse = gate_decision(s, tau)
+        m = np.concatenate([[False], reuse])                # class token never reused
+        rec["masks"][f, l] = m
+        C, R = np.flatnonzero(~m), np.flatnonzero(m)
+        src = np.where(np.concatenate([[False], from_fut]), fut if fut is not None else past,
+                       past)[R]                             # reference of each reused token
+        q_c, k_c, v_c = qkv_rows(x[f, C], P)
+        k_t, v_t = np.empty((N, D)), np.empty((N, D))
+        k_t[C], v_t[C] = k_c, v_c                           # fresh keys/values ...
+        k_t[R], v_t[R] = k_eff[src, R], v_eff[src, R]       # ... and the reference's
+        o_c, t_next[f] = attention(q_c, k_t, v_t, H, first_probs=True)
+        y[f, C] = finish_rows(x[f, C], o_c, P)
+        y[f, R] = y[src, R]                                 # reused rows: the reference's output
+        if cfg.get("restore"):
+            y[f, R] += restore_rows(x[f, R] - x[src, R], P)
+        k_eff[f], v_eff[f] = k_t, v_t
+    return y, t_next
+
+
 def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64,
            return_layers=False):
     """Reuse-aware encoder forward over ``frames`` [F, 3, S, S].
@@ -232,6 +340,8 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
       dec    [F, L, N]   decision-MLP output d_i (only with cfg["decision"]; NaN where not
                          evaluated)
       t      [F, L, N]   its class-token attention input t_i (same conditions)
+      src    [F, L, N]   with cfg["reorder"]: 1 where the future reference gave the larger
+                         cosine (and supplies a reused token), 0 past, -1 not evaluated
       tokens [F, N, D]   output of the last layer
       layers (optional)  list of the L+1 token buffers x^0..x^L
     """
@@ -252,9 +362,20 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
     out_t = np.full((F, L, N), np.nan) if decide else None
     t_cls = np.full((F, N), 1.0 / N) if decide else None  # class-token attention, previous layer
     hist = [x.copy()] if return_layers else None
+    reorder = bool(cfg.get("reorder"))
+    if reorder and G % 4:
+        raise ValueError("reordered referencing needs a group size that is a multiple of 4")
+    out_s = np.full((F, L, N), -1, dtype=np.int8) if reorder else None
 
     for l in range(L):
         P = W["layers"][l]
+        if reorder:
+            rec = {"masks": out_m, "cos": out_c, "src": out_s, "dec": out_d, "t": out_t}
+            x, t_cls = reordered_layer(x, P, cfg, G, l, tau, masks,
+                                       t_cls if decide else np.full((F, N), 1.0 / N), rec)
+            if return_layers:
+                hist.append(x.copy())
+            continue
         y = np.empty_like(x)
         t_next = np.empty((F, N)) if decide else None
         for r in range(0, F, G):
@@ -302,6 +423,8 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
     if decide:
         res["dec"] = out_d
         res["t"] = out_t
+    if reorder:
+        res["src"] = out_s
     if return_layers:
         res["layers"] = hist
     return res

@@ -26,6 +26,7 @@ class ModelConfig:
     dtype: str  # "f32" or "bf16": arithmetic type of the GEMM/attention operands
     restore: bool = False   # per-layer restoration MLP on reused tokens (hidden RESTORE_HIDDEN)
     decision: bool = False  # per-layer learned decision MLP as the gate (hidden DECISION_HIDDEN)
+    reorder: bool = False   # I/P/B referencing with past and future references (no weights)
 
     @property
     def n_patches(self) -> int:
@@ -42,7 +43,7 @@ class ModelConfig:
     def as_dict(self):
         return dict(image_size=self.image_size, patch=self.patch, depth=self.depth,
                     width=self.width, heads=self.heads, mlp=self.mlp, dtype=self.dtype,
-                    restore=self.restore, decision=self.decision)
+                    restore=self.restore, decision=self.decision, reorder=self.reorder)
 
 
 @dataclass(frozen=True)

@@ -38,6 +38,14 @@ What pins what:
                d == tau recomputes
   decision_mlp       the MLP itself == torch Linear/GELU/Linear on the features
   decision_brute     == the per-token loop implementation (with and without restoration)
+  reordered referencing (I/P/B frames with past and future references):
+  reorder_pattern    the reference graph of the paper's I -> (P -> B_dist2 -> B_dist1 -> B_dist1)
+               pattern, written out for 16 frames in groups of 8 and 4, and a processing order
+               that puts every frame after its references
+  reorder_future     a B frame equal to its future anchor reuses from it at every layer and
+               copies its outputs; swapping the anchors' roles swaps the source
+  reorder_brute      == the per-token loop implementation (gate and injection modes, with
+               restoration and with the decision MLP, groups of 4, 8 and 12, short last groups)
 """
 import numpy as np
 
@@ -498,8 +506,84 @@ def pin_decision_brute(ora):
             _close(r["emb"], b["emb"], 1e-12, f"emb tau={tau}")
 
 
+M_BO = ModelConfig(48, 16, 2, 16, 2, 32, "f32")   # M_B, run with cfg["reorder"]
+
+
+def reorder_cfg(m):
+    import dataclasses
+    return dataclasses.replace(m, reorder=True).as_dict()
+
+
+# the paper's pattern, frames 0..15: (type, past reference, future reference), types
+# 0 I, 1 P, 2 B_dist2, 3 B_dist1
+PATTERN_G8 = [(0, None, None), (3, 0, 2), (2, 0, 4), (3, 2, 4), (1, 0, None), (3, 4, 6),
+              (2, 4, 8), (3, 6, 8), (0, None, None), (3, 8, 10), (2, 8, 12), (3, 10, 12),
+              (1, 8, None), (3, 12, 14), (2, 12, None), (3, 14, None)]
+PATTERN_G4 = [(0, None, None), (3, 0, 2), (2, 0, 4), (3, 2, 4), (0, None, None), (3, 4, 6),
+              (2, 4, 8), (3, 6, 8), (0, None, None), (3, 8, 10), (2, 8, 12), (3, 10, 12),
+              (0, None, None), (3, 12, 14), (2, 12, None), (3, 14, None)]
+
+
+def pin_reorder_pattern(ora):
+    for G, want in ((8, PATTERN_G8), (4, PATTERN_G4)):
+        got = [ora.reference_frames(f, G, 16) for f in range(16)]
+        assert got == want, f"reference graph, groups of {G}: {got}"
+        order = ora.processing_order(16, G)
+        assert sorted(order) == list(range(16))
+        at = {f: k for k, f in enumerate(order)}
+        for f, (_, a, b) in enumerate(got):
+            assert all(at[r] < at[f] for r in (a, b) if r is not None), f"frame {f} before a ref"
+    assert ora.processing_order(16, 8)[:5] == [0, 4, 2, 1, 3]
+    # groups of 12: a chain of P frames, each referencing the anchor four frames back
+    assert [ora.reference_frames(f, 12, 14)[:2] for f in (4, 8, 12)] == [(1, 0), (1, 4), (0, None)]
+    assert ora.reference_frames(10, 12, 14) == (2, 8, 12)
+
+
+def pin_reorder_future(ora):
+    m = M_BO
+    w, blob = weights(m, 36)
+    fr = mixed_frames(m, 9, 8, seed=36)
+    fr[4] = np.random.default_rng(37).standard_normal(fr[4].shape)   # the P anchor: a new scene
+    fr[2] = fr[4]                                                      # B_dist2 == future anchor
+    for tau in (0.9, np.inf):
+        r = ora.encode(fr, blob, reorder_cfg(m), 8, tau=tau)
+        assert r["masks"][2, :, 1:].all(), "every token of frame 2 reused"
+        # at layer 0 from the future anchor (later, where the anchor itself copied frame 0,
+        # both references hold equal rows and the tie takes the past one)
+        assert (r["src"][2, 0, 1:] == 1).all(), "... from its future anchor"
+        assert_copy(r, 2, 4)
+    # the mirror case: frame 2 equal to its past anchor (frame 0) reuses from the past
+    fr = mixed_frames(m, 9, 8, seed=38)
+    fr[4] = np.random.default_rng(39).standard_normal(fr[4].shape)
+    fr[2] = fr[0]
+    r = ora.encode(fr, blob, reorder_cfg(m), 8, tau=0.9)
+    assert r["masks"][2, :, 1:].all() and (r["src"][2, :, 1:] == 0).all()
+    assert_copy(r, 2, 0)
+
+
+def pin_reorder_brute(ora):
+    cases = ((M_A, 4, 11), (M_B, 8, 13), (M_B, 12, 14), (M_BR, 4, 9), (M_BD, 8, 10))
+    for m, G, F in cases:
+        w, blob = weights(m, 40 + G)
+        fr = mixed_frames(m, F, G, seed=F)
+        cfg = reorder_cfg(m)
+        taus = (0.0, 1.0, 2.0) if m.decision else (0.3, 0.8, 0.97, np.inf)
+        for tau in taus:
+            r = ora.encode(fr, blob, cfg, G, tau=tau)
+            b = encode_bruteforce(fr, blob, cfg, G, tau=tau)
+            assert np.array_equal(r["masks"], b["masks"]), f"masks differ at tau={tau}"
+            _close(r["tokens"], b["tokens"], 1e-12, f"tokens tau={tau}")
+            _close(r["emb"], b["emb"], 1e-12, f"emb tau={tau}")
+        mk = (np.random.default_rng(F).random((F, m.depth, m.n_tokens)) < 0.6).astype(np.uint8)
+        r = ora.encode(fr, blob, cfg, G, masks=mk)
+        b = encode_bruteforce(fr, blob, cfg, G, masks=mk)
+        assert np.array_equal(r["masks"], b["masks"]), "effective injected masks differ"
+        _close(r["tokens"], b["tokens"], 1e-12, "tokens (injected)")
+
+
 ALL_PINS = [pin_library, pin_dense_vit, pin_bruteforce, pin_copy, pin_ref_dense, pin_monotone,
             pin_static, pin_g1, pin_groups, pin_inject_one, pin_extremes, pin_star, pin_cosine,
             pin_partial, pin_rate, pin_restore_zero, pin_restore_brute, pin_restore_one,
             pin_restore_static, pin_decision_threshold, pin_decision_attention, pin_decision_type,
-            pin_decision_mlp, pin_decision_brute]
+            pin_decision_mlp, pin_decision_brute, pin_reorder_pattern, pin_reorder_future,
+            pin_reorder_brute]

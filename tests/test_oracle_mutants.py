@@ -59,6 +59,19 @@ MUTANTS = [
     ("decision_attention_from_reference", "t_next[f] = p_c", "t_next[f] = p_r"),
     ("decision_attention_starts_at_zero", "np.full((F, N), 1.0 / N)", "np.zeros((F, N))"),
     ("decision_attention_of_last_query", "p0 += pr[0]", "p0 += pr[-1]"),
+    ("reorder_min_similarity", "s = np.maximum(c_past, c_fut)", "s = np.minimum(c_past, c_fut)"),
+    ("reorder_tie_to_future", "from_fut = c_fut > c_past", "from_fut = c_fut >= c_past"),
+    ("reorder_index_order", "for f in processing_order(F, G):", "for f in range(F):"),
+    ("reorder_b1_skips_b2", "t, past, fut = 3, a0, a0 + 2", "t, past, fut = 3, a0, a0 + 4"),
+    ("reorder_p_from_group_start", "return 1, f - 4, None", "return 1, f - p, None"),
+    ("reorder_b2_past_only", "t, past, fut = 2, a0, a0 + 4", "t, past, fut = 2, a0, None"),
+    ("reorder_kv_from_past", "k_t[R], v_t[R] = k_eff[src, R], v_eff[src, R]",
+     "k_t[R], v_t[R] = k_eff[past, R], v_eff[past, R]"),
+    ("reorder_output_from_past", "y[f, R] = y[src, R]", "y[f, R] = y[past, R]"),
+    ("reorder_type_cue_p", "dv = decision_values(s, t_cls[f, 1:], ftype, P)",
+     "dv = decision_values(s, t_cls[f, 1:], 1, P)"),
+    ("reorder_restore_from_past", "x[f, R] - x[src, R]", "x[f, R] - x[past, R]"),
+    ("reorder_anchor_after_b", "            put(a0 + 4)\n", ""),
 ]
 
 
