@@ -48,7 +48,7 @@ def active_rows(masks, G):
 
 def reuse_of(masks, G):
     nonref = [f for f in range(masks.shape[0]) if f % G]
-    return float(masks[nonref].mean()) if nonref else 0.0
+    return float((masks[nonref] != 0).mean()) if nonref else 0.0
 
 
 def stage_flops(stage, m, Ml):
@@ -223,6 +223,8 @@ def main():
     ap.add_argument("--decision", action="store_true",
                     help="gate with the learned decision MLP (random decision weights; the "
                          "threshold on its output is calibrated like tau)")
+    ap.add_argument("--reorder", action="store_true",
+                    help="reordered I/P/B referencing with past and future references")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device-to-device copy (HBM counter calibration)")
     ap.add_argument("--traffic-record", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_OUT"),
@@ -255,6 +257,10 @@ def main():
     if args.decision:
         import dataclasses
         m = dataclasses.replace(m, decision=True)
+        w = dataclasses.replace(w, model=m)
+    if args.reorder:
+        import dataclasses
+        m = dataclasses.replace(m, reorder=True)
         w = dataclasses.replace(w, model=m)
     G, F = w.group_size, w.batch_frames
     t0 = time.time()
@@ -397,6 +403,8 @@ def main():
                                   else "")
                                + ("learned decision MLP gate (hidden 64); " if m.decision
                                   else "")
+                               + ("reordered I/P/B referencing (past and future anchors); "
+                                  if m.reorder else "")
                                + "reuse levels "
                                + "/".join(f"{t:.0%}" for t in targets if t is not None),
                    "frames_per_step": F * len(taus), "group_size": G},

@@ -80,7 +80,7 @@ typedef struct dv_config {
     int mlp;               /* Dm: MLP hidden width */
     int dtype;             /* DV_F32 or DV_BF16 */
     int max_batch_frames;  /* frames per internal batch (rounded down to whole groups per call) */
-    unsigned flags;        /* DV_FLAG_RESTORE | DV_FLAG_DECISION or 0; other bits must be 0 */
+    unsigned flags;        /* DV_FLAG_RESTORE, DV_FLAG_DECISION, DV_FLAG_REORDER or 0 */
 } dv_config;
 
 /* Restoration layer on reused tokens (Section 3.3): after each layer, a reused token i of a
@@ -108,6 +108,20 @@ typedef struct dv_config {
 #define DV_FLAG_DECISION 2u
 #define DV_DECISION_HIDDEN 64     /* hidden width of the decision MLP */
 #define DV_DECISION_FEATURES 6    /* its input width: s, t and the four frame types */
+
+/* Reordered referencing with past and future references (Section 3.1, frame reordering;
+ * Eq. 1 with two references) instead of the star.  The group size must be a multiple of 4.
+ * Within a group of G frames the first is the I frame (computed in full); positions 4, 8, ...
+ * are P frames referencing the anchor four frames back; between anchors a and a + 4 (the next
+ * group's I frame closes the group's last block) the frame at a + 2 is B_dist2, referencing
+ * both anchors, and the frames at a + 1 and a + 3 are B_dist1, referencing their neighbours
+ * among a, a + 2, a + 4.  A reference past the last frame of the call is absent.  A token's
+ * similarity is the larger of its two cosines; when reused, its keys, values and layer output
+ * come from the reference that gave it (the past one on a tie).  The decision MLP's type cue is
+ * the frame's own type.  Frame indices are those of the call; internal batches also compute
+ * the next batch's first frame, so batching does not change results.  Not combinable with
+ * DV_FLAG_RESTORE (DV_EUNSUPPORTED).  No extra weights. */
+#define DV_FLAG_REORDER 4u
 
 typedef struct dv_handle dv_handle;
 
@@ -146,18 +160,20 @@ int dv_workspace_bytes(const dv_handle* h, size_t* bytes);
 
 /* Gate mode.  frames: device fp32 [n_frames, 3, S, S], already normalised.
  * out_embeddings: device fp32 [n_frames, D] (final LayerNorm of the class token).
- * out_masks: device u8 [n_frames, depth, N] (1 = reused) or NULL.
+ * out_masks: device u8 [n_frames, depth, N] (1 = reused; with DV_FLAG_REORDER, 2 = reused
+ * from the future reference) or NULL.
  * Frame f's reference is frame G*floor(f/G) (frame indices within this call;
- * a short last group still uses its first frame).  Work is split into
- * internal batches of whole groups, so the result does not depend on
- * max_batch_frames.  tau = -INFINITY turns reuse off (the same kernels run
+ * a short last group still uses its first frame), or its I/P/B anchors with
+ * DV_FLAG_REORDER.  Work is split into internal batches of whole groups, so the
+ * result does not depend on max_batch_frames.  tau = -INFINITY turns reuse off (the same kernels run
  * densely, masks all 0); tau = +INFINITY reuses every non-class token of
  * every non-reference frame; a finite tau applies the rule above
  * (tau > 1 reuses nothing, tau <= -1 everything) or, with DV_FLAG_DECISION,
  * the decision MLP's rule d_i > tau.  NaN tau -> DV_EINVAL.
  * Enqueued on `stream`, asynchronous, no host synchronisation.
  * Errors: DV_EINVAL (null handle/frames/embeddings, n_frames < 1,
- * group_size < 1 or > max_batch_frames, NaN tau), DV_EHIP. */
+ * group_size < 1 or > max_batch_frames, NaN tau, group_size not a multiple of 4 with
+ * DV_FLAG_REORDER), DV_EHIP. */
 int dv_encode(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
               float* out_embeddings, uint8_t* out_masks, hipStream_t stream);
 

@@ -140,7 +140,7 @@ def encode_bruteforce(frames, blob, cfg, group_size, tau=None, masks=None):
                 if reuse[i]:
                     KEY[f, i] = KEY[src[i], i]
                     VAL[f, i] = VAL[src[i], i]
-                    M[f, l, i] = 1
+                    M[f, l, i] = 2 if (reorder and src[i] != refs[0]) else 1   # 2: future
                 else:
                     t = Wqkv @ norm(X[f, i], g1, b1) + bqkv
                     Q[i], KEY[f, i], VAL[f, i] = t[:D], t[D:2 * D], t[2 * D:]

@@ -277,10 +277,12 @@ def finish_rows(x_rows, o_rows, P):
     return z + h @ P["W_2"].T + P["b_2"]
 
 
-def reordered_layer(x, P, cfg, G, l, tau, masks, t_cls, rec):
+def reordered_layer(x, P, cfg, G, l, tau, masks, sources, t_cls, rec):
     """One layer over all frames with the reordered referencing; returns the layer output and
     the class-token attention weights of every frame (for the next layer's decision cue).
-    rec: the per-(frame, layer, token) records (masks, cos, src, dec, t) to fill."""
+    rec: the per-(frame, layer, token) records (masks, cos, cos_past, cos_fut, src, dec, t) to
+    fill.  sources (injection mode, optional): replaces the choice of reference of reused
+    tokens (nonzero = the future one)."""
     F, N, D = x.shape
     H = cfg["heads"]
     decide = bool(cfg.get("decision"))
@@ -300,7 +302,12 @@ def reordered_layer(x, P, cfg, G, l, tau, masks, t_cls, rec):
         s = np.maximum(c_past, c_fut)                       # similarity cue: the better reference
         from_fut = c_fut > c_past                           # a tie takes the past reference
         rec["cos"][f, l, 1:] = s
+        rec["cos_past"][f, l, 1:] = c_past
+        if fut is not None:
+            rec["cos_fut"][f, l, 1:] = c_fut
         rec["src"][f, l, 1:] = from_fut
+        if sources is not None and fut is not None:
+            from_fut = np.asarray(sources[f, l, 1:]) != 0
         if decide:
             dv = decision_values(s, t_cls[f, 1:], ftype, P)
             rec["dec"][f, l, 1:] = dv
@@ -312,7 +319,7 @@ def reordered_layer(x, P, cfg, G, l, tau, masks, t_cls, rec):
         else:
             reuse = gate_decision(s, tau)
         m = np.concatenate([[False], reuse])                # class token never reused
-        rec["masks"][f, l] = m
+        rec["masks"][f, l] = m * np.concatenate([[1], 1 + from_fut])   # 2: from the future
         C, R = np.flatnonzero(~m), np.flatnonzero(m)
         src = np.where(np.concatenate([[False], from_fut]), fut if fut is not None else past,
                        past)[R]                             # reference of each reused token
@@ -330,7 +337,7 @@ def reordered_layer(x, P, cfg, G, l, tau, masks, t_cls, rec):
 
 
 def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64,
-           return_layers=False):
+           return_layers=False, sources=None):
     """Reuse-aware encoder forward over ``frames`` [F, 3, S, S].
 
     Returns a dict with
@@ -341,7 +348,9 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
                          evaluated)
       t      [F, L, N]   its class-token attention input t_i (same conditions)
       src    [F, L, N]   with cfg["reorder"]: 1 where the future reference gave the larger
-                         cosine (and supplies a reused token), 0 past, -1 not evaluated
+                         cosine (and supplies a reused token), 0 past, -1 not evaluated;
+                         masks then hold 2 for a token reused from the future reference
+      cos_past, cos_fut  [F, L, N]  the two cosines (reorder; NaN where absent)
       tokens [F, N, D]   output of the last layer
       layers (optional)  list of the L+1 token buffers x^0..x^L
     """
@@ -366,12 +375,15 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
     if reorder and G % 4:
         raise ValueError("reordered referencing needs a group size that is a multiple of 4")
     out_s = np.full((F, L, N), -1, dtype=np.int8) if reorder else None
+    out_cp = np.full((F, L, N), np.nan) if reorder else None
+    out_cf = np.full((F, L, N), np.nan) if reorder else None
 
     for l in range(L):
         P = W["layers"][l]
         if reorder:
-            rec = {"masks": out_m, "cos": out_c, "src": out_s, "dec": out_d, "t": out_t}
-            x, t_cls = reordered_layer(x, P, cfg, G, l, tau, masks,
+            rec = {"masks": out_m, "cos": out_c, "cos_past": out_cp, "cos_fut": out_cf,
+                   "src": out_s, "dec": out_d, "t": out_t}
+            x, t_cls = reordered_layer(x, P, cfg, G, l, tau, masks, sources,
                                        t_cls if decide else np.full((F, N), 1.0 / N), rec)
             if return_layers:
                 hist.append(x.copy())
@@ -425,6 +437,8 @@ def encode(frames, blob, cfg, group_size, tau=None, masks=None, dtype=np.float64
         res["t"] = out_t
     if reorder:
         res["src"] = out_s
+        res["cos_past"] = out_cp
+        res["cos_fut"] = out_cf
     if return_layers:
         res["layers"] = hist
     return res
@@ -437,4 +451,4 @@ def reuse_rate(masks, group_size):
     nonref = [f for f in range(F) if f % group_size != 0]
     if not nonref:
         return 0.0
-    return float(np.asarray(masks)[nonref].astype(np.float64).mean())
+    return float((np.asarray(masks)[nonref] != 0).astype(np.float64).mean())

@@ -16,6 +16,11 @@
 //     [decision MLP: the gate evaluates it on (cosine, class-token attention of the previous
 //      layer, frame type); after attention the class-token weights of every frame are
 //      computed for the next layer]
+//     [reordered referencing: the gate compares each token with the frame's past and future
+//      anchors and records which one supplies it; after the compaction every reused token's
+//      key/value row is resolved along those sources to the frame that recomputes it; after
+//      FC2 every reused row is copied from that frame's new row.  An internal batch also
+//      carries the next batch's first frame (an I frame, the future anchor of its last block).]
 //   final LayerNorm of the class tokens.
 // Nothing is read back to the host inside an encode call.
 //
@@ -78,6 +83,8 @@ struct Dims {
     bool bf16;
     bool restore;   // DV_FLAG_RESTORE
     bool decision;  // DV_FLAG_DECISION
+    bool reorder;   // DV_FLAG_REORDER
+    int Bw;         // frames of workspace: B, plus one look-ahead frame with reordering
 };
 
 constexpr int RH = DV_RESTORE_HIDDEN;
@@ -89,8 +96,11 @@ int check_config(const dv_config* c, Dims* d) {
         c->mlp < 1 || c->max_batch_frames < 1)
         return fail(DV_EINVAL, "config sizes must be >= 1");
     if (c->dtype != DV_F32 && c->dtype != DV_BF16) return fail(DV_EINVAL, "unknown dtype %d", c->dtype);
-    if (c->flags & ~(DV_FLAG_RESTORE | DV_FLAG_DECISION))
+    if (c->flags & ~(DV_FLAG_RESTORE | DV_FLAG_DECISION | DV_FLAG_REORDER))
         return fail(DV_EUNSUPPORTED, "unknown flag bits 0x%x", c->flags);
+    if ((c->flags & DV_FLAG_RESTORE) && (c->flags & DV_FLAG_REORDER))
+        return fail(DV_EUNSUPPORTED, "the restoration layer is not supported with reordered "
+                    "referencing");
     if (c->image_size % c->patch) return fail(DV_EUNSUPPORTED, "image_size %% patch != 0");
     if (c->width % c->heads) return fail(DV_EUNSUPPORTED, "width %% heads != 0");
     const int dh = c->width / c->heads;
@@ -114,10 +124,12 @@ int check_config(const dv_config* c, Dims* d) {
     d->bf16 = bf;
     d->restore = (c->flags & DV_FLAG_RESTORE) != 0;
     d->decision = (c->flags & DV_FLAG_DECISION) != 0;
+    d->reorder = (c->flags & DV_FLAG_REORDER) != 0;
+    d->Bw = d->B + (d->reorder ? 1 : 0);
     if (!attention_supported(bf, d->N, dh))
         return fail(DV_EUNSUPPORTED, "attention for N=%d tokens, head dim %d is not supported "
                     "(bf16: head dim 64/80/96/128; keys and values of a head must fit in LDS)", d->N, dh);
-    const size_t T = (size_t)d->B * d->N;
+    const size_t T = (size_t)d->Bw * d->N;
     const size_t widest = (size_t)std::max(std::max(3 * d->D, d->Dm), d->Kp);
     if (round_up(T, ROW_PAD) * widest >= (1ull << 31) || T >= (1ull << 30))
         return fail(DV_EUNSUPPORTED, "max_batch_frames * tokens too large for 32-bit row indices");
@@ -162,6 +174,8 @@ struct dv_handle {
     int* ridx = nullptr;   // [T] reused tokens (restoration)
     float* tcls = nullptr; // [B, H, N] class-token attention weights of the last layer, per head
                            // (decision MLP)
+    uint8_t* srcmap = nullptr;   // [T] reordered: 1 where the future anchor supplies the token
+    int* root = nullptr;         // [T] reordered: frame that recomputes a reused token
     void* Hr = nullptr;    // [Tp, 128] elem: restoration hidden rows
     int *idx_id, *pos_id, *qoff_id;  // identity lists (reuse off)
     int id_frames = -1;              // frames the identity lists were built for
@@ -265,6 +279,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
     const bool restore = d.restore && !dense;
     // learned decision gate: gate mode only (injected maps and the sentinels bypass it)
     const bool decide = d.decision && mode == GATE_COS;
+    const bool reord = d.reorder && !dense;
 
     for (int l = 0; l < L; ++l) {
         const LayerW& w = h->layers[l];
@@ -282,8 +297,9 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             ga.layer = l;
             ga.mode = mode;
             ga.tau = tau;
-            // restored rows differ from the reference's: no shortcut from the previous map
-            ga.prev = (mode == GATE_COS && !restore) ? prev : nullptr;
+            // restored rows differ from the reference's, and under reordering a token's source
+            // may change from layer to layer: no shortcut from the previous map
+            ga.prev = (mode == GATE_COS && !restore && !reord) ? prev : nullptr;
             ga.inj = inj;
             ga.cur = dense ? nullptr : cur;
             ga.out_masks = om;
@@ -295,6 +311,8 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             ga.dec = decide ? w.dec : nullptr;
             ga.tcls = (decide && l > 0) ? h->tcls : nullptr;
             ga.H = d.H;
+            ga.reorder = reord;
+            ga.src = reord ? h->srcmap : nullptr;
             launch_gate(bf, ga, s);
         }
         if (!dense) {
@@ -302,6 +320,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             launch_scan(h->cnt, gate_chunks(N), F, restore ? T : 0, h->qoff, h->M, s);
             launch_compact(cur, h->qoff, F, N, G, h->idx, h->pos_, nullptr,
                            restore ? h->ridx : nullptr, s);
+            if (reord) launch_resolve(cur, h->srcmap, F, N, G, h->pos_, h->root, s);
         }
         if (restore) {   // restoration hidden rows: GELU(dx W_r1^T + b_r1), before LN2 reuses A
             Scope sc(h, DV_STAGE_RESTORE, s);
@@ -346,7 +365,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         at.N = N;
         at.D = D;
         at.H = d.H;
-        at.G = dense ? 0 : G;
+        at.G = (dense || reord) ? 0 : G;   // per-group blocks assume the star
         at.cus = h->cus;
         {
             Scope sc(h, DV_STAGE_ATTN, s);
@@ -354,7 +373,9 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         }
         if (decide && l + 1 < L) {   // the next layer's importance cue
             Scope sc(h, DV_STAGE_CLS, s);
-            launch_cls_attention(bf, at, h->tcls, s);
+            AttnArgs ac = at;
+            ac.G = G;   // I frames are not gated
+            launch_cls_attention(bf, ac, h->tcls, s);
         }
         {
             Scope sc(h, DV_STAGE_OPROJ, s);
@@ -411,11 +432,14 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             r.N = N;
             r.G = G;
             launch_gemm(Epi::Restore, bf, r, s);
+        } else if (reord) {   // reused rows: the new row of the frame that recomputed them
+            Scope sc(h, DV_STAGE_MERGE, s);
+            launch_merge(h->x, cur, h->root, F, N, D, G, s);
         } else if (mode == GATE_INJECT || mode == GATE_ALL ||
                    (mode == GATE_COS && tokens && l == L - 1)) {
             // reused rows take the reference's new row (gate mode: only to hand out tokens)
             Scope sc(h, DV_STAGE_MERGE, s);
-            launch_merge(h->x, cur, F, N, D, G, s);
+            launch_merge(h->x, cur, nullptr, F, N, D, G, s);
         }
     }
     {
@@ -442,11 +466,17 @@ int encode_impl(dv_handle* h, const float* frames, int n, int G, float tau, cons
         mode = (tau == -INFINITY) ? GATE_NONE : (tau == INFINITY) ? GATE_ALL : GATE_COS;
     }
     const Dims& d = h->d;
+    if (d.reorder && G % 4)
+        return fail(DV_EINVAL, "reordered referencing needs a group_size that is a multiple of 4 "
+                    "(got %d)", G);
     const int per = (d.B / G) * G;
     const size_t img = (size_t)3 * d.S * d.S;
     HIP_TRY(hipSetDevice(h->device));
     for (int f0 = 0; f0 < n; f0 += per) {
-        const int F = std::min(per, n - f0);
+        const int F0 = std::min(per, n - f0);
+        // reordering: the next batch's first frame, an I frame, closes this batch's last block
+        // (its results are computed again, identically, as part of the next batch)
+        const int F = F0 + (d.reorder && f0 + F0 < n ? 1 : 0);
         const size_t ml = (size_t)d.L * d.N;
         int rc = run_batch(h, frames + (size_t)f0 * img, F, G, mode, tau,
                            masks ? masks + (size_t)f0 * ml : nullptr, emb + (size_t)f0 * d.D,
@@ -638,7 +668,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     }
 
     // --- workspace ----------------------------------------------------------------------------
-    const size_t T = (size_t)d.B * N, Tp = round_up(T, ROW_PAD);
+    const size_t T = (size_t)d.Bw * N, Tp = round_up(T, ROW_PAD);
     const size_t Awide = std::max((size_t)D, (size_t)d.Kp);
     size_t need = 0;
     auto sz = [&](size_t bytes) { need += round_up(bytes, 256); };
@@ -653,15 +683,19 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     for (int i = 0; i < 2; ++i) {
         sz(T * 4);
         sz(T * 4);
-        sz((d.B + 1) * 4);
+        sz((d.Bw + 1) * 4);
     }
-    sz((size_t)d.B * gate_chunks(d.N) * 4);
+    sz((size_t)d.Bw * gate_chunks(d.N) * 4);
     sz(4 * 4);
     if (d.restore) {
         sz(T * 4);             // ridx
         sz(Tp * RH * el);      // Hr
     }
     if (d.decision) sz(T * d.H * 4);   // tcls
+    if (d.reorder) {
+        sz(T);       // srcmap
+        sz(T * 4);   // root
+    }
     {
         hipError_t e = hipMalloc(&h->ws, need);
         if (e != hipSuccess) {
@@ -685,17 +719,21 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     h->mask[1] = carve<uint8_t>(p, T);
     h->idx = carve<int>(p, T);
     h->pos_ = carve<int>(p, T);
-    h->qoff = carve<int>(p, d.B + 1);
+    h->qoff = carve<int>(p, d.Bw + 1);
     h->idx_id = carve<int>(p, T);
     h->pos_id = carve<int>(p, T);
-    h->qoff_id = carve<int>(p, d.B + 1);
-    h->cnt = carve<int>(p, (size_t)d.B * gate_chunks(d.N));
+    h->qoff_id = carve<int>(p, d.Bw + 1);
+    h->cnt = carve<int>(p, (size_t)d.Bw * gate_chunks(d.N));
     h->M = carve<int>(p, 4);
     if (d.restore) {
         h->ridx = carve<int>(p, T);
         h->Hr = carve<char>(p, Tp * RH * el);
     }
     if (d.decision) h->tcls = carve<float>(p, T * d.H);
+    if (d.reorder) {
+        h->srcmap = carve<uint8_t>(p, T);
+        h->root = carve<int>(p, T);
+    }
     *out = h;
     return DV_OK;
 }

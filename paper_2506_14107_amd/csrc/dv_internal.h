@@ -23,6 +23,29 @@ __host__ __device__ inline float bf16_to_f32(uint16_t h) {
 // `units` units of G items each, in whole rounds of 8:
 inline int xcd_unit_grid(int units, int G) { return (units + 7) / 8 * 8 * G; }
 
+// ---- reordered referencing (I/P/B frames with past and future references) --------------------
+// Groups of G frames (G a multiple of 4) start with an I frame, computed in full.  Positions
+// 4, 8, ... of a group are P frames referencing the anchor four frames back.  Between two
+// anchors a and a + 4 (the next group's I frame closes the group's last block) the frame at
+// a + 2 is B_dist2, referencing both anchors, and those at a + 1 and a + 3 are B_dist1,
+// referencing their neighbours among a, a + 2, a + 4.  A reference at or past frame F (the
+// end of the frames at hand) is absent (-1).  type: 0 I, 1 P, 2 B_dist2, 3 B_dist1.
+struct FrameRefs {
+    int type, past, fut;
+};
+__host__ __device__ inline FrameRefs reorder_refs(int f, int G, int F) {
+    const int p = f % G;
+    if (p == 0) return {0, -1, -1};
+    const int d = p & 3, a = f - d;
+    FrameRefs q;
+    if (d == 0) q = {1, f - 4, -1};
+    else if (d == 2) q = {2, a, a + 4};
+    else if (d == 1) q = {3, a, a + 2};
+    else q = {3, a + 2, a + 4};
+    if (q.fut >= F) q.fut = -1;
+    return q;
+}
+
 // ---- GEMM ------------------------------------------------------------------------------------
 // C[M, Nout] = A[M, K] * W[Nout, K]^T with a fused epilogue.  M is read on the device.
 enum class Epi : int {
@@ -117,6 +140,8 @@ struct GateArgs {
     const float* tcls;    // [F, H, N] class-token attention weights of the previous layer, per
                           // head (nullptr: 1/N); the cue is their mean over the H heads
     int H;
+    int reorder;          // reordered referencing (reorder_refs) instead of the star
+    uint8_t* src;         // [F*N] reordered: 1 where the future reference supplies the token
 };
 constexpr int DEC_HIDDEN = 64;   // decision MLP hidden units: one per lane of a wavefront
 constexpr int DEC_FEAT = 6;      // its features: s, t, one-hot type (I, P, B_dist2, B_dist1)
@@ -140,8 +165,14 @@ void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G,
 // LayerNorm of rows (optionally gathered through idx) into elem rows: dst[r] = LN(src[g(r)])
 void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* Mdev, int Mmax,
                     int D, const float* g, const float* b, void* dst, hipStream_t s);
-// x[f*N+i] = x[ref(f)*N+i] for every token with cur[f*N+i] != 0
-void launch_merge(float* x, const uint8_t* cur, int F, int N, int D, int G, hipStream_t s);
+// x[f*N+i] = x[r*N+i] for every token with cur[f*N+i] != 0, r = root[f*N+i] (root == nullptr:
+// the group's first frame)
+void launch_merge(float* x, const uint8_t* cur, const int* root, int F, int N, int D, int G,
+                  hipStream_t s);
+// Reordered referencing: for every reused token, follow the sources (src, reorder_refs) to the
+// frame r that recomputes it; pos[f*N+i] = pos[r*N+i], root[f*N+i] = r.
+void launch_resolve(const uint8_t* cur, const uint8_t* src, int F, int N, int G, int* pos,
+                    int* root, hipStream_t s);
 // emb[f] = LN(x[f*N]) (class token)
 void launch_final_ln(const float* x, int F, int N, int D, const float* g, const float* b,
                      float* emb, hipStream_t s);

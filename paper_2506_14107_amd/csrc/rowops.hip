@@ -67,12 +67,27 @@ __global__ void cls_init_k(float* x, const float* cls, const float* pos, int F, 
 // With `prev`, a token reused at the previous layer holds no row of its own (it is the
 // reference's row): its cosine is exactly 1.  Under the decision MLP such a token may be
 // recomputed; the gate then writes the reference's row into the token's row first.
-template <bool BF, bool DEC>
+// Under reordered referencing a frame has up to two references: the similarity is the larger
+// cosine, `src` records which reference gave it (1: the future one; a tie keeps the past one),
+// and the cosines are taken in every mode but reuse-off, since they choose the source.
+template <bool BF, bool DEC, bool REORD>
 __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     const int N = a.N, D = a.D;
     const int chunks = (N + GATE_TOK - 1) / GATE_TOK;
     const int f = blockIdx.x / chunks, ch = blockIdx.x % chunks;
-    const int r = (f / a.G) * a.G;
+    // the frame's references: star -- the group's first frame (the others play P frames);
+    // reordered -- its I/P/B anchors
+    int ftype, r, rfut;
+    if constexpr (REORD) {
+        const FrameRefs q = reorder_refs(f, a.G, a.F);
+        ftype = q.type;
+        r = q.past;
+        rfut = q.fut;
+    } else {
+        r = (f / a.G) * a.G;
+        ftype = r == f ? 0 : 1;
+        rfut = -1;
+    }
     const int lane = threadIdx.x & (WAVE - 1), wave = threadIdx.x / WAVE;
     const int nwaves = blockDim.x / WAVE;
     const int nchunk = D / 4;
@@ -81,15 +96,15 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     const float4* g4 = (const float4*)a.ln_g;
     const float4* b4 = (const float4*)a.ln_b;
     // decision MLP (Section 3.3): lane k holds hidden unit k -- its input weights for s and t,
-    // its bias plus the weight of the P entry of the one-hot frame type (every non-reference
-    // frame references its group's first frame alone), and its output weight
+    // its bias plus the weight of the frame's entry of the one-hot frame type, and its output
+    // weight
     static_assert(DEC_HIDDEN == WAVE, "one hidden unit per lane");
     float dw_s = 0.f, dw_t = 0.f, dw_b = 0.f, dw_o = 0.f, db_o = 0.f;
     if constexpr (DEC) {
         const float* w1 = a.dec + lane * DEC_FEAT;
         dw_s = w1[0];
         dw_t = w1[1];
-        dw_b = a.dec[DEC_HIDDEN * DEC_FEAT + lane] + w1[2 + 1];
+        dw_b = a.dec[DEC_HIDDEN * DEC_FEAT + lane] + w1[2 + ftype];
         dw_o = a.dec[DEC_HIDDEN * DEC_FEAT + DEC_HIDDEN + lane];
         db_o = a.dec[DEC_HIDDEN * DEC_FEAT + 2 * DEC_HIDDEN];
     }
@@ -112,15 +127,40 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     for (int i = ch * GATE_TOK + wave; i < i_end; i += nwaves) {
         const size_t row = (size_t)f * N + i;
         float4* xf = (float4*)(a.x + row * D);
-        int reuse = 0;
+        int reuse = 0, from_fut = 0;
         bool loaded = false;
         float4 v[MAX_CHUNKS];
-        if (f != r && i != 0) {
-            if (a.mode == GATE_INJECT) {
+        // cosine of this token's row (loaded into v on the first call) with reference row xr
+        auto cosine = [&](const float4* xr) {
+            float dot = 0.f, na = 0.f, nb = 0.f;
+            int eq = 1;
+#pragma unroll
+            for (int k = 0; k < MAX_CHUNKS; ++k) {
+                const int c = lane + k * WAVE;
+                if (c < nchunk) {
+                    if (!loaded) v[k] = xf[c];
+                    const float4 u = v[k], w = xr[c];
+                    dot += u.x * w.x + u.y * w.y + u.z * w.z + u.w * w.w;
+                    na += u.x * u.x + u.y * u.y + u.z * u.z + u.w * u.w;
+                    nb += w.x * w.x + w.y * w.y + w.z * w.z + w.w * w.w;
+                    eq &= (u.x == w.x) & (u.y == w.y) & (u.z == w.z) & (u.w == w.w);
+                }
+            }
+            loaded = true;
+            dot = wave_sum(dot);
+            na = wave_sum(na);
+            nb = wave_sum(nb);
+            const bool same = __all(eq);
+            float cs = dot / fmaxf(sqrtf(na) * sqrtf(nb), 1e-8f);
+            cs = fminf(1.0f, fmaxf(-1.0f, cs));
+            return same ? 1.0f : cs;
+        };
+        if (ftype != 0 && i != 0) {
+            if (a.mode == GATE_INJECT && !REORD) {
                 reuse = a.inj[((size_t)f * a.L + a.layer) * N + i] != 0;
-            } else if (a.mode == GATE_ALL) {
+            } else if (a.mode == GATE_ALL && !REORD) {
                 reuse = 1;
-            } else if (a.mode == GATE_COS) {
+            } else if (a.mode != GATE_NONE) {
                 if (a.prev && a.prev[row]) {
                     // a reused token stands for the reference's row: cosine exactly 1
                     if constexpr (DEC) {
@@ -141,30 +181,17 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
                         reuse = a.tau <= 1.0f;
                     }
                 } else {
-                    const float4* xr = (const float4*)(a.x + ((size_t)r * N + i) * D);
-                    float dot = 0.f, na = 0.f, nb = 0.f;
-                    int eq = 1;
-#pragma unroll
-                    for (int k = 0; k < MAX_CHUNKS; ++k) {
-                        const int c = lane + k * WAVE;
-                        if (c < nchunk) {
-                            const float4 u = xf[c], w = xr[c];
-                            v[k] = u;
-                            dot += u.x * w.x + u.y * w.y + u.z * w.z + u.w * w.w;
-                            na += u.x * u.x + u.y * u.y + u.z * u.z + u.w * u.w;
-                            nb += w.x * w.x + w.y * w.y + w.z * w.z + w.w * w.w;
-                            eq &= (u.x == w.x) & (u.y == w.y) & (u.z == w.z) & (u.w == w.w);
-                        }
+                    float cs = cosine((const float4*)(a.x + ((size_t)r * N + i) * D));
+                    if (REORD && rfut >= 0) {   // the better of the two references
+                        const float c2 = cosine((const float4*)(a.x + ((size_t)rfut * N + i) * D));
+                        from_fut = c2 > cs;
+                        cs = fmaxf(cs, c2);
                     }
-                    loaded = true;
-                    dot = wave_sum(dot);
-                    na = wave_sum(na);
-                    nb = wave_sum(nb);
-                    const bool same = __all(eq);
-                    float cs = dot / fmaxf(sqrtf(na) * sqrtf(nb), 1e-8f);
-                    cs = fminf(1.0f, fmaxf(-1.0f, cs));
-                    if (same) cs = 1.0f;
-                    if constexpr (DEC) {
+                    if (a.mode == GATE_INJECT) {
+                        reuse = a.inj[((size_t)f * a.L + a.layer) * N + i] != 0;
+                    } else if (a.mode == GATE_ALL) {
+                        reuse = 1;
+                    } else if constexpr (DEC) {
                         reuse = decision(cs, i) > a.tau;
                     } else {
                         reuse = cs >= a.tau;
@@ -237,7 +264,8 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
         }
         if (lane == 0) {
             if (a.cur) a.cur[row] = (uint8_t)reuse;
-            if (om) om[i] = (uint8_t)reuse;
+            if (REORD) a.src[row] = (uint8_t)from_fut;
+            if (om) om[i] = (uint8_t)(reuse ? 1 + from_fut : 0);   // 2: from the future anchor
             active += !reuse;
         }
     }
@@ -407,19 +435,43 @@ __global__ __launch_bounds__(256) void ln_rows_k(const float* __restrict__ src,
     }
 }
 
-__global__ __launch_bounds__(256) void merge_k(float* x, const uint8_t* cur, int F, int N, int D,
-                                               int G) {
+__global__ __launch_bounds__(256) void merge_k(float* x, const uint8_t* cur, const int* root, int F,
+                                               int N, int D, int G) {
     const int lane = threadIdx.x & 63;
     const int total = F * N;
     for (int t = (blockIdx.x * blockDim.x + threadIdx.x) / 64; t < total;
          t += gridDim.x * blockDim.x / 64) {
         if (!cur[t]) continue;
         const int f = t / N, i = t % N;
-        const int r = (f / G) * G;
+        const int r = root ? root[t] : (f / G) * G;
         if (r == f) continue;
         const float4* s = (const float4*)(x + ((size_t)r * N + i) * D);
         float4* d = (float4*)(x + (size_t)t * D);
         for (int c = lane; c < D / 4; c += 64) d[c] = s[c];
+    }
+}
+
+// --- reordered referencing: where a reused token's key/value row and new row come from -------
+// A reused token takes them from the same token of the reference that supplied it, which may be
+// reused in turn; the chain ends at a frame that recomputes the token (I frames recompute every
+// token, and every step moves to an earlier frame of the processing order, so a chain is at
+// most a few frames long).  pos of recomputed tokens is already set; reused ones copy it.
+__global__ __launch_bounds__(256) void resolve_k(const uint8_t* __restrict__ cur,
+                                                 const uint8_t* __restrict__ src, int F, int N,
+                                                 int G, int* pos, int* root) {
+    const int total = F * N;
+    for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += gridDim.x * blockDim.x) {
+        if (!cur[t]) continue;
+        const int i = t % N;
+        int r = t / N;
+        for (int hop = 0; hop < 64 && cur[(size_t)r * N + i]; ++hop) {
+            const FrameRefs q = reorder_refs(r, G, F);
+            const int next = src[(size_t)r * N + i] ? q.fut : q.past;
+            if (next < 0) break;
+            r = next;
+        }
+        pos[t] = pos[(size_t)r * N + i];
+        root[t] = r;
     }
 }
 
@@ -481,14 +533,18 @@ void launch_cls_init(float* x, const float* cls, const float* pos, int F, int N,
 }
 
 void launch_gate(bool bf16, const GateArgs& a, hipStream_t s) {
-    const int grid = a.F * gate_chunks(a.N);
+    const dim3 grid(a.F * gate_chunks(a.N)), block(256);
     const bool dec = a.dec != nullptr && a.mode == GATE_COS;
-    if (bf16) {
-        if (dec) hipLaunchKernelGGL((gate_k<true, true>), dim3(grid), dim3(256), 0, s, a);
-        else hipLaunchKernelGGL((gate_k<true, false>), dim3(grid), dim3(256), 0, s, a);
-    } else {
-        if (dec) hipLaunchKernelGGL((gate_k<false, true>), dim3(grid), dim3(256), 0, s, a);
-        else hipLaunchKernelGGL((gate_k<false, false>), dim3(grid), dim3(256), 0, s, a);
+    const int v = (bf16 ? 4 : 0) + (dec ? 2 : 0) + (a.reorder ? 1 : 0);
+    switch (v) {
+        case 0: hipLaunchKernelGGL((gate_k<false, false, false>), grid, block, 0, s, a); break;
+        case 1: hipLaunchKernelGGL((gate_k<false, false, true>), grid, block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((gate_k<false, true, false>), grid, block, 0, s, a); break;
+        case 3: hipLaunchKernelGGL((gate_k<false, true, true>), grid, block, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((gate_k<true, false, false>), grid, block, 0, s, a); break;
+        case 5: hipLaunchKernelGGL((gate_k<true, false, true>), grid, block, 0, s, a); break;
+        case 6: hipLaunchKernelGGL((gate_k<true, true, false>), grid, block, 0, s, a); break;
+        default: hipLaunchKernelGGL((gate_k<true, true, true>), grid, block, 0, s, a); break;
     }
 }
 
@@ -517,9 +573,16 @@ void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* M
                            D, g, b, dst);
 }
 
-void launch_merge(float* x, const uint8_t* cur, int F, int N, int D, int G, hipStream_t s) {
+void launch_merge(float* x, const uint8_t* cur, const int* root, int F, int N, int D, int G,
+                  hipStream_t s) {
     hipLaunchKernelGGL(merge_k, dim3(grid_for((size_t)F * N, 4, 4096)), dim3(256), 0, s, x, cur,
-                       F, N, D, G);
+                       root, F, N, D, G);
+}
+
+void launch_resolve(const uint8_t* cur, const uint8_t* src, int F, int N, int G, int* pos,
+                    int* root, hipStream_t s) {
+    hipLaunchKernelGGL(resolve_k, dim3(grid_for((size_t)F * N, 256)), dim3(256), 0, s, cur, src,
+                       F, N, G, pos, root);
 }
 
 void launch_final_ln(const float* x, int F, int N, int D, const float* g, const float* b,

@@ -20,6 +20,7 @@ STAGES = ["patch", "gate", "compact", "ln1", "qkv", "attn", "oproj", "ln2", "fc1
           "merge", "final", "restore", "cls"]
 DV_FLAG_RESTORE = 1
 DV_FLAG_DECISION = 2
+DV_FLAG_REORDER = 4
 
 
 class DejaVuError(RuntimeError):
@@ -163,7 +164,8 @@ class Encoder:
         m = model
         self.model = m
         flags = (DV_FLAG_RESTORE if getattr(m, "restore", False) else 0) | \
-            (DV_FLAG_DECISION if getattr(m, "decision", False) else 0)
+            (DV_FLAG_DECISION if getattr(m, "decision", False) else 0) | \
+            (DV_FLAG_REORDER if getattr(m, "reorder", False) else 0)
         self.cfg = make_config(m.image_size, m.patch, m.depth, m.width, m.heads, m.mlp, m.dtype,
                                max_batch_frames, flags)
         self.handle = dv_create(self.cfg, weights)
