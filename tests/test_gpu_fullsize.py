@@ -87,3 +87,67 @@ def test_full_size_restoration():
               f"{c_e:.5f} rel {r_e:.2e}, tok cos {c_t:.5f} rel {r_t:.2e}", flush=True)
         assert bad == 0, f"{bad} decisions differ outside the 1e-3 band"
     enc.close()
+
+
+def test_full_size_decision_gate():
+    """ViT-L/14, 256 frames gated by the decision MLP (random decision weights, threshold at
+    about 70 % reuse): sampled groups against the oracle replaying the GPU's maps, decisions
+    judged outside the weight-derived margin."""
+    from .test_gpu_decision import decision_band, decision_parity
+    torch = require_gpu()
+    w = synth.get_config("vit_l14")
+    m, G = dataclasses.replace(w.model, decision=True), w.group_size
+    tau = -0.875
+    wts = synth.make_weights(m, w.weight_seed)
+    blob = synth.pack_weights(wts, m)
+    fr = synth.render_frames(w.video, m.image_size, 0, 256)
+    enc = encoder(m, blob, w.batch_frames)
+    emb, masks, toks = enc.encode(dev(fr), G, tau, want_tokens=True)
+    torch.cuda.synchronize()
+    mg = host(masks)
+    rho = oracle.reuse_rate(mg, G)
+    print(f"[vit_l14 decision] GPU reuse {rho:.3f}", flush=True)
+    assert 0.05 < rho < 0.99, f"threshold gives degenerate reuse {rho}"
+    for g0 in (0, 128):
+        sl = slice(g0, g0 + G)
+        r = oracle.encode(fr[sl], blob, m.as_dict(), G, masks=mg[sl])
+        bad, inside = decision_parity(mg[sl], r, decision_band(wts, m, r["t"]), tau)
+        c_e, r_e = check_close(host(emb[sl]), r["emb"], "bf16", f"group {g0} embeddings")
+        c_t, r_t = check_close(host(toks[sl]), r["tokens"], "bf16", f"group {g0} tokens")
+        print(f"[vit_l14 decision] group {g0}: decisions off {bad}, in band {inside:.2%}, emb "
+              f"cos {c_e:.5f} rel {r_e:.2e}, tok cos {c_t:.5f} rel {r_t:.2e}", flush=True)
+        assert bad == 0, f"{bad} decisions differ outside the margin"
+    enc.close()
+
+
+def test_full_size_reordered_referencing():
+    """ViT-L/14, 256 frames with reordered I/P/B referencing: sampled groups (plus the next
+    group's I frame, their last block's future anchor) against the oracle replaying the GPU's
+    maps and sources."""
+    from .test_gpu_reorder import reorder_parity
+    torch = require_gpu()
+    w = synth.get_config("vit_l14")
+    m, G = dataclasses.replace(w.model, reorder=True), w.group_size
+    tau = float(np.float32(0.955))
+    blob = synth.make_blob(m, w.weight_seed)
+    fr = synth.render_frames(w.video, m.image_size, 0, 256)
+    enc = encoder(m, blob, w.batch_frames)
+    emb, masks, toks = enc.encode(dev(fr), G, tau, want_tokens=True)
+    torch.cuda.synchronize()
+    mg = host(masks)
+    rho = oracle.reuse_rate(mg, G)
+    print(f"[vit_l14 reorder] GPU reuse {rho:.3f}, from future anchors "
+          f"{np.mean(mg[mg != 0] == 2):.2%}", flush=True)
+    assert 0.05 < rho < 0.99, f"threshold gives degenerate reuse {rho}"
+    for g0 in (0, 128):
+        sl = slice(g0, g0 + G + 1)
+        r = oracle.encode(fr[sl], blob, m.as_dict(), G, masks=(mg[sl] != 0),
+                          sources=(mg[sl] == 2))
+        bad, bad_src, inside = reorder_parity(mg[sl], r, tau)
+        c_e, r_e = check_close(host(emb[sl]), r["emb"], "bf16", f"group {g0} embeddings")
+        c_t, r_t = check_close(host(toks[sl]), r["tokens"], "bf16", f"group {g0} tokens")
+        print(f"[vit_l14 reorder] group {g0}: decisions off {bad}, sources off {bad_src}, in "
+              f"band {inside:.2%}, emb cos {c_e:.5f} rel {r_e:.2e}, tok cos {c_t:.5f} rel "
+              f"{r_t:.2e}", flush=True)
+        assert bad == 0 and bad_src == 0
+    enc.close()
