@@ -225,6 +225,9 @@ def main():
                          "threshold on its output is calibrated like tau)")
     ap.add_argument("--reorder", action="store_true",
                     help="reordered I/P/B referencing with past and future references")
+    ap.add_argument("--stream-chunk", type=int, default=0,
+                    help="deliver each batch to the timed encodes as a stream of calls of this "
+                         "many frames (dv_stream_encode; groups span calls)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device-to-device copy (HBM counter calibration)")
     ap.add_argument("--traffic-record", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_OUT"),
@@ -306,11 +309,20 @@ def main():
     dominant = max(prof, key=lambda s: prof[s][0])
     log("[bench] stage ms per sweep: " + ", ".join(f"{k} {v[0]:.2f}" for k, v in prof.items() if v[1]))
 
+    def encode_all(tau):
+        """One encode of the batch: one call, or a stream of calls of --stream-chunk frames."""
+        if not args.stream_chunk:
+            enc.encode(x, G, tau, want_masks=False)
+            return
+        enc.stream_reset()
+        for k in range(0, F, args.stream_chunk):
+            enc.stream_encode(x[k:k + args.stream_chunk], G, tau, want_masks=False)
+
     # dense reference (same kernels, reuse off)
     def time_calls(tau_list, steps, warmup, profile_stage=None):
         for _ in range(warmup):
             for tau in tau_list:
-                enc.encode(x, G, tau, want_masks=False)
+                encode_all(tau)
         torch.cuda.synchronize()
         if profile_stage:
             enc.profile([profile_stage])
@@ -318,7 +330,7 @@ def main():
         s.record()
         for _ in range(steps):
             for tau in tau_list:
-                enc.encode(x, G, tau, want_masks=False)
+                encode_all(tau)
         e.record()
         torch.cuda.synchronize()
         ms = s.elapsed_time(e)
@@ -405,6 +417,8 @@ def main():
                                   else "")
                                + ("reordered I/P/B referencing (past and future anchors); "
                                   if m.reorder else "")
+                               + (f"streamed in calls of {args.stream_chunk} frames; "
+                                  if args.stream_chunk else "")
                                + "reuse levels "
                                + "/".join(f"{t:.0%}" for t in targets if t is not None),
                    "frames_per_step": F * len(taus), "group_size": G},

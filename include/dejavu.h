@@ -194,6 +194,24 @@ int dv_encode_tokens(dv_handle* h, const float* frames, int n_frames, int group_
                      const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,
                      float* out_tokens, hipStream_t stream);
 
+/* Streaming (frames arriving in calls of any size; Section 6.3's periodic I frame every G
+ * frames, and a group may span calls).  The handle numbers the frames of successive
+ * dv_stream_encode calls g = 0, 1, ... since the last dv_stream_reset (or creation); frame g's
+ * reference is frame G * floor(g / G), which may have come in an earlier call: the handle then
+ * keeps that reference's per-layer input rows and keys/values in a cache ((L+1) N D fp32 plus
+ * L N 2D dtype elements, allocated by the first stream call) instead of recomputing it.  Results
+ * are those of one dv_encode_tokens call over all frames of the stream.  frames, masks (NULL:
+ * gate mode with tau), out_embeddings, out_masks and out_tokens (both may be NULL) cover this
+ * call's frames, with the layouts of dv_encode_tokens.  group_size must stay the same until the
+ * next reset.  Not available with DV_FLAG_REORDER (DV_EUNSUPPORTED).  Errors as
+ * dv_encode_tokens, plus DV_EINVAL for a changed group_size or a stream left inconsistent by a
+ * failed call (reset it), DV_ENOMEM for the cache. */
+int dv_stream_encode(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
+                     const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,
+                     float* out_tokens, hipStream_t stream);
+/* Forget the stream position and the cached reference (the cache memory is kept). */
+int dv_stream_reset(dv_handle* h);
+
 /* Stream compaction of a reuse map on its own (token filtration, Section 3.3;
  * stream compaction across the frames of a batch, Section 5.3).
  * masks: device u8 [n_frames, n_tokens], 1 = reused; entries of reference

@@ -21,6 +21,12 @@
 //      key/value row is resolved along those sources to the frame that recomputes it; after
 //      FC2 every reused row is copied from that frame's new row.  An internal batch also
 //      carries the next batch's first frame (an I frame, the future anchor of its last block).]
+//   [stream (dv_stream_encode): a group may span calls.  The reference of a group that is still
+//    open when a call ends keeps its per-layer input rows and keys/values in a cache; the next
+//    call's first batch starts with that reference as local frame 0 (rows copied from the
+//    cache, not recomputed), then gap frames standing for the group's frames of earlier calls,
+//    then the call's own frames, so that groups keep their positions (frame f's reference is
+//    frame G * floor(f / G) of the batch).]
 //   final LayerNorm of the class tokens.
 // Nothing is read back to the host inside an encode call.
 //
@@ -176,6 +182,14 @@ struct dv_handle {
                            // (decision MLP)
     uint8_t* srcmap = nullptr;   // [T] reordered: 1 where the future anchor supplies the token
     int* root = nullptr;         // [T] reordered: frame that recomputes a reused token
+    int ext_row = 0;             // packed row of the cached reference's first key/value row
+    // stream state: frames seen since the last reset, their group size, and the cached
+    // reference (stream frame index, -1 none) with its rows
+    long long st_pos = 0;
+    int st_G = 0;
+    long long st_ref = -1;
+    float* xc = nullptr;   // [L+1, N, D] the cached reference's layer inputs x^0 .. x^L
+    void* kvc = nullptr;   // [L, N, 2D] elem: its keys and values per layer
     void* Hr = nullptr;    // [Tp, 128] elem: restoration hidden rows
     int *idx_id, *pos_id, *qoff_id;  // identity lists (reuse off)
     int id_frames = -1;              // frames the identity lists were built for
@@ -236,8 +250,13 @@ int collect(dv_handle* h) {
 }
 
 // ---- one batch of whole groups --------------------------------------------------------------
+// frames, inj, emb, om, tokens start at local frame `skip`; frames below skip are carried over
+// from an earlier call of a stream (0: the cached reference; the others stand for frames
+// already returned).  fill >= 0: cache local frame fill, a reference whose group continues in
+// the next call.
 int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float tau,
-              const uint8_t* inj, float* emb, uint8_t* om, float* tokens, hipStream_t s) {
+              const uint8_t* inj, float* emb, uint8_t* om, float* tokens, hipStream_t s,
+              int skip = 0, int fill = -1) {
     const Dims& d = h->d;
     const bool bf = d.bf16;
     const int N = d.N, D = d.D, L = d.L;
@@ -250,10 +269,16 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         h->id_frames = F;
     }
 
+    const size_t row_bytes = (size_t)N * D * sizeof(float);   // one frame's token rows
+    const size_t el = bf ? 2 : 4;
+    const size_t kv_bytes = (size_t)N * 2 * D * el;           // one frame's keys and values
+    float* xs = h->x + (size_t)skip * N * D;                  // the first computed frame's rows
+    if (skip > 0)   // the cached reference's layer-0 rows
+        HIP_TRY(hipMemcpyAsync(h->x, h->xc, row_bytes, hipMemcpyDeviceToDevice, s));
     {   // patch embedding + class-token rows
         Scope sc(h, DV_STAGE_PATCH, s);
-        launch_im2col(bf, frames, F, d.S, d.p, d.Kp, h->A, s);
-        launch_cls_init(h->x, h->cls, h->pos, F, N, D, s);
+        launch_im2col(bf, frames, F - skip, d.S, d.p, d.Kp, h->A, s);
+        launch_cls_init(xs, h->cls, h->pos, F - skip, N, D, s);
         GemmArgs g{};
         g.A = h->A;
         g.W = h->W_pe;
@@ -261,10 +286,10 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         g.K = d.Kp;
         g.Nout = D;
         g.Mdev = nullptr;
-        g.Mconst = F * d.P;
-        g.Mmax = F * d.P;
+        g.Mconst = (F - skip) * d.P;
+        g.Mmax = (F - skip) * d.P;
         g.cus = h->cus;
-        g.out = h->x;
+        g.out = xs;
         g.pos = h->pos;
         g.P = d.P;
         g.N = N;
@@ -285,6 +310,9 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         const LayerW& w = h->layers[l];
         uint8_t* cur = h->mask[l & 1];
         uint8_t* prev = l > 0 ? h->mask[(l - 1) & 1] : nullptr;
+        if (fill >= 0)   // the layer input of a reference carried to the next call
+            HIP_TRY(hipMemcpyAsync(h->xc + (size_t)l * N * D, h->x + (size_t)fill * N * D,
+                                   row_bytes, hipMemcpyDeviceToDevice, s));
         {   // reuse gate + LN1 of every recomputed token (reuse off: LN1 of every token)
             Scope sc(h, DV_STAGE_GATE, s);
             GateArgs ga{};
@@ -313,13 +341,14 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             ga.H = d.H;
             ga.reorder = reord;
             ga.src = reord ? h->srcmap : nullptr;
+            ga.skip = skip;
             launch_gate(bf, ga, s);
         }
         if (!dense) {
             Scope sc(h, DV_STAGE_COMPACT, s);
-            launch_scan(h->cnt, gate_chunks(N), F, restore ? T : 0, h->qoff, h->M, s);
+            launch_scan(h->cnt, gate_chunks(N), F, restore ? (F - skip) * N : 0, h->qoff, h->M, s);
             launch_compact(cur, h->qoff, F, N, G, h->idx, h->pos_, nullptr,
-                           restore ? h->ridx : nullptr, s);
+                           restore ? h->ridx : nullptr, s, skip, h->ext_row);
             if (reord) launch_resolve(cur, h->srcmap, F, N, G, h->pos_, h->root, s);
         }
         if (restore) {   // restoration hidden rows: GELU(dx W_r1^T + b_r1), before LN2 reuses A
@@ -355,6 +384,13 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             g.out = h->qkv;
             launch_gemm(Epi::Qkv, bf, g, s);
         }
+        if (skip > 0)   // the cached reference's keys and values, at packed rows ext_row ..
+            HIP_TRY(hipMemcpy2DAsync((char*)h->qkv + ((size_t)h->ext_row * 3 * D + D) * el,
+                                     3 * D * el, (const char*)h->kvc + (size_t)l * kv_bytes,
+                                     2 * D * el, 2 * D * el, N, hipMemcpyDeviceToDevice, s));
+        if (fill >= 0)
+            launch_copy_ref_kv(h->qkv, qoff, fill, N, D, (int)el,
+                               (char*)h->kvc + (size_t)l * kv_bytes, s);
         g.a_idx = nullptr;
         AttnArgs at{};
         at.qkv = h->qkv;
@@ -365,7 +401,9 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         at.N = N;
         at.D = D;
         at.H = d.H;
-        at.G = (dense || reord) ? 0 : G;   // per-group blocks assume the star
+        // per-group blocks assume the star with the reference's rows packed in the batch
+        at.G = (dense || reord || skip > 0) ? 0 : G;
+        at.skip = skip;
         at.cus = h->cus;
         {
             Scope sc(h, DV_STAGE_ATTN, s);
@@ -414,6 +452,12 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             g.resid = h->Z;
             launch_gemm(Epi::Fc2, bf, g, s);
         }
+        if (skip > 0)   // the cached reference's new rows, for the restoration, merges, next gate
+            HIP_TRY(hipMemcpyAsync(h->x, h->xc + (size_t)(l + 1) * N * D, row_bytes,
+                                   hipMemcpyDeviceToDevice, s));
+        if (fill >= 0 && l == L - 1)
+            HIP_TRY(hipMemcpyAsync(h->xc + (size_t)L * N * D, h->x + (size_t)fill * N * D,
+                                   row_bytes, hipMemcpyDeviceToDevice, s));
         if (restore) {   // reused rows: the reference token's new row + Hr W_r2^T + b_r2
             Scope sc(h, DV_STAGE_RESTORE, s);
             GemmArgs r{};
@@ -444,10 +488,11 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
     }
     {
         Scope sc(h, DV_STAGE_FINAL, s);
-        launch_final_ln(h->x, F, N, D, h->lnf_g, h->lnf_b, emb, s);
+        launch_final_ln(xs, F - skip, N, D, h->lnf_g, h->lnf_b, emb, s);
     }
     if (tokens)
-        HIP_TRY(hipMemcpyAsync(tokens, h->x, (size_t)T * D * sizeof(float), hipMemcpyDeviceToDevice, s));
+        HIP_TRY(hipMemcpyAsync(tokens, xs, (size_t)(F - skip) * row_bytes, hipMemcpyDeviceToDevice,
+                               s));
     return DV_OK;
 }
 
@@ -484,6 +529,67 @@ int encode_impl(dv_handle* h, const float* frames, int n, int G, float tau, cons
                            tokens ? tokens + (size_t)f0 * d.N * d.D : nullptr, s);
         if (rc) return rc;
     }
+    HIP_TRY(hipGetLastError());
+    return DV_OK;
+}
+
+// A stream call: frames get stream indices st_pos .. st_pos + n - 1; frame g's reference is
+// frame G * floor(g / G), possibly from an earlier call (then read from the cache).
+int stream_impl(dv_handle* h, const float* frames, int n, int G, float tau, const uint8_t* masks,
+                float* emb, uint8_t* om, float* tokens, hipStream_t s) {
+    if (!h) return fail(DV_EINVAL, "handle is NULL");
+    if (!frames || !emb) return fail(DV_EINVAL, "frames and out_embeddings must not be NULL");
+    if (n < 1) return fail(DV_EINVAL, "n_frames must be >= 1 (got %d)", n);
+    if (G < 1) return fail(DV_EINVAL, "group_size must be >= 1 (got %d)", G);
+    const Dims& d = h->d;
+    if (G > d.B) return fail(DV_EINVAL, "group_size %d exceeds max_batch_frames %d", G, d.B);
+    if (d.reorder)
+        return fail(DV_EUNSUPPORTED, "streaming with reordered referencing is not supported");
+    if (h->st_pos > 0 && G != h->st_G)
+        return fail(DV_EINVAL, "group_size %d differs from the stream's %d (dv_stream_reset "
+                    "starts a new stream)", G, h->st_G);
+    int mode;
+    if (masks) {
+        mode = GATE_INJECT;
+    } else {
+        if (std::isnan(tau)) return fail(DV_EINVAL, "tau is NaN");
+        mode = (tau == -INFINITY) ? GATE_NONE : (tau == INFINITY) ? GATE_ALL : GATE_COS;
+    }
+    HIP_TRY(hipSetDevice(h->device));
+    const size_t el = d.bf16 ? 2 : 4, N = d.N, D = d.D, L = d.L;
+    if (!h->xc) {   // the reference cache, on the first stream call
+        hipError_t e = hipMalloc((void**)&h->xc, (L + 1) * N * D * sizeof(float));
+        if (e == hipSuccess) e = hipMalloc(&h->kvc, L * N * 2 * D * el);
+        if (e != hipSuccess)
+            return fail(e == hipErrorOutOfMemory ? DV_ENOMEM : DV_EHIP, "stream cache: %s",
+                        hipGetErrorString(e));
+    }
+    const size_t img = (size_t)3 * d.S * d.S, ml = L * N;
+    const long long g0 = h->st_pos;
+    const long long last = (g0 + n - 1) / G * G;   // the last group's reference
+    const bool open = g0 + n < last + G;           // ... whose group continues after this call
+    for (int k = 0; k < n;) {
+        const long long gk = g0 + k, gs = gk / G * G;
+        int lead = 0;   // carried-over frames ahead of frame gk: its reference and the gaps
+        if (gs < gk && mode != GATE_NONE) {
+            if (h->st_ref != gs)
+                return fail(DV_EINVAL, "the stream lost its cached reference (an earlier call "
+                            "failed?): call dv_stream_reset");
+            lead = (int)(gk - gs);
+        }
+        int cnt = std::min(d.B - lead, n - k);
+        if (k + cnt < n) cnt = (int)((gk + cnt) / G * G - gk);   // end on a group boundary
+        const int fill = (open && last >= gk && last < gk + cnt) ? (int)(last - gk) + lead : -1;
+        int rc = run_batch(h, frames + (size_t)k * img, lead + cnt, G, mode, tau,
+                           masks ? masks + (size_t)k * ml : nullptr, emb + (size_t)k * D,
+                           om ? om + (size_t)k * ml : nullptr,
+                           tokens ? tokens + (size_t)k * N * D : nullptr, s, lead, fill);
+        if (rc) return rc;
+        if (fill >= 0) h->st_ref = last;
+        k += cnt;
+    }
+    h->st_pos = g0 + n;
+    h->st_G = G;
     HIP_TRY(hipGetLastError());
     return DV_OK;
 }
@@ -674,7 +780,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     auto sz = [&](size_t bytes) { need += round_up(bytes, 256); };
     sz(T * D * 4);        // x
     sz(Tp * Awide * el);  // A
-    sz(Tp * 3 * D * el);  // qkv
+    sz((Tp + round_up(N, ROW_PAD)) * 3 * D * el);  // qkv (+ a stream's cached reference rows)
     sz(Tp * D * el);      // O
     sz(Tp * D * 4);       // Z
     sz(Tp * Dm * el);     // H
@@ -711,7 +817,8 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     char* p = (char*)h->ws;
     h->x = carve<float>(p, T * D);
     h->A = carve<char>(p, Tp * Awide * el);
-    h->qkv = carve<char>(p, Tp * 3 * D * el);
+    h->qkv = carve<char>(p, (Tp + round_up(N, ROW_PAD)) * 3 * D * el);
+    h->ext_row = (int)Tp;
     h->O = carve<char>(p, Tp * D * el);
     h->Z = carve<float>(p, Tp * D);
     h->Hb = carve<char>(p, Tp * Dm * el);
@@ -749,6 +856,8 @@ int dv_destroy(dv_handle* h) {
     for (auto e : h->pool) (void)hipEventDestroy(e);
     if (h->wmem) (void)hipFree(h->wmem);
     if (h->ws) (void)hipFree(h->ws);
+    if (h->xc) (void)hipFree(h->xc);
+    if (h->kvc) (void)hipFree(h->kvc);
     delete h;
     return DV_OK;
 }
@@ -778,6 +887,21 @@ int dv_encode_tokens(dv_handle* h, const float* frames, int n_frames, int group_
                      float* out_tokens, hipStream_t stream) {
     return encode_impl(h, frames, n_frames, group_size, tau, masks, out_embeddings, out_masks,
                        out_tokens, stream);
+}
+
+int dv_stream_encode(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
+                     const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,
+                     float* out_tokens, hipStream_t stream) {
+    return stream_impl(h, frames, n_frames, group_size, tau, masks, out_embeddings, out_masks,
+                       out_tokens, stream);
+}
+
+int dv_stream_reset(dv_handle* h) {
+    if (!h) return fail(DV_EINVAL, "handle is NULL");
+    h->st_pos = 0;
+    h->st_G = 0;
+    h->st_ref = -1;
+    return DV_OK;
 }
 
 int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size, int32_t* idx,

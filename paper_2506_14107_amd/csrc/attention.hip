@@ -551,7 +551,8 @@ __global__ __launch_bounds__(256) void cls_attn_k(AttnArgs a, float* __restrict_
     const int f = blockIdx.x;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int h = blockIdx.y * 4 + wave;
-    if ((a.G > 0 && f % a.G == 0) || h >= a.H) return;   // reference frames are never gated
+    // reference frames are never gated; frames carried over from an earlier call have no rows
+    if ((a.G > 0 && f % a.G == 0) || f < a.skip || h >= a.H) return;
     const int N = a.N, D = a.D, dh = D / a.H, nch = dh / CE;
     const int sub = lane & 7, kq = lane >> 3;
     float* sc = (float*)smem + (size_t)wave * N;   // scores, then exponentials

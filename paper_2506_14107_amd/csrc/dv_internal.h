@@ -104,6 +104,7 @@ struct AttnArgs {
     int F, N, D, H;
     int G;             // group size, 0 without reuse (block placement only)
     int cus;           // compute units of the device (0: one block per work item)
+    int skip;          // leading frames carried over from an earlier call (no rows, no queries)
 };
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
 // Class-token attention weights of every non-reference frame (G > 0: frames f % G == 0 are
@@ -142,6 +143,9 @@ struct GateArgs {
     int H;
     int reorder;          // reordered referencing (reorder_refs) instead of the star
     uint8_t* src;         // [F*N] reordered: 1 where the future reference supplies the token
+    int skip;             // leading frames carried over from an earlier call of a stream: frame 0
+                          // is the cached reference (its rows already in x), the others gaps;
+                          // none is gated, and inj / out_masks start at frame skip
 };
 constexpr int DEC_HIDDEN = 64;   // decision MLP hidden units: one per lane of a wavefront
 constexpr int DEC_FEAT = 6;      // its features: s, t, one-hot type (I, P, B_dist2, B_dist1)
@@ -159,8 +163,14 @@ void launch_scan(const int* cnt, int per, int F, int tokens, int* qoff, int* M, 
 // lists, qoff_in ignored and qoff_out written)
 // ridx (or nullptr): the reused tokens f*N+i of non-reference frames in frame-major order, at
 // slot (f*N - qoff[f]) + (reused tokens of frame f before i)
+// skip > 0 (stream): frames below skip have no rows; frame 0 is the cached reference, whose keys
+// and values sit at packed rows ext_row .. ext_row + N - 1 (pos of its reused tokens points there)
 void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,
-                    int* pos, int* qoff_out, int* ridx, hipStream_t s);
+                    int* pos, int* qoff_out, int* ridx, hipStream_t s, int skip = 0,
+                    int ext_row = 0);
+// dst[i, 0:2D] = K|V of frame f's packed row qoff[f] + i (a fully recomputed frame), el-byte elems
+void launch_copy_ref_kv(const void* qkv, const int* qoff, int f, int N, int D, int el, void* dst,
+                        hipStream_t s);
 
 // LayerNorm of rows (optionally gathered through idx) into elem rows: dst[r] = LN(src[g(r)])
 void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* Mdev, int Mmax,

@@ -75,6 +75,13 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     const int N = a.N, D = a.D;
     const int chunks = (N + GATE_TOK - 1) / GATE_TOK;
     const int f = blockIdx.x / chunks, ch = blockIdx.x % chunks;
+    if (f < a.skip) {   // carried over from an earlier call: nothing to decide, no rows
+        for (int i = ch * GATE_TOK + (int)threadIdx.x; i < min(N, (ch + 1) * GATE_TOK);
+             i += blockDim.x)
+            if (a.cur) a.cur[(size_t)f * N + i] = 0;
+        if (threadIdx.x == 0 && a.cnt) a.cnt[f * chunks + ch] = 0;
+        return;
+    }
     // the frame's references: star -- the group's first frame (the others play P frames);
     // reordered -- its I/P/B anchors
     int ftype, r, rfut;
@@ -92,7 +99,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     const int nwaves = blockDim.x / WAVE;
     const int nchunk = D / 4;
     __shared__ int wcount[16];
-    uint8_t* om = a.out_masks ? a.out_masks + ((size_t)f * a.L + a.layer) * N : nullptr;
+    uint8_t* om = a.out_masks ? a.out_masks + ((size_t)(f - a.skip) * a.L + a.layer) * N : nullptr;
     const float4* g4 = (const float4*)a.ln_g;
     const float4* b4 = (const float4*)a.ln_b;
     // decision MLP (Section 3.3): lane k holds hidden unit k -- its input weights for s and t,
@@ -157,7 +164,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
         };
         if (ftype != 0 && i != 0) {
             if (a.mode == GATE_INJECT && !REORD) {
-                reuse = a.inj[((size_t)f * a.L + a.layer) * N + i] != 0;
+                reuse = a.inj[((size_t)(f - a.skip) * a.L + a.layer) * N + i] != 0;
             } else if (a.mode == GATE_ALL && !REORD) {
                 reuse = 1;
             } else if (a.mode != GATE_NONE) {
@@ -188,7 +195,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
                         cs = fmaxf(cs, c2);
                     }
                     if (a.mode == GATE_INJECT) {
-                        reuse = a.inj[((size_t)f * a.L + a.layer) * N + i] != 0;
+                        reuse = a.inj[((size_t)(f - a.skip) * a.L + a.layer) * N + i] != 0;
                     } else if (a.mode == GATE_ALL) {
                         reuse = 1;
                     } else if constexpr (DEC) {
@@ -338,13 +345,18 @@ __global__ __launch_bounds__(1024) void scan_k(const int* cnt, int per, int F, i
 // reused token's rank is i minus the recomputed tokens of its frame before i).
 __global__ __launch_bounds__(256) void compact_k(const uint8_t* cur, const int* qoff_in, int F,
                                                  int N, int G, int* idx, int* pos, int* qoff_out,
-                                                 int* ridx) {
+                                                 int* ridx, int skip, int ext_row) {
     const int f = blockIdx.x;
     const int r = (f / G) * G;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (f < skip) {   // carried over from an earlier call: no rows; frame 0's keys/values are the
+                      // cached rows at ext_row (the other carried-over frames are never read)
+        for (int i = tid; i < N; i += 256) pos[(size_t)f * N + i] = ext_row + i;
+        return;
+    }
     __shared__ int wtot[4];
     const int off = cur ? qoff_in[f] : f * N;
-    const int refoff = cur ? qoff_in[r] : r * N;
+    const int refoff = (skip > 0 && r == 0) ? ext_row : cur ? qoff_in[r] : r * N;
     int running = 0;
     for (int base = 0; base < N; base += 256) {
         const int i = base + tid;
@@ -364,7 +376,7 @@ __global__ __launch_bounds__(256) void compact_k(const uint8_t* cur, const int* 
         } else if (valid) {
             pos[(size_t)f * N + i] = refoff + i;
             // rank among reused tokens: those of earlier frames, then the frame's before i
-            if (ridx) ridx[(f * N - off) + i - rank] = f * N + i;
+            if (ridx) ridx[((f - skip) * N - off) + i - rank] = f * N + i;
         }
         running += wtot[0] + wtot[1] + wtot[2] + wtot[3];
     }
@@ -475,6 +487,21 @@ __global__ __launch_bounds__(256) void resolve_k(const uint8_t* __restrict__ cur
     }
 }
 
+// --- keys/values of one fully recomputed frame (its packed rows qoff[f] .. qoff[f] + N - 1) to a
+// dense [N, 2D] copy: the reference carried to the next call of a stream
+__global__ __launch_bounds__(256) void copy_ref_kv_k(const void* qkv, const int* qoff, int f, int N,
+                                                     int D, int el, void* dst) {
+    const size_t per = (size_t)2 * D * el / 16;   // 16-byte pieces of a key/value row
+    const size_t total = (size_t)N * per;
+    const size_t row0 = (size_t)qoff[f];
+    for (size_t t = blockIdx.x * (size_t)blockDim.x + threadIdx.x; t < total;
+         t += (size_t)gridDim.x * blockDim.x) {
+        const size_t i = t / per, c = t % per;
+        const uint4* src = (const uint4*)((const char*)qkv + ((row0 + i) * 3 * D + D) * el);
+        ((uint4*)dst)[t] = src[c];
+    }
+}
+
 __global__ __launch_bounds__(256) void final_ln_k(const float* x, int F, int N, int D,
                                                   const float* g, const float* b, float* emb) {
     const int lane = threadIdx.x & 63;
@@ -557,9 +584,15 @@ void launch_scan(const int* cnt, int per, int F, int tokens, int* qoff, int* M, 
 }
 
 void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,
-                    int* pos, int* qoff_out, int* ridx, hipStream_t s) {
+                    int* pos, int* qoff_out, int* ridx, hipStream_t s, int skip, int ext_row) {
     hipLaunchKernelGGL(compact_k, dim3(F), dim3(256), 0, s, cur, qoff_in, F, N, G, idx, pos,
-                       qoff_out, ridx);
+                       qoff_out, ridx, skip, ext_row);
+}
+
+void launch_copy_ref_kv(const void* qkv, const int* qoff, int f, int N, int D, int el, void* dst,
+                        hipStream_t s) {
+    hipLaunchKernelGGL(copy_ref_kv_k, dim3(grid_for((size_t)N * 2 * D * el / 16, 256)), dim3(256),
+                       0, s, qkv, qoff, f, N, D, el, dst);
 }
 
 void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* Mdev, int Mmax,

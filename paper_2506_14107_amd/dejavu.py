@@ -63,6 +63,9 @@ def load(path=None):
                                             _P, _P, _P, _P, _P]),
         "dv_compact": (ctypes.c_int, [_P, ctypes.c_int, ctypes.c_int, ctypes.c_int, _P, _P, _P,
                                       _P, _P]),
+        "dv_stream_encode": (ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_float,
+                                            _P, _P, _P, _P, _P]),
+        "dv_stream_reset": (ctypes.c_int, [_P]),
         "dv_profile": (ctypes.c_int, [_P, ctypes.c_uint]),
         "dv_profile_read": (ctypes.c_int, [_P, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_longlong)]),
@@ -127,6 +130,16 @@ def dv_encode_tokens(handle, frames, n_frames, group_size, tau, masks, out_embed
                      out_tokens, stream):
     _check(load().dv_encode_tokens(handle, frames, n_frames, group_size, tau, masks,
                                    out_embeddings, out_masks, out_tokens, stream))
+
+
+def dv_stream_encode(handle, frames, n_frames, group_size, tau, masks, out_embeddings, out_masks,
+                     out_tokens, stream):
+    _check(load().dv_stream_encode(handle, frames, n_frames, group_size, tau, masks,
+                                   out_embeddings, out_masks, out_tokens, stream))
+
+
+def dv_stream_reset(handle):
+    _check(load().dv_stream_reset(handle))
 
 
 def dv_compact(masks, n_frames, n_tokens, group_size, idx, pos, qoff, count, stream):
@@ -227,6 +240,20 @@ class Encoder:
             dv_encode_masked(self.handle, _ptr(frames), n, group_size, _ptr(masks_in), _ptr(emb),
                              _ptr(masks), _stream(stream))
         return emb, masks, toks
+
+    def stream_encode(self, frames, group_size, tau=0.0, masks_in=None, want_masks=True,
+                      want_tokens=False, stream=None):
+        """The next frames of a stream (gate mode with tau, or injected masks_in)."""
+        self._check_frames(frames)
+        n = frames.shape[0]
+        emb, masks, toks = self._outs(n, want_masks, want_tokens)
+        dv_stream_encode(self.handle, _ptr(frames), n, group_size, float(tau),
+                         _ptr(masks_in) if masks_in is not None else 0, _ptr(emb), _ptr(masks),
+                         _ptr(toks), _stream(stream))
+        return emb, masks, toks
+
+    def stream_reset(self):
+        dv_stream_reset(self.handle)
 
     def profile(self, stages=True):
         """stages: True (all), False (off), or an iterable of stage names."""

@@ -1,0 +1,134 @@
+"""Streaming (dv_stream_encode): frames arrive in calls of any size and a group may span calls;
+the reference of an open group is carried between calls in the handle's cache.  The stream's
+outputs must equal, bit for bit, one encode over all frames (whose parity with the CPU oracle
+the other tests establish), in every mode; one group spanning calls is also checked against
+the oracle directly."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth.configs import ModelConfig
+
+from .gpu_util import check_close, dev, encoder, host, mask_parity, require_gpu
+from .test_gpu_parity import _video
+
+pytestmark = pytest.mark.gpu
+
+TINY = synth.get_config("tiny")
+SMALL = ModelConfig(64, 16, 2, 128, 2, 256, "bf16")
+MID = ModelConfig(112, 16, 3, 256, 4, 512, "bf16")
+MID_R = dataclasses.replace(MID, restore=True)
+MID_D = dataclasses.replace(MID, decision=True)
+
+
+def _frames(m, F, seed):
+    if m.dtype == "f32":
+        return synth.render_frames(TINY.video, m.image_size, 0, F)
+    return _video(m, F, seed=seed, sigma=0.02, pan=1.0)
+
+
+def _one_shot(m, blob, fr, G, tau, masks, batch):
+    torch = require_gpu()
+    enc = encoder(m, blob, batch)
+    if masks is None:
+        out = enc.encode(dev(fr), G, tau, want_tokens=True)
+    else:
+        out = enc.encode_masked(dev(fr), G, dev(masks), want_tokens=True)
+    torch.cuda.synchronize()
+    return [host(o) for o in out]
+
+
+def _streamed(m, blob, fr, G, tau, masks, batch, chunks):
+    torch = require_gpu()
+    enc = encoder(m, blob, batch)
+    outs, k = [], 0
+    for c in chunks:
+        mk = dev(masks[k:k + c]) if masks is not None else None
+        outs.append(enc.stream_encode(dev(fr[k:k + c]), G, tau, masks_in=mk, want_tokens=True))
+        k += c
+    torch.cuda.synchronize()
+    assert k == fr.shape[0]
+    return [np.concatenate([host(o[j]) for o in outs]) for j in range(3)]
+
+
+CASES = [
+    # model, group, frames, internal batch, call sizes, tau (None: injected masks)
+    ("tiny", TINY.model, 4, 14, 8, [3, 5, 1, 5], 0.95),
+    ("small", SMALL, 8, 30, 8, [3, 5, 1, 8, 13], 0.9),
+    ("small-inf", SMALL, 8, 20, 16, [6, 7, 7], float("inf")),
+    ("small-dense", SMALL, 8, 20, 16, [6, 7, 7], float("-inf")),
+    ("mid-injected", MID, 4, 22, 8, [5, 2, 9, 6], None),
+    ("mid-restore", MID_R, 8, 26, 16, [11, 4, 11], 0.9),
+    ("mid-decision", MID_D, 8, 26, 16, [11, 4, 11], 0.0),
+]
+
+
+@pytest.mark.parametrize("name,m,G,F,batch,chunks,tau", CASES, ids=[c[0] for c in CASES])
+def test_stream_equals_one_shot_bitwise(name, m, G, F, batch, chunks, tau):
+    blob = synth.make_blob(m, 61, perturb_ln=True)
+    fr = _frames(m, F, 61)
+    masks = None
+    if tau is None:
+        masks = (np.random.default_rng(62).random((F, m.depth, m.n_tokens)) < 0.6).astype(np.uint8)
+        tau = 0.0
+    tau = float(np.float32(tau))
+    want = _one_shot(m, blob, fr, G, tau, masks, batch)
+    got = _streamed(m, blob, fr, G, tau, masks, batch, chunks)
+    if np.isfinite(tau) or masks is not None:
+        assert 0.05 < oracle.reuse_rate(want[1], G) < 0.99, "want a mixed map"
+    for a, b, what in zip(got, want, ("embeddings", "masks", "tokens")):
+        assert np.array_equal(a, b), f"{what} differ from one encode over all frames"
+
+
+def test_stream_one_frame_per_call_against_oracle():
+    """Groups of 8 delivered one frame per call: every non-reference frame finds its reference
+    in the cache; the group spanning calls 5..12 is checked against the oracle replaying the
+    GPU's map."""
+    torch = require_gpu()
+    m = SMALL
+    blob = synth.make_blob(m, 63)
+    G, F = 8, 20
+    fr = _frames(m, F, 63)
+    tau = float(np.float32(0.9))
+    emb, mk, toks = _streamed(m, blob, fr, G, tau, None, 8, [1] * F)
+    want = _one_shot(m, blob, fr, G, tau, None, 8)
+    for a, b in zip((emb, mk, toks), want):
+        assert np.array_equal(a, b)
+    sl = slice(8, 16)
+    r = oracle.encode(fr[sl], blob, m.as_dict(), G, masks=mk[sl])
+    bad, _ = mask_parity(mk[sl], r["cos"], tau)
+    assert bad == 0
+    check_close(emb[sl], r["emb"], "bf16", "embeddings")
+    check_close(toks[sl], r["tokens"], "bf16", "tokens")
+    torch.cuda.synchronize()
+
+
+def test_stream_group_size_and_reset():
+    from paper_2506_14107_amd import dejavu as dj
+    require_gpu()
+    m = SMALL
+    blob = synth.make_blob(m, 64)
+    fr = _frames(m, 12, 64)
+    enc = encoder(m, blob, 8)
+    enc.stream_encode(dev(fr[:5]), 4, 0.9)
+    with pytest.raises(dj.DejaVuError) as e:
+        enc.stream_encode(dev(fr[5:9]), 8, 0.9)
+    assert e.value.code == dj.DV_EINVAL and "group_size" in dj.dv_last_error()
+    enc.stream_reset()
+    a = enc.stream_encode(dev(fr[:7]), 8, 0.9)[0]
+    b = enc.stream_encode(dev(fr[7:12]), 8, 0.9)[0]
+    want = _one_shot(m, blob, fr, 8, float(np.float32(0.9)), None, 8)[0]
+    assert np.array_equal(np.concatenate([host(a), host(b)]), want)
+
+
+def test_stream_with_reordering_is_rejected():
+    from paper_2506_14107_amd import dejavu as dj
+    require_gpu()
+    m = dataclasses.replace(SMALL, reorder=True)
+    enc = encoder(m, synth.make_blob(m, 65), 8)
+    with pytest.raises(dj.DejaVuError) as e:
+        enc.stream_encode(dev(_frames(m, 4, 65)), 4, 0.9)
+    assert e.value.code == dj.DV_EUNSUPPORTED
