@@ -18,8 +18,9 @@
 //      computed for the next layer]
 //     [reordered referencing: the gate compares each token with the frame's past and future
 //      anchors and records which one supplies it; after the compaction every reused token's
-//      key/value row is resolved along those sources to the frame that recomputes it; after
-//      FC2 every reused row is copied from that frame's new row.  An internal batch also
+//      key/value row is resolved along those sources to the frame that recomputes it (its
+//      root); a reused token's row stays that frame's new row, read through the root map by the
+//      next layer's gate, and is filled in only to hand out tokens.  An internal batch also
 //      carries the next batch's first frame (an I frame, the future anchor of its last block).]
 //   [stream (dv_stream_encode): a group may span calls.  The reference of a group that is still
 //    open when a call ends keeps its per-layer input rows and keys/values in a cache; the next
@@ -341,6 +342,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             ga.H = d.H;
             ga.reorder = reord;
             ga.src = reord ? h->srcmap : nullptr;
+            ga.root = (reord && l > 0) ? h->root : nullptr;
             ga.skip = skip;
             launch_gate(bf, ga, s);
         }
@@ -476,9 +478,13 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             r.N = N;
             r.G = G;
             launch_gemm(Epi::Restore, bf, r, s);
-        } else if (reord) {   // reused rows: the new row of the frame that recomputed them
-            Scope sc(h, DV_STAGE_MERGE, s);
-            launch_merge(h->x, cur, h->root, F, N, D, G, s);
+        } else if (reord) {
+            // reused rows stay aliases of the frame that recomputed them (the root map); they
+            // are filled in only to hand out the tokens
+            if (tokens && l == L - 1) {
+                Scope sc(h, DV_STAGE_MERGE, s);
+                launch_merge(h->x, cur, h->root, F, N, D, G, s);
+            }
         } else if (mode == GATE_INJECT || mode == GATE_ALL ||
                    (mode == GATE_COS && tokens && l == L - 1)) {
             // reused rows take the reference's new row (gate mode: only to hand out tokens)

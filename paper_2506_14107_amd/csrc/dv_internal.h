@@ -143,6 +143,8 @@ struct GateArgs {
     int H;
     int reorder;          // reordered referencing (reorder_refs) instead of the star
     uint8_t* src;         // [F*N] reordered: 1 where the future reference supplies the token
+    const int* root;      // [F*N] reordered: the previous layer's root map (nullptr: every token
+                          // holds its own row); a recomputed token gets its root's row copied in
     int skip;             // leading frames carried over from an earlier call of a stream: frame 0
                           // is the cached reference (its rows already in x), the others gaps;
                           // none is gated, and inj / out_masks start at frame skip
@@ -180,7 +182,7 @@ void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* M
 void launch_merge(float* x, const uint8_t* cur, const int* root, int F, int N, int D, int G,
                   hipStream_t s);
 // Reordered referencing: for every reused token, follow the sources (src, reorder_refs) to the
-// frame r that recomputes it; pos[f*N+i] = pos[r*N+i], root[f*N+i] = r.
+// frame r that recomputes it; pos[f*N+i] = pos[r*N+i], root[f*N+i] = r (f for recomputed ones).
 void launch_resolve(const uint8_t* cur, const uint8_t* src, int F, int N, int G, int* pos,
                     int* root, hipStream_t s);
 // emb[f] = LN(x[f*N]) (class token)

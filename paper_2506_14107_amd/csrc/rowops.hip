@@ -134,6 +134,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     for (int i = ch * GATE_TOK + wave; i < i_end; i += nwaves) {
         const size_t row = (size_t)f * N + i;
         float4* xf = (float4*)(a.x + row * D);
+        const float4* xo = xf;   // the token's current row (reordered: through its root)
         int reuse = 0, from_fut = 0;
         bool loaded = false;
         float4 v[MAX_CHUNKS];
@@ -145,7 +146,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
             for (int k = 0; k < MAX_CHUNKS; ++k) {
                 const int c = lane + k * WAVE;
                 if (c < nchunk) {
-                    if (!loaded) v[k] = xf[c];
+                    if (!loaded) v[k] = xo[c];
                     const float4 u = v[k], w = xr[c];
                     dot += u.x * w.x + u.y * w.y + u.z * w.z + u.w * w.w;
                     na += u.x * u.x + u.y * u.y + u.z * u.z + u.w * u.w;
@@ -188,9 +189,22 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
                         reuse = a.tau <= 1.0f;
                     }
                 } else {
-                    float cs = cosine((const float4*)(a.x + ((size_t)r * N + i) * D));
+                    // reordered: rows are read through the previous layer's roots (a token reused
+                    // there is the row of the frame that recomputed it); one root, one row, and
+                    // a cosine of exactly 1 without reading it
+                    int own = f, rp = r, rq = rfut;
+                    if (REORD && a.root) {
+                        own = a.root[row];
+                        rp = a.root[(size_t)r * N + i];
+                        if (rfut >= 0) rq = a.root[(size_t)rfut * N + i];
+                        xo = (const float4*)(a.x + ((size_t)own * N + i) * D);
+                    }
+                    float cs = own == rp ? 1.0f
+                                         : cosine((const float4*)(a.x + ((size_t)rp * N + i) * D));
                     if (REORD && rfut >= 0) {   // the better of the two references
-                        const float c2 = cosine((const float4*)(a.x + ((size_t)rfut * N + i) * D));
+                        const float c2 =
+                            own == rq ? 1.0f
+                                      : cosine((const float4*)(a.x + ((size_t)rq * N + i) * D));
                         from_fut = c2 > cs;
                         cs = fmaxf(cs, c2);
                     }
@@ -202,6 +216,17 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
                         reuse = decision(cs, i) > a.tau;
                     } else {
                         reuse = cs >= a.tau;
+                    }
+                    if (REORD && !reuse && own != f) {   // recomputed after being reused: the
+#pragma unroll                                           // token gets its root's row back
+                        for (int k = 0; k < MAX_CHUNKS; ++k) {
+                            const int c = lane + k * WAVE;
+                            if (c < nchunk) {
+                                if (!loaded) v[k] = xo[c];
+                                xf[c] = v[k];
+                            }
+                        }
+                        loaded = true;
                     }
                 }
             }
@@ -230,7 +255,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
 #pragma unroll
                 for (int k = 0; k < MAX_CHUNKS; ++k) {
                     const int c = lane + k * WAVE;
-                    if (c < nchunk) v[k] = xf[c];
+                    if (c < nchunk) v[k] = xo[c];
                 }
             }
             float sum = 0.f;
@@ -468,12 +493,16 @@ __global__ __launch_bounds__(256) void merge_k(float* x, const uint8_t* cur, con
 // reused in turn; the chain ends at a frame that recomputes the token (I frames recompute every
 // token, and every step moves to an earlier frame of the processing order, so a chain is at
 // most a few frames long).  pos of recomputed tokens is already set; reused ones copy it.
+// root: for every token, the frame whose row after this layer is the token's next row.
 __global__ __launch_bounds__(256) void resolve_k(const uint8_t* __restrict__ cur,
                                                  const uint8_t* __restrict__ src, int F, int N,
                                                  int G, int* pos, int* root) {
     const int total = F * N;
     for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += gridDim.x * blockDim.x) {
-        if (!cur[t]) continue;
+        if (!cur[t]) {   // recomputed: its own frame holds its next row
+            root[t] = t / N;
+            continue;
+        }
         const int i = t % N;
         int r = t / N;
         for (int hop = 0; hop < 64 && cur[(size_t)r * N + i]; ++hop) {
