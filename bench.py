@@ -249,7 +249,7 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2506_14107_amd.dejavu import Encoder
+    from paper_2506_14107_amd.dejavu import Encoder, dv_workspace_bytes
 
     w = synth.get_config(args.workload)
     m = w.model
@@ -284,13 +284,18 @@ def main():
         rhos.append(rho)
         log(f"[bench] target reuse {tgt}: tau {tau:.6f} -> reuse {rho}")
 
-    # per-level reuse maps and active rows (deterministic: same as in the timed region)
+    # per-level reuse maps and active rows (deterministic: same as in the timed region), and the
+    # embeddings' cosine to those of the same kernels with reuse off (the paper's accuracy proxy)
+    e_dense, _, _ = enc.encode(x, G, float("-inf"), want_masks=False)
     levels = []
     for tau in taus:
-        _, mk, _ = enc.encode(x, G, tau)
+        e, mk, _ = enc.encode(x, G, tau)
         torch.cuda.synchronize()
         mk = mk.cpu().numpy()
-        levels.append({"tau": tau, "reuse": reuse_of(mk, G), "Ml": active_rows(mk, G)})
+        cos = torch.nn.functional.cosine_similarity(e.double(), e_dense.double(), dim=1)
+        cos = cos.cpu().numpy()[[f for f in range(F) if f % G]]
+        levels.append({"tau": tau, "reuse": reuse_of(mk, G), "Ml": active_rows(mk, G),
+                       "cos": (float(cos.mean()), float(cos.min()))})
 
     # the dominant stage: one profiled pass over every level (stage times also logged per level)
     prof = {}
@@ -379,7 +384,9 @@ def main():
         dense = patch + per_row * F * N * m.depth
         sweep.append({"tau": lv["tau"], "reuse": round(lv["reuse"], 4),
                       "frames_per_s": round(fps, 1), "speedup_vs_dense": round(fps / dense_fps, 3),
-                      "ideal_speedup": round(dense / algo, 3)})
+                      "ideal_speedup": round(dense / algo, 3),
+                      "emb_cos_vs_dense_mean": round(lv["cos"][0], 5),
+                      "emb_cos_vs_dense_min": round(lv["cos"][1], 5)})
 
     if args.copy_calibration:   # one plain copy kernel of known size for the HBM counters
         src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
@@ -427,6 +434,7 @@ def main():
         "roofline": roof,
         "stages": stages,
         "cpu_baseline": cpu,
+        "workspace_bytes": dv_workspace_bytes(enc.handle),
     }
     print(json.dumps(out), flush=True)
 

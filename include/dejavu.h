@@ -144,7 +144,9 @@ size_t dv_weights_floats(const dv_config* cfg);
  * rounds the matrices to bf16 (nearest, ties to even) when dtype is
  * DV_BF16, and allocates the workspace for max_batch_frames frames.
  * Synchronous.  Errors: DV_EINVAL (null pointer, wrong blob size, sizes < 1),
- * DV_EUNSUPPORTED (S % p, D % H, head dim, unknown flag bits), DV_ENOMEM, DV_EHIP.
+ * DV_EUNSUPPORTED (S % p, D % H, head dim, unknown flag bits), DV_ENOMEM (an allocation
+ * failed, or the weights and workspace exceed the environment variable DV_MAX_DEVICE_BYTES when
+ * it is set -- checked before any device call), DV_EHIP.
  * On error *out is set to NULL. */
 int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, dv_handle** out);
 

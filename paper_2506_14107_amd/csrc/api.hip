@@ -41,6 +41,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -149,6 +150,40 @@ size_t blob_floats(const Dims& d) {
     const size_t restore = d.restore ? (size_t)d.L * (2 * RH * D + RH + D) : 0;
     const size_t decision = d.decision ? (size_t)d.L * DEC_FLOATS : 0;
     return D * 3 * p * p + D + D + N * D + (size_t)d.L * per_layer + 2 * D + restore + decision;
+}
+
+// Bytes of workspace a handle of these dimensions allocates (the order of dv_create's carving).
+size_t workspace_need(const Dims& d) {
+    const size_t N = d.N, D = d.D, Dm = d.Dm, el = d.bf16 ? 2 : 4;
+    const size_t T = (size_t)d.Bw * N, Tp = round_up(T, ROW_PAD);
+    const size_t Awide = std::max((size_t)D, (size_t)d.Kp);
+    size_t need = 0;
+    auto sz = [&](size_t bytes) { need += round_up(bytes, 256); };
+    sz(T * D * 4);        // x
+    sz(Tp * Awide * el);  // A
+    sz((Tp + round_up(N, ROW_PAD)) * 3 * D * el);  // qkv (+ a stream's cached reference rows)
+    sz(Tp * D * el);      // O
+    sz(Tp * D * 4);       // Z
+    sz(Tp * Dm * el);     // H
+    sz(T);
+    sz(T);                // masks
+    for (int i = 0; i < 2; ++i) {
+        sz(T * 4);
+        sz(T * 4);
+        sz((d.Bw + 1) * 4);
+    }
+    sz((size_t)d.Bw * gate_chunks(d.N) * 4);
+    sz(4 * 4);
+    if (d.restore) {
+        sz(T * 4);             // ridx
+        sz(Tp * RH * el);      // Hr
+    }
+    if (d.decision) sz(T * d.H * 4);   // tcls
+    if (d.reorder) {
+        sz(T);       // srcmap
+        sz(T * 4);   // root
+    }
+    return need;
 }
 
 struct Stage {
@@ -676,6 +711,14 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     }
     std::vector<size_t> dco(d.decision ? L : 0);
     for (auto& o : dco) o = reserve(DEC_FLOATS * 4);
+    // an optional cap on the device memory a handle may take (weights and workspace), checked
+    // before any device call: DV_MAX_DEVICE_BYTES in the environment
+    if (const char* cap = getenv("DV_MAX_DEVICE_BYTES")) {
+        const unsigned long long c = strtoull(cap, nullptr, 10);
+        if (wbytes + workspace_need(d) > c)
+            return fail(DV_ENOMEM, "the handle needs %zu bytes of device memory, above "
+                        "DV_MAX_DEVICE_BYTES=%llu", wbytes + workspace_need(d), c);
+    }
     try {
         host.assign(wbytes, 0);
     } catch (const std::bad_alloc&) {
@@ -782,32 +825,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     // --- workspace ----------------------------------------------------------------------------
     const size_t T = (size_t)d.Bw * N, Tp = round_up(T, ROW_PAD);
     const size_t Awide = std::max((size_t)D, (size_t)d.Kp);
-    size_t need = 0;
-    auto sz = [&](size_t bytes) { need += round_up(bytes, 256); };
-    sz(T * D * 4);        // x
-    sz(Tp * Awide * el);  // A
-    sz((Tp + round_up(N, ROW_PAD)) * 3 * D * el);  // qkv (+ a stream's cached reference rows)
-    sz(Tp * D * el);      // O
-    sz(Tp * D * 4);       // Z
-    sz(Tp * Dm * el);     // H
-    sz(T);
-    sz(T);                // masks
-    for (int i = 0; i < 2; ++i) {
-        sz(T * 4);
-        sz(T * 4);
-        sz((d.Bw + 1) * 4);
-    }
-    sz((size_t)d.Bw * gate_chunks(d.N) * 4);
-    sz(4 * 4);
-    if (d.restore) {
-        sz(T * 4);             // ridx
-        sz(Tp * RH * el);      // Hr
-    }
-    if (d.decision) sz(T * d.H * 4);   // tcls
-    if (d.reorder) {
-        sz(T);       // srcmap
-        sz(T * 4);   // root
-    }
+    const size_t need = workspace_need(d);
     {
         hipError_t e = hipMalloc(&h->ws, need);
         if (e != hipSuccess) {

@@ -134,3 +134,15 @@ def test_profile_calls_reject_null_handle():
     assert lib.dv_profile_read(None, 0, ctypes.byref(ms), ctypes.byref(n)) == dj.DV_EINVAL
     size = ctypes.c_size_t()
     assert lib.dv_workspace_bytes(None, ctypes.byref(size)) == dj.DV_EINVAL
+
+
+def test_create_reports_enomem_above_the_device_memory_cap(monkeypatch):
+    """DV_MAX_DEVICE_BYTES caps a handle's device memory; the check precedes any device call, so
+    it runs here without a GPU."""
+    import synth
+    m = synth.get_config("tiny").model
+    blob = synth.make_blob(m, 1)
+    monkeypatch.setenv("DV_MAX_DEVICE_BYTES", "1000")
+    with pytest.raises(dj.DejaVuError) as e:
+        dj.dv_create(_cfg(), blob)
+    assert e.value.code == dj.DV_ENOMEM and "DV_MAX_DEVICE_BYTES" in dj.dv_last_error()
