@@ -67,8 +67,9 @@ def _frames(m, F, seed):
 
 @pytest.mark.parametrize("m,G,F,batch", [(TINY_O, 4, 8, 8), (SMALL_O, 8, 16, 16),
                                          (MID_O, 8, 21, 8), (N257_O, 8, 16, 16),
-                                         (DH80_O, 4, 10, 8)],
-                         ids=["tiny", "small", "mid-batched", "n257", "dh80-batched"])
+                                         (DH80_O, 4, 10, 8), (SMALL_O, 12, 30, 16)],
+                         ids=["tiny", "small", "mid-batched", "n257", "dh80-batched",
+                              "p-chain-g12"])
 def test_reorder_gate_parity(m, G, F, batch):
     blob = synth.make_blob(m, 51, perturb_ln=True)
     fr = _frames(m, F, 51)
