@@ -119,8 +119,10 @@ typedef struct dv_config {
  * similarity is the larger of its two cosines; when reused, its keys, values and layer output
  * come from the reference that gave it (the past one on a tie).  The decision MLP's type cue is
  * the frame's own type.  Frame indices are those of the call; internal batches also compute
- * the next batch's first frame, so batching does not change results.  Not combinable with
- * DV_FLAG_RESTORE (DV_EUNSUPPORTED).  No extra weights. */
+ * the next batch's first frame, so batching does not change results.  With DV_FLAG_RESTORE a
+ * reused token's new row is its source token's new row plus its own restoration output (of its
+ * input's difference to the source's input); the group size is then at most 60 (chains of
+ * sources up to 16 long).  No extra weights. */
 #define DV_FLAG_REORDER 4u
 
 typedef struct dv_handle dv_handle;
@@ -175,7 +177,7 @@ int dv_workspace_bytes(const dv_handle* h, size_t* bytes);
  * Enqueued on `stream`, asynchronous, no host synchronisation.
  * Errors: DV_EINVAL (null handle/frames/embeddings, n_frames < 1,
  * group_size < 1 or > max_batch_frames, NaN tau, group_size not a multiple of 4 with
- * DV_FLAG_REORDER), DV_EHIP. */
+ * DV_FLAG_REORDER, or above 60 with DV_FLAG_REORDER and DV_FLAG_RESTORE), DV_EHIP. */
 int dv_encode(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
               float* out_embeddings, uint8_t* out_masks, hipStream_t stream);
 

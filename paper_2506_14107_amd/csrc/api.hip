@@ -106,9 +106,6 @@ int check_config(const dv_config* c, Dims* d) {
     if (c->dtype != DV_F32 && c->dtype != DV_BF16) return fail(DV_EINVAL, "unknown dtype %d", c->dtype);
     if (c->flags & ~(DV_FLAG_RESTORE | DV_FLAG_DECISION | DV_FLAG_REORDER))
         return fail(DV_EUNSUPPORTED, "unknown flag bits 0x%x", c->flags);
-    if ((c->flags & DV_FLAG_RESTORE) && (c->flags & DV_FLAG_REORDER))
-        return fail(DV_EUNSUPPORTED, "the restoration layer is not supported with reordered "
-                    "referencing");
     if (c->image_size % c->patch) return fail(DV_EUNSUPPORTED, "image_size %% patch != 0");
     if (c->width % c->heads) return fail(DV_EUNSUPPORTED, "width %% heads != 0");
     const int dh = c->width / c->heads;
@@ -183,6 +180,10 @@ size_t workspace_need(const Dims& d) {
         sz(T);       // srcmap
         sz(T * 4);   // root
     }
+    if (d.reorder && d.restore) {
+        sz(T * 4);         // rslot
+        sz(Tp * D * 4);    // rbuf: restoration outputs of reused tokens
+    }
     return need;
 }
 
@@ -214,6 +215,8 @@ struct dv_handle {
     uint8_t* mask[2]; // [T] per-layer maps (ping-pong)
     int *idx, *pos_, *qoff, *cnt, *M;   // M[0]: recomputed rows, M[1]: reused tokens
     int* ridx = nullptr;   // [T] reused tokens (restoration)
+    int* rslot = nullptr;  // [T] reordered restoration: a reused token's slot in ridx
+    float* rbuf = nullptr; // [Tp, D] reordered restoration: restoration outputs, in ridx order
     float* tcls = nullptr; // [B, H, N] class-token attention weights of the last layer, per head
                            // (decision MLP)
     uint8_t* srcmap = nullptr;   // [T] reordered: 1 where the future anchor supplies the token
@@ -377,7 +380,8 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             ga.H = d.H;
             ga.reorder = reord;
             ga.src = reord ? h->srcmap : nullptr;
-            ga.root = (reord && l > 0) ? h->root : nullptr;
+            // restored rows are written out every layer; otherwise reused rows alias their root
+            ga.root = (reord && !restore && l > 0) ? h->root : nullptr;
             ga.skip = skip;
             launch_gate(bf, ga, s);
         }
@@ -385,7 +389,8 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             Scope sc(h, DV_STAGE_COMPACT, s);
             launch_scan(h->cnt, gate_chunks(N), F, restore ? (F - skip) * N : 0, h->qoff, h->M, s);
             launch_compact(cur, h->qoff, F, N, G, h->idx, h->pos_, nullptr,
-                           restore ? h->ridx : nullptr, s, skip, h->ext_row);
+                           restore ? h->ridx : nullptr, s, skip, h->ext_row,
+                           restore && reord ? h->rslot : nullptr);
             if (reord) launch_resolve(cur, h->srcmap, F, N, G, h->pos_, h->root, s);
         }
         if (restore) {   // restoration hidden rows: GELU(dx W_r1^T + b_r1), before LN2 reuses A
@@ -495,7 +500,23 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         if (fill >= 0 && l == L - 1)
             HIP_TRY(hipMemcpyAsync(h->xc + (size_t)L * N * D, h->x + (size_t)fill * N * D,
                                    row_bytes, hipMemcpyDeviceToDevice, s));
-        if (restore) {   // reused rows: the reference token's new row + Hr W_r2^T + b_r2
+        if (restore && reord) {   // restoration outputs, then each reused row along its chain
+            Scope sc(h, DV_STAGE_RESTORE, s);
+            GemmArgs r{};
+            r.A = h->Hr;
+            r.W = w.W_r2;
+            r.bias = w.b_r2;
+            r.K = RH;
+            r.Nout = D;
+            r.Mdev = h->M + 1;
+            r.Mconst = T;
+            r.Mmax = T;
+            r.cus = h->cus;
+            r.out = h->rbuf;
+            launch_gemm(Epi::Delta, bf, r, s);
+            launch_restore_chain(h->x, h->rbuf, h->ridx, h->rslot, cur, h->srcmap, h->M + 1, T, F,
+                                 N, D, G, s);
+        } else if (restore) {   // reused rows: the reference token's new row + Hr W_r2^T + b_r2
             Scope sc(h, DV_STAGE_RESTORE, s);
             GemmArgs r{};
             r.A = h->Hr;
@@ -555,6 +576,9 @@ int encode_impl(dv_handle* h, const float* frames, int n, int G, float tau, cons
     if (d.reorder && G % 4)
         return fail(DV_EINVAL, "reordered referencing needs a group_size that is a multiple of 4 "
                     "(got %d)", G);
+    if (d.reorder && d.restore && G / 4 + 1 > CHAIN_MAX)
+        return fail(DV_EINVAL, "reordered referencing with restoration supports group_size <= %d "
+                    "(got %d)", 4 * (CHAIN_MAX - 1), G);
     const int per = (d.B / G) * G;
     const size_t img = (size_t)3 * d.S * d.S;
     HIP_TRY(hipSetDevice(h->device));
@@ -864,6 +888,10 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
     if (d.reorder) {
         h->srcmap = carve<uint8_t>(p, T);
         h->root = carve<int>(p, T);
+    }
+    if (d.reorder && d.restore) {
+        h->rslot = carve<int>(p, T);
+        h->rbuf = carve<float>(p, Tp * D);
     }
     *out = h;
     return DV_OK;

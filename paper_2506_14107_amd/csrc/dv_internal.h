@@ -56,6 +56,7 @@ enum class Epi : int {
     Fc2 = 4,    // x[idx[r], c] = acc + bias[c] + z[r, c]                              (fp32 out)
     Restore = 5,  // x[t, c] = acc + bias[c] + x[ref(t), c], t = idx[r]: a reused token's row
                   // from its reference token's new row (ref(t): same token of frame G*floor(f/G))
+    Delta = 6,    // out[r, c] = acc + bias[c]                                        (fp32 out)
 };
 
 struct GemmArgs {
@@ -149,6 +150,10 @@ struct GateArgs {
                           // is the cached reference (its rows already in x), the others gaps;
                           // none is gated, and inj / out_masks start at frame skip
 };
+// Reordering with restoration: a reused row is built along its chain of sources; a group of G
+// frames has chains of at most G/4 + 1 reused links (B_dist1, B_dist2, then the P frames back
+// to the I frame), so G <= 4 * (CHAIN_MAX - 1).
+constexpr int CHAIN_MAX = 16;
 constexpr int DEC_HIDDEN = 64;   // decision MLP hidden units: one per lane of a wavefront
 constexpr int DEC_FEAT = 6;      // its features: s, t, one-hot type (I, P, B_dist2, B_dist1)
 constexpr int DEC_FLOATS = DEC_HIDDEN * DEC_FEAT + 2 * DEC_HIDDEN + 1;
@@ -167,9 +172,10 @@ void launch_scan(const int* cnt, int per, int F, int tokens, int* qoff, int* M, 
 // slot (f*N - qoff[f]) + (reused tokens of frame f before i)
 // skip > 0 (stream): frames below skip have no rows; frame 0 is the cached reference, whose keys
 // and values sit at packed rows ext_row .. ext_row + N - 1 (pos of its reused tokens points there)
+// rslot (or nullptr): for every reused token, its slot in ridx
 void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,
                     int* pos, int* qoff_out, int* ridx, hipStream_t s, int skip = 0,
-                    int ext_row = 0);
+                    int ext_row = 0, int* rslot = nullptr);
 // dst[i, 0:2D] = K|V of frame f's packed row qoff[f] + i (a fully recomputed frame), el-byte elems
 void launch_copy_ref_kv(const void* qkv, const int* qoff, int f, int N, int D, int el, void* dst,
                         hipStream_t s);
@@ -181,6 +187,13 @@ void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* M
 // the group's first frame)
 void launch_merge(float* x, const uint8_t* cur, const int* root, int F, int N, int D, int G,
                   hipStream_t s);
+// Reordered referencing with the restoration layer: every reused token's new row, built along its
+// chain of sources from the root's new row: x[t] = ((x[root] + d[link_1]) + ...) + d[t], where
+// d[u] = rbuf[rslot[u]] is token u's restoration output and the links run from the root outward.
+// Mdev: the number of reused tokens (rows of ridx).
+void launch_restore_chain(float* x, const float* rbuf, const int* ridx, const int* rslot,
+                          const uint8_t* cur, const uint8_t* src, const int* Mdev, int Mmax, int F,
+                          int N, int D, int G, hipStream_t s);
 // Reordered referencing: for every reused token, follow the sources (src, reorder_refs) to the
 // frame r that recomputes it; pos[f*N+i] = pos[r*N+i], root[f*N+i] = r (f for recomputed ones).
 void launch_resolve(const uint8_t* cur, const uint8_t* src, int F, int N, int G, int* pos,

@@ -86,6 +86,8 @@ __device__ inline void epi_store(const GemmArgs& a, int row, int col, float acc)
     } else if constexpr (E == Epi::Fc2) {
         v += a.resid[(size_t)row * a.Nout + col];
         ((float*)a.out)[(size_t)a.idx[row] * a.Nout + col] = v;
+    } else if constexpr (E == Epi::Delta) {
+        ((float*)a.out)[(size_t)row * a.Nout + col] = v;
     } else {  // Restore: a reused token's row from its reference token's new row
         const int t = a.idx[row], f = t / a.N;
         const int rt = (f / a.G * a.G) * a.N + t % a.N;
@@ -203,6 +205,8 @@ __device__ inline void epilogue_lds(const GemmArgs& a, f32x16 (&acc)[TI][TJ], fl
             } else if constexpr (E == Epi::Fc1) {
                 const f32x4 gl = {gelu_poly(v[0]), gelu_poly(v[1]), gelu_poly(v[2]), gelu_poly(v[3])};
                 __builtin_amdgcn_raw_buffer_store_b64(pack_bf16x4(gl), rout, off, 0, 0);
+            } else if constexpr (E == Epi::Delta) {
+                __builtin_amdgcn_raw_buffer_store_b128(v, rout, off, 0, 0);
             } else {
                 __builtin_amdgcn_raw_buffer_store_b128(v + extra[i & 1][q], rout, off, 0, 0);
             }
@@ -609,6 +613,7 @@ void launch_gemm(Epi e, bool bf16, const GemmArgs& a, hipStream_t s) {
         case Epi::Fc1: launch_one<Epi::Fc1>(bf16, a, s); break;
         case Epi::Fc2: launch_one<Epi::Fc2>(bf16, a, s); break;
         case Epi::Restore: launch_one<Epi::Restore>(bf16, a, s); break;
+        case Epi::Delta: launch_one<Epi::Delta>(bf16, a, s); break;
     }
 }
 

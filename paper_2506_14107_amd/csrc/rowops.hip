@@ -232,7 +232,8 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
             }
         }
         if (reuse && a.d_out) {   // reused (restoration): x_f - x_ref into the token-indexed buffer
-            const float4* xr = (const float4*)(a.x + ((size_t)r * N + i) * D);
+            const int rs = from_fut ? rfut : r;   // the reference that supplies the token
+            const float4* xr = (const float4*)(a.x + ((size_t)rs * N + i) * D);
 #pragma unroll
             for (int k = 0; k < MAX_CHUNKS; ++k) {
                 const int c = lane + k * WAVE;
@@ -370,7 +371,7 @@ __global__ __launch_bounds__(1024) void scan_k(const int* cnt, int per, int F, i
 // reused token's rank is i minus the recomputed tokens of its frame before i).
 __global__ __launch_bounds__(256) void compact_k(const uint8_t* cur, const int* qoff_in, int F,
                                                  int N, int G, int* idx, int* pos, int* qoff_out,
-                                                 int* ridx, int skip, int ext_row) {
+                                                 int* ridx, int skip, int ext_row, int* rslot) {
     const int f = blockIdx.x;
     const int r = (f / G) * G;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -401,7 +402,9 @@ __global__ __launch_bounds__(256) void compact_k(const uint8_t* cur, const int* 
         } else if (valid) {
             pos[(size_t)f * N + i] = refoff + i;
             // rank among reused tokens: those of earlier frames, then the frame's before i
-            if (ridx) ridx[((f - skip) * N - off) + i - rank] = f * N + i;
+            const int slot = ((f - skip) * N - off) + i - rank;
+            if (ridx) ridx[slot] = f * N + i;
+            if (rslot) rslot[(size_t)f * N + i] = slot;
         }
         running += wtot[0] + wtot[1] + wtot[2] + wtot[3];
     }
@@ -531,6 +534,48 @@ __global__ __launch_bounds__(256) void copy_ref_kv_k(const void* qkv, const int*
     }
 }
 
+// --- reordered referencing with the restoration layer: one wavefront per reused token --------
+// Its new row is its source token's new row plus its own restoration output; the source may be
+// reused in turn, so the row is built from the chain's root (a frame recomputing the token, whose
+// new row FC2 wrote) outward, adding each link's restoration output, the token's own last.
+__global__ __launch_bounds__(256) void restore_chain_k(float* x, const float* __restrict__ rbuf,
+                                                       const int* __restrict__ ridx,
+                                                       const int* __restrict__ rslot,
+                                                       const uint8_t* __restrict__ cur,
+                                                       const uint8_t* __restrict__ src,
+                                                       const int* Mdev, int F, int N, int D,
+                                                       int G) {
+    const int lane = threadIdx.x & 63;
+    const int M = *Mdev;
+    for (int r = (blockIdx.x * blockDim.x + threadIdx.x) / 64; r < M;
+         r += gridDim.x * blockDim.x / 64) {
+        const int t = ridx[r], i = t % N;
+        int link[CHAIN_MAX];   // the chain's reused tokens' frames, the token's own first
+        int n = 0, g = t / N;
+        while (n < CHAIN_MAX && cur[(size_t)g * N + i]) {
+            link[n++] = g;
+            const FrameRefs q = reorder_refs(g, G, F);
+            const int next = src[(size_t)g * N + i] ? q.fut : q.past;
+            if (next < 0) break;
+            g = next;
+        }
+        const float4* root = (const float4*)(x + ((size_t)g * N + i) * D);
+        float4* out = (float4*)(x + (size_t)t * D);
+        for (int c = lane; c < D / 4; c += 64) {
+            float4 v = root[c];
+            for (int k = n - 1; k >= 0; --k) {
+                const size_t slot = (size_t)rslot[(size_t)link[k] * N + i];
+                const float4 d = ((const float4*)(rbuf + slot * D))[c];
+                v.x += d.x;
+                v.y += d.y;
+                v.z += d.z;
+                v.w += d.w;
+            }
+            out[c] = v;
+        }
+    }
+}
+
 __global__ __launch_bounds__(256) void final_ln_k(const float* x, int F, int N, int D,
                                                   const float* g, const float* b, float* emb) {
     const int lane = threadIdx.x & 63;
@@ -613,9 +658,17 @@ void launch_scan(const int* cnt, int per, int F, int tokens, int* qoff, int* M, 
 }
 
 void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,
-                    int* pos, int* qoff_out, int* ridx, hipStream_t s, int skip, int ext_row) {
+                    int* pos, int* qoff_out, int* ridx, hipStream_t s, int skip, int ext_row,
+                    int* rslot) {
     hipLaunchKernelGGL(compact_k, dim3(F), dim3(256), 0, s, cur, qoff_in, F, N, G, idx, pos,
-                       qoff_out, ridx, skip, ext_row);
+                       qoff_out, ridx, skip, ext_row, rslot);
+}
+
+void launch_restore_chain(float* x, const float* rbuf, const int* ridx, const int* rslot,
+                          const uint8_t* cur, const uint8_t* src, const int* Mdev, int Mmax, int F,
+                          int N, int D, int G, hipStream_t s) {
+    hipLaunchKernelGGL(restore_chain_k, dim3(grid_for((size_t)Mmax, 4, 8192)), dim3(256), 0, s, x,
+                       rbuf, ridx, rslot, cur, src, Mdev, F, N, D, G);
 }
 
 void launch_copy_ref_kv(const void* qkv, const int* qoff, int f, int N, int D, int el, void* dst,

@@ -562,7 +562,8 @@ def pin_reorder_future(ora):
 
 
 def pin_reorder_brute(ora):
-    cases = ((M_A, 4, 11), (M_B, 8, 13), (M_B, 12, 14), (M_BR, 4, 9), (M_BD, 8, 10))
+    cases = ((M_A, 4, 11), (M_B, 8, 13), (M_B, 12, 14), (M_BR, 4, 9), (M_BD, 8, 10),
+             (M_BRD, 4, 9))
     for m, G, F in cases:
         w, blob = weights(m, 40 + G)
         fr = mixed_frames(m, F, G, seed=F)

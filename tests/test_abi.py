@@ -82,7 +82,6 @@ def test_weights_floats_with_decision_section():
     (dict(dtype=7), dj.DV_EINVAL),
     (dict(width=200, heads=2), dj.DV_EUNSUPPORTED),   # width not a tile multiple
     (dict(flags=8), dj.DV_EUNSUPPORTED),              # unknown flag bit
-    (dict(flags=5), dj.DV_EUNSUPPORTED),              # restoration with reordering
 ])
 def test_create_rejects_bad_config(kw, code):
     cfg = _cfg(**kw)

@@ -170,3 +170,85 @@ def test_reorder_needs_group_multiple_of_4():
     with pytest.raises(dj.DejaVuError) as e:
         enc.encode(dev(fr), 6, 0.9)
     assert e.value.code == dj.DV_EINVAL and "multiple of 4" in dj.dv_last_error()
+    # with restoration, chains of sources are bounded: at most 60 frames per group
+    mr = dataclasses.replace(m, restore=True)
+    enc = encoder(mr, synth.make_blob(mr, 59), 64)
+    with pytest.raises(dj.DejaVuError) as e:
+        enc.encode(dev(fr[:4]), 64, 0.9)
+    assert e.value.code == dj.DV_EINVAL and "<= 60" in dj.dv_last_error()
+    enc.encode(dev(fr[:4]), 60, 0.9)
+
+
+TINY_OR = dataclasses.replace(TINY_O, restore=True)
+MID_OR = ModelConfig(112, 16, 3, 256, 4, 512, "bf16", restore=True, reorder=True)
+
+
+def longest_chain(mg, G):
+    """Longest chain of reused sources in a map (out_masks codes: 1 past, 2 future)."""
+    from oracle.reusevit import reference_frames
+    F, L, N = mg.shape
+    best = 0
+    for l in range(L):
+        for f in range(F):
+            for i in range(N):
+                g, n = f, 0
+                while mg[g, l, i]:
+                    n += 1
+                    _, past, fut = reference_frames(g, G, F)
+                    g = fut if mg[g, l, i] == 2 else past
+                best = max(best, n)
+    return best
+
+
+@pytest.mark.parametrize("m,G,F,batch", [(TINY_OR, 4, 8, 8), (MID_OR, 8, 21, 8),
+                                         (TINY_OR, 60, 61, 64)],
+                         ids=["tiny", "mid-batched", "tiny-g60-longest-chains"])
+def test_reorder_with_restoration(m, G, F, batch):
+    """Restoration on reused rows under reordering: a reused row is its source's new row plus the
+    restoration MLP of its input difference to the source, built along chains of sources."""
+    w = synth.make_weights(m, 60, perturb_ln=True, std=0.05)
+    blob = synth.pack_weights(w, m)
+    fr = _frames(m, F, 60)
+    dt = "f32" if m.dtype == "f32" else "bf16"
+    for tau in ((0.95,) if m.dtype == "f32" else (0.9, 0.6)):
+        tau = float(np.float32(tau))
+        emb, mg, toks = _run(m, blob, fr, G, tau, batch)
+        r = oracle.encode(fr, blob, m.as_dict(), G, masks=(mg != 0), sources=(mg == 2))
+        bad, bad_src, inside = reorder_parity(mg, r, tau)
+        assert bad == 0 and bad_src == 0, f"tau={tau}: {bad} decisions, {bad_src} sources off"
+        assert 0.05 < oracle.reuse_rate(mg, G) < 0.99
+        check_close(emb, r["emb"], dt, f"embeddings tau={tau}")
+        check_close(toks, r["tokens"], dt, f"tokens tau={tau}")
+    # the restoration changes reused rows: without it the outputs differ
+    base = dataclasses.replace(m, restore=False)
+    r0 = oracle.encode(fr, synth.pack_weights(w, base), base.as_dict(), G, masks=(mg != 0),
+                       sources=(mg == 2))
+    assert np.max(np.abs(r0["tokens"] - r["tokens"])) > 1e-3
+    if G == 60:
+        assert longest_chain(mg, G) == 16, "want chains of the maximum length"
+    # batching (with the look-ahead I frame) does not change results
+    again = _run(m, blob, fr, G, tau, 2 * batch)
+    for a, b in zip(again, (emb, mg, toks)):
+        assert np.array_equal(a, b)
+
+
+def test_full_method_decision_restoration_reordering():
+    """The paper's full method on the GPU: the decision MLP gating with reordered references and
+    the restoration layer on reused rows, against the oracle replaying the GPU's map and sources
+    (decisions judged outside the weight-derived margin)."""
+    m = ModelConfig(112, 16, 3, 256, 4, 512, "bf16", restore=True, decision=True, reorder=True)
+    w = synth.make_weights(m, 61, perturb_ln=True, std=0.05)
+    blob = synth.pack_weights(w, m)
+    G, F = 8, 17
+    fr = _frames(m, F, 61)
+    r0 = oracle.encode(fr, blob, m.as_dict(), G, tau=0.0)
+    tau = float(np.float32(np.quantile(r0["dec"][~np.isnan(r0["dec"])], 0.4)))
+    emb, mg, toks = _run(m, blob, fr, G, tau, 8)
+    r = oracle.encode(fr, blob, m.as_dict(), G, masks=(mg != 0), sources=(mg == 2))
+    d = r["dec"]
+    ok = ~np.isnan(d) & (np.abs(d - tau) >= decision_band(w, m, r["t"]))
+    assert int(np.sum((mg[ok] != 0) != (d[ok] > tau))) == 0
+    assert reorder_parity(mg, r)[1] == 0
+    assert 0.1 < oracle.reuse_rate(mg, G) < 0.95
+    check_close(emb, r["emb"], "bf16", "embeddings")
+    check_close(toks, r["tokens"], "bf16", "tokens")
