@@ -227,7 +227,8 @@ def main():
                     help="reordered I/P/B referencing with past and future references")
     ap.add_argument("--stream-chunk", type=int, default=0,
                     help="deliver each batch to the timed encodes as a stream of calls of this "
-                         "many frames (dv_stream_encode; groups span calls)")
+                         "many frames (dv_stream_encode; groups span calls; a reordered stream "
+                         "is flushed at the end)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device-to-device copy (HBM counter calibration)")
     ap.add_argument("--traffic-record", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_OUT"),
@@ -322,6 +323,7 @@ def main():
         enc.stream_reset()
         for k in range(0, F, args.stream_chunk):
             enc.stream_encode(x[k:k + args.stream_chunk], G, tau, want_masks=False)
+        enc.stream_flush(want_masks=False)   # frames held by a reordered stream
 
     # dense reference (same kernels, reuse off)
     def time_calls(tau_list, steps, warmup, profile_stage=None):

@@ -207,14 +207,39 @@ int dv_encode_tokens(dv_handle* h, const float* frames, int n_frames, int group_
  * are those of one dv_encode_tokens call over all frames of the stream.  frames, masks (NULL:
  * gate mode with tau), out_embeddings, out_masks and out_tokens (both may be NULL) cover this
  * call's frames, with the layouts of dv_encode_tokens.  group_size must stay the same until the
- * next reset.  Not available with DV_FLAG_REORDER (DV_EUNSUPPORTED).  Errors as
- * dv_encode_tokens, plus DV_EINVAL for a changed group_size or a stream left inconsistent by a
- * failed call (reset it), DV_ENOMEM for the cache. */
+ * next reset.
+ * With DV_FLAG_REORDER (the paper's streaming use of reordering, which buffers a few frames):
+ * a frame between anchors a and a + 4 (stream indices that are multiples of 4) needs the later
+ * anchor, so the frames after the last anchor received so far (at most 3) are held by the
+ * handle and encoded by the call that brings their anchor.  A call then outputs the frames it
+ * completes, in stream order: the frames held before it, then its own frames up to its last
+ * anchor; their number is n_frames + (frames held before) - (frames held after), see
+ * dv_stream_held, and the output buffers must have room for n_frames + 3 frames.  A held
+ * frame is encoded with the tau of the call that completes it; a stream holding frames must
+ * keep to gate mode or to injected maps (DV_EINVAL otherwise); the held frames' maps are kept.
+ * dv_stream_flush encodes the held frames as the stream's last.  Results, with the flush, are
+ * those of one dv_encode_tokens call over all frames of the stream.  Needs max_batch_frames >
+ * group_size; the handle also keeps the held frames' pixels and maps and a staging area for
+ * maps (3 frames of pixels, (3 + max_batch_frames) L N bytes).
+ * Errors as dv_encode_tokens, plus DV_EINVAL for a changed group_size, a stream left
+ * inconsistent by a failed call (reset it), a reordered stream switching between gate mode and
+ * injected maps while frames are held, or max_batch_frames <= group_size under reordering;
+ * DV_ENOMEM for the cache. */
 int dv_stream_encode(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
                      const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,
                      float* out_tokens, hipStream_t stream);
-/* Forget the stream position and the cached reference (the cache memory is kept). */
+/* Forget the stream position, the cached reference and any held frames (the memory is kept). */
 int dv_stream_reset(dv_handle* h);
+/* Number of frames a reordered stream holds (0 .. 3; always 0 without DV_FLAG_REORDER), a host
+ * value known when the last call returned.  Errors: DV_EINVAL (null handle or n_held). */
+int dv_stream_held(const dv_handle* h, int* n_held);
+/* End a stream: encode the held frames (DV_FLAG_REORDER) as its last frames, whose later anchor
+ * is absent, with the mode and tau of the last dv_stream_encode call, write their results to
+ * out_embeddings, out_masks and out_tokens (the latter two may be NULL; layouts as
+ * dv_stream_encode), then reset the stream.  With no held frames only the reset happens.
+ * Errors: DV_EINVAL (null handle; null out_embeddings while frames are held), DV_EHIP. */
+int dv_stream_flush(dv_handle* h, float* out_embeddings, uint8_t* out_masks, float* out_tokens,
+                    hipStream_t stream);
 
 /* Stream compaction of a reuse map on its own (token filtration, Section 3.3;
  * stream compaction across the frames of a batch, Section 5.3).

@@ -229,6 +229,16 @@ struct dv_handle {
     long long st_ref = -1;
     float* xc = nullptr;   // [L+1, N, D] the cached reference's layer inputs x^0 .. x^L
     void* kvc = nullptr;   // [L, N, 2D] elem: its keys and values per layer
+    // reordered streams: frames held until their later anchor arrives (stream frames
+    // st_pos - st_hold .. st_pos - 1), with the pixels, the maps of a mask-injection stream, a
+    // staging area for a batch's maps, and the mode and tau of the last call
+    int st_hold = 0;
+    float* hold = nullptr;     // [3, 3, S, S]
+    uint8_t* holdm = nullptr;  // [3, L, N]
+    uint8_t* injs = nullptr;   // [B, L, N]
+    int st_masks = -1;         // -1: no frame yet, 0: gate mode, 1: injected maps
+    int st_mode = 0;
+    float st_tau = 0.f;
     void* Hr = nullptr;    // [Tp, 128] elem: restoration hidden rows
     int *idx_id, *pos_id, *qoff_id;  // identity lists (reuse off)
     int id_frames = -1;              // frames the identity lists were built for
@@ -290,12 +300,14 @@ int collect(dv_handle* h) {
 
 // ---- one batch of whole groups --------------------------------------------------------------
 // frames, inj, emb, om, tokens start at local frame `skip`; frames below skip are carried over
-// from an earlier call of a stream (0: the cached reference; the others stand for frames
-// already returned).  fill >= 0: cache local frame fill, a reference whose group continues in
-// the next call.
+// from an earlier call of a stream (local frame `cached`: the cached reference; the others stand
+// for frames already returned).  fill >= 0: cache local frame fill, a reference needed by frames
+// of the next call.  npend > 0: the first npend computed frames' pixels are at `pend`, the rest
+// at `frames`.
 int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float tau,
               const uint8_t* inj, float* emb, uint8_t* om, float* tokens, hipStream_t s,
-              int skip = 0, int fill = -1) {
+              int skip = 0, int fill = -1, int cached = 0, const float* pend = nullptr,
+              int npend = 0) {
     const Dims& d = h->d;
     const bool bf = d.bf16;
     const int N = d.N, D = d.D, L = d.L;
@@ -312,11 +324,16 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
     const size_t el = bf ? 2 : 4;
     const size_t kv_bytes = (size_t)N * 2 * D * el;           // one frame's keys and values
     float* xs = h->x + (size_t)skip * N * D;                  // the first computed frame's rows
+    float* xcached = h->x + (size_t)cached * N * D;
     if (skip > 0)   // the cached reference's layer-0 rows
-        HIP_TRY(hipMemcpyAsync(h->x, h->xc, row_bytes, hipMemcpyDeviceToDevice, s));
+        HIP_TRY(hipMemcpyAsync(xcached, h->xc, row_bytes, hipMemcpyDeviceToDevice, s));
     {   // patch embedding + class-token rows
         Scope sc(h, DV_STAGE_PATCH, s);
-        launch_im2col(bf, frames, F - skip, d.S, d.p, d.Kp, h->A, s);
+        if (npend > 0)
+            launch_im2col(bf, pend, npend, d.S, d.p, d.Kp, h->A, s);
+        if (F - skip > npend)
+            launch_im2col(bf, frames, F - skip - npend, d.S, d.p, d.Kp,
+                          (char*)h->A + (size_t)npend * d.P * d.Kp * el, s);
         launch_cls_init(xs, h->cls, h->pos, F - skip, N, D, s);
         GemmArgs g{};
         g.A = h->A;
@@ -344,14 +361,16 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
     // learned decision gate: gate mode only (injected maps and the sentinels bypass it)
     const bool decide = d.decision && mode == GATE_COS;
     const bool reord = d.reorder && !dense;
+    // reordered without restoration: reused rows are aliases, resolved through the root map
+    const bool alias = reord && !restore;
 
     for (int l = 0; l < L; ++l) {
         const LayerW& w = h->layers[l];
         uint8_t* cur = h->mask[l & 1];
         uint8_t* prev = l > 0 ? h->mask[(l - 1) & 1] : nullptr;
         if (fill >= 0)   // the layer input of a reference carried to the next call
-            HIP_TRY(hipMemcpyAsync(h->xc + (size_t)l * N * D, h->x + (size_t)fill * N * D,
-                                   row_bytes, hipMemcpyDeviceToDevice, s));
+            launch_copy_rows(h->x, (alias && l > 0) ? h->root : nullptr, fill, N, D,
+                             h->xc + (size_t)l * N * D, s);
         {   // reuse gate + LN1 of every recomputed token (reuse off: LN1 of every token)
             Scope sc(h, DV_STAGE_GATE, s);
             GateArgs ga{};
@@ -381,7 +400,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             ga.reorder = reord;
             ga.src = reord ? h->srcmap : nullptr;
             // restored rows are written out every layer; otherwise reused rows alias their root
-            ga.root = (reord && !restore && l > 0) ? h->root : nullptr;
+            ga.root = (alias && l > 0) ? h->root : nullptr;
             ga.skip = skip;
             launch_gate(bf, ga, s);
         }
@@ -431,7 +450,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
                                      3 * D * el, (const char*)h->kvc + (size_t)l * kv_bytes,
                                      2 * D * el, 2 * D * el, N, hipMemcpyDeviceToDevice, s));
         if (fill >= 0)
-            launch_copy_ref_kv(h->qkv, qoff, fill, N, D, (int)el,
+            launch_copy_ref_kv(h->qkv, pos, fill, N, D, (int)el,
                                (char*)h->kvc + (size_t)l * kv_bytes, s);
         g.a_idx = nullptr;
         AttnArgs at{};
@@ -495,11 +514,8 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             launch_gemm(Epi::Fc2, bf, g, s);
         }
         if (skip > 0)   // the cached reference's new rows, for the restoration, merges, next gate
-            HIP_TRY(hipMemcpyAsync(h->x, h->xc + (size_t)(l + 1) * N * D, row_bytes,
+            HIP_TRY(hipMemcpyAsync(xcached, h->xc + (size_t)(l + 1) * N * D, row_bytes,
                                    hipMemcpyDeviceToDevice, s));
-        if (fill >= 0 && l == L - 1)
-            HIP_TRY(hipMemcpyAsync(h->xc + (size_t)L * N * D, h->x + (size_t)fill * N * D,
-                                   row_bytes, hipMemcpyDeviceToDevice, s));
         if (restore && reord) {   // restoration outputs, then each reused row along its chain
             Scope sc(h, DV_STAGE_RESTORE, s);
             GemmArgs r{};
@@ -547,6 +563,9 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             Scope sc(h, DV_STAGE_MERGE, s);
             launch_merge(h->x, cur, nullptr, F, N, D, G, s);
         }
+        if (fill >= 0 && l == L - 1)   // the reference's last-layer rows (restored ones included)
+            launch_copy_rows(h->x, alias ? h->root : nullptr, fill, N, D,
+                             h->xc + (size_t)L * N * D, s);
     }
     {
         Scope sc(h, DV_STAGE_FINAL, s);
@@ -598,6 +617,110 @@ int encode_impl(dv_handle* h, const float* frames, int n, int G, float tau, cons
     return DV_OK;
 }
 
+// The stream's device buffers, on its first call: the reference cache and, under reordering, the
+// held frames' pixels and maps and the map staging area.
+int stream_buffers(dv_handle* h) {
+    const Dims& d = h->d;
+    const size_t el = d.bf16 ? 2 : 4, N = d.N, D = d.D, L = d.L;
+    hipError_t e = hipSuccess;
+    if (!h->xc) e = hipMalloc((void**)&h->xc, (L + 1) * N * D * sizeof(float));
+    if (e == hipSuccess && !h->kvc) e = hipMalloc(&h->kvc, L * N * 2 * D * el);
+    if (d.reorder) {
+        if (e == hipSuccess && !h->hold)
+            e = hipMalloc((void**)&h->hold, (size_t)3 * 3 * d.S * d.S * sizeof(float));
+        if (e == hipSuccess && !h->holdm) e = hipMalloc((void**)&h->holdm, 3 * L * N);
+        if (e == hipSuccess && !h->injs) e = hipMalloc((void**)&h->injs, (size_t)d.B * L * N);
+    }
+    if (e != hipSuccess)
+        return fail(e == hipErrorOutOfMemory ? DV_ENOMEM : DV_EHIP, "stream buffers: %s",
+                    hipGetErrorString(e));
+    return DV_OK;
+}
+
+// A reordered stream.  A frame between anchors a and a + 4 (stream indices that are multiples of
+// 4) references the later one, so the frames after the last anchor received are held (at most 3)
+// and encoded by the call that brings their anchor, or by a flush, which encodes them as the
+// stream's last frames (no later anchor) and ends the stream.  A call outputs the frames it
+// completes, in stream order: the held ones, then its own up to its last anchor.  Each batch
+// starts at a group boundary: the frames before the first one computed are carried over (the
+// last of them, the anchor of the first computed frame, from the cache), and ends on an anchor,
+// which is cached for the next batch.
+int stream_reorder_impl(dv_handle* h, const float* frames, int n, int G, int mode, float tau,
+                        const uint8_t* masks, float* emb, uint8_t* om, float* tokens,
+                        hipStream_t s, bool flush) {
+    const Dims& d = h->d;
+    if (d.B <= G)
+        return fail(DV_EINVAL, "streaming with reordered referencing needs max_batch_frames > "
+                    "group_size (%d <= %d)", d.B, G);
+    const size_t img = (size_t)3 * d.S * d.S, ml = (size_t)d.L * d.N, N = d.N, D = d.D;
+    const long long st = h->st_pos;                   // frames received before this call
+    const long long total = st + n;
+    const long long done = st - h->st_hold;           // the first frame not yet output
+    const long long last = flush ? total - 1 : (total - 1) / 4 * 4;   // the last it completes
+    for (long long u = done; u <= last;) {
+        int lead = 0;   // carried-over frames: the gaps since the group start, then the anchor
+        if (u % G != 0 && mode != GATE_NONE) {
+            if (h->st_ref != u - 1)
+                return fail(DV_EINVAL, "the stream lost its cached reference (an earlier call "
+                            "failed?): call dv_stream_reset");
+            lead = (int)(u - (u - 1) / G * G);
+        }
+        long long cnt = std::min<long long>(d.B - lead, last - u + 1);
+        if (u + cnt - 1 < last) cnt = (u + cnt - 1) / 4 * 4 - u + 1;   // end on an anchor
+        if (cnt < 1) return fail(DV_EINVAL, "internal: empty stream batch");
+        const long long e = u + cnt - 1;
+        const int F = lead + (int)cnt;
+        const int npend = (int)std::max<long long>(0, std::min(st, e + 1) - u);
+        const float* pend = npend ? h->hold + (size_t)(u - done) * img : nullptr;
+        const float* fr = frames ? frames + (size_t)std::max<long long>(0, u - st) * img : nullptr;
+        const uint8_t* inj = nullptr;
+        if (masks || (flush && mode == GATE_INJECT)) {
+            if (npend) {   // held frames' maps, then the call's own
+                HIP_TRY(hipMemcpyAsync(h->injs, h->holdm + (size_t)(u - done) * ml, npend * ml,
+                                       hipMemcpyDeviceToDevice, s));
+                if (cnt > npend)
+                    HIP_TRY(hipMemcpyAsync(h->injs + npend * ml, masks, (cnt - npend) * ml,
+                                           hipMemcpyDeviceToDevice, s));
+                inj = h->injs;
+            } else {
+                inj = masks + (size_t)(u - st) * ml;
+            }
+        }
+        const size_t k = (size_t)(u - done);
+        const int fill = flush ? -1 : F - 1;
+        int rc = run_batch(h, fr, F, G, mode, tau, inj, emb + k * D, om ? om + k * ml : nullptr,
+                           tokens ? tokens + k * N * D : nullptr, s, lead, fill,
+                           lead > 0 ? lead - 1 : 0, pend, npend);
+        if (rc) return rc;
+        if (fill >= 0) h->st_ref = e;
+        u = e + 1;
+    }
+    if (flush) {
+        h->st_pos = 0;
+        h->st_hold = 0;
+        h->st_ref = -1;
+        h->st_masks = -1;
+        return DV_OK;
+    }
+    // the frames after the last anchor wait for the next call; those held already stay in place
+    // (when this call completed nothing) or are all replaced by frames of this call
+    const long long h0 = last + 1;
+    for (long long g = std::max(h0, st); g < total; ++g) {
+        HIP_TRY(hipMemcpyAsync(h->hold + (size_t)(g - h0) * img, frames + (size_t)(g - st) * img,
+                               img * sizeof(float), hipMemcpyDeviceToDevice, s));
+        if (masks)
+            HIP_TRY(hipMemcpyAsync(h->holdm + (size_t)(g - h0) * ml, masks + (size_t)(g - st) * ml,
+                                   ml, hipMemcpyDeviceToDevice, s));
+    }
+    h->st_hold = (int)(total - h0);
+    h->st_pos = total;
+    h->st_G = G;
+    h->st_masks = masks ? 1 : 0;
+    h->st_mode = mode;
+    h->st_tau = tau;
+    return DV_OK;
+}
+
 // A stream call: frames get stream indices st_pos .. st_pos + n - 1; frame g's reference is
 // frame G * floor(g / G), possibly from an earlier call (then read from the cache).
 int stream_impl(dv_handle* h, const float* frames, int n, int G, float tau, const uint8_t* masks,
@@ -608,8 +731,6 @@ int stream_impl(dv_handle* h, const float* frames, int n, int G, float tau, cons
     if (G < 1) return fail(DV_EINVAL, "group_size must be >= 1 (got %d)", G);
     const Dims& d = h->d;
     if (G > d.B) return fail(DV_EINVAL, "group_size %d exceeds max_batch_frames %d", G, d.B);
-    if (d.reorder)
-        return fail(DV_EUNSUPPORTED, "streaming with reordered referencing is not supported");
     if (h->st_pos > 0 && G != h->st_G)
         return fail(DV_EINVAL, "group_size %d differs from the stream's %d (dv_stream_reset "
                     "starts a new stream)", G, h->st_G);
@@ -620,15 +741,24 @@ int stream_impl(dv_handle* h, const float* frames, int n, int G, float tau, cons
         if (std::isnan(tau)) return fail(DV_EINVAL, "tau is NaN");
         mode = (tau == -INFINITY) ? GATE_NONE : (tau == INFINITY) ? GATE_ALL : GATE_COS;
     }
+    if (d.reorder && G % 4)
+        return fail(DV_EINVAL, "reordered referencing needs a group_size that is a multiple of 4 "
+                    "(got %d)", G);
+    if (d.reorder && d.restore && G / 4 + 1 > CHAIN_MAX)
+        return fail(DV_EINVAL, "reordered referencing with restoration supports group_size <= %d "
+                    "(got %d)", 4 * (CHAIN_MAX - 1), G);
+    if (d.reorder && h->st_hold > 0 && (masks != nullptr) != (h->st_masks == 1))
+        return fail(DV_EINVAL, "a reordered stream holding frames cannot switch between gate "
+                    "mode and injected maps");
     HIP_TRY(hipSetDevice(h->device));
-    const size_t el = d.bf16 ? 2 : 4, N = d.N, D = d.D, L = d.L;
-    if (!h->xc) {   // the reference cache, on the first stream call
-        hipError_t e = hipMalloc((void**)&h->xc, (L + 1) * N * D * sizeof(float));
-        if (e == hipSuccess) e = hipMalloc(&h->kvc, L * N * 2 * D * el);
-        if (e != hipSuccess)
-            return fail(e == hipErrorOutOfMemory ? DV_ENOMEM : DV_EHIP, "stream cache: %s",
-                        hipGetErrorString(e));
+    if (int rc = stream_buffers(h)) return rc;
+    if (d.reorder) {
+        int rc = stream_reorder_impl(h, frames, n, G, mode, tau, masks, emb, om, tokens, s, false);
+        if (rc) return rc;
+        HIP_TRY(hipGetLastError());
+        return DV_OK;
     }
+    const size_t N = d.N, D = d.D, L = d.L;
     const size_t img = (size_t)3 * d.S * d.S, ml = L * N;
     const long long g0 = h->st_pos;
     const long long last = (g0 + n - 1) / G * G;   // the last group's reference
@@ -910,6 +1040,9 @@ int dv_destroy(dv_handle* h) {
     if (h->ws) (void)hipFree(h->ws);
     if (h->xc) (void)hipFree(h->xc);
     if (h->kvc) (void)hipFree(h->kvc);
+    if (h->hold) (void)hipFree(h->hold);
+    if (h->holdm) (void)hipFree(h->holdm);
+    if (h->injs) (void)hipFree(h->injs);
     delete h;
     return DV_OK;
 }
@@ -953,7 +1086,30 @@ int dv_stream_reset(dv_handle* h) {
     h->st_pos = 0;
     h->st_G = 0;
     h->st_ref = -1;
+    h->st_hold = 0;
+    h->st_masks = -1;
     return DV_OK;
+}
+
+int dv_stream_held(const dv_handle* h, int* n_held) {
+    if (!h || !n_held) return fail(DV_EINVAL, "handle and n_held must not be NULL");
+    *n_held = h->st_hold;
+    return DV_OK;
+}
+
+int dv_stream_flush(dv_handle* h, float* out_embeddings, uint8_t* out_masks, float* out_tokens,
+                    hipStream_t stream) {
+    if (!h) return fail(DV_EINVAL, "handle is NULL");
+    if (h->st_hold > 0 && !out_embeddings)
+        return fail(DV_EINVAL, "out_embeddings must not be NULL while frames are held");
+    if (h->st_hold > 0) {
+        HIP_TRY(hipSetDevice(h->device));
+        int rc = stream_reorder_impl(h, nullptr, 0, h->st_G, h->st_mode, h->st_tau, nullptr,
+                                     out_embeddings, out_masks, out_tokens, stream, true);
+        if (rc) return rc;
+        HIP_TRY(hipGetLastError());
+    }
+    return dv_stream_reset(h);
 }
 
 int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size, int32_t* idx,

@@ -170,15 +170,19 @@ void launch_scan(const int* cnt, int per, int F, int tokens, int* qoff, int* M, 
 // lists, qoff_in ignored and qoff_out written)
 // ridx (or nullptr): the reused tokens f*N+i of non-reference frames in frame-major order, at
 // slot (f*N - qoff[f]) + (reused tokens of frame f before i)
-// skip > 0 (stream): frames below skip have no rows; frame 0 is the cached reference, whose keys
-// and values sit at packed rows ext_row .. ext_row + N - 1 (pos of its reused tokens points there)
+// skip > 0 (stream): frames below skip have no rows; one of them is the cached reference (the
+// first in the star, the last under reordering), whose keys and values sit at packed rows
+// ext_row .. ext_row + N - 1: pos of every token of those frames points there
 // rslot (or nullptr): for every reused token, its slot in ridx
 void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,
                     int* pos, int* qoff_out, int* ridx, hipStream_t s, int skip = 0,
                     int ext_row = 0, int* rslot = nullptr);
-// dst[i, 0:2D] = K|V of frame f's packed row qoff[f] + i (a fully recomputed frame), el-byte elems
-void launch_copy_ref_kv(const void* qkv, const int* qoff, int f, int N, int D, int el, void* dst,
+// dst[i, 0:2D] = K|V of packed row pos[f*N + i], el-byte elems
+void launch_copy_ref_kv(const void* qkv, const int* pos, int f, int N, int D, int el, void* dst,
                         hipStream_t s);
+// dst[i, 0:D] = x row of token i of frame root[f*N + i] (root == nullptr: of frame f)
+void launch_copy_rows(const float* x, const int* root, int f, int N, int D, float* dst,
+                      hipStream_t s);
 
 // LayerNorm of rows (optionally gathered through idx) into elem rows: dst[r] = LN(src[g(r)])
 void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* Mdev, int Mmax,

@@ -375,8 +375,8 @@ __global__ __launch_bounds__(256) void compact_k(const uint8_t* cur, const int* 
     const int f = blockIdx.x;
     const int r = (f / G) * G;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    if (f < skip) {   // carried over from an earlier call: no rows; frame 0's keys/values are the
-                      // cached rows at ext_row (the other carried-over frames are never read)
+    if (f < skip) {   // carried over from an earlier call: no rows; the cached reference's
+                      // keys/values are the rows at ext_row (the other such frames are never read)
         for (int i = tid; i < N; i += 256) pos[(size_t)f * N + i] = ext_row + i;
         return;
     }
@@ -519,18 +519,32 @@ __global__ __launch_bounds__(256) void resolve_k(const uint8_t* __restrict__ cur
     }
 }
 
-// --- keys/values of one fully recomputed frame (its packed rows qoff[f] .. qoff[f] + N - 1) to a
-// dense [N, 2D] copy: the reference carried to the next call of a stream
-__global__ __launch_bounds__(256) void copy_ref_kv_k(const void* qkv, const int* qoff, int f, int N,
+// --- keys/values of frame f (token i's at packed row pos[f*N + i]: its own, or its source's
+// when reused) to a dense [N, 2D] copy: the reference carried to the next call of a stream
+__global__ __launch_bounds__(256) void copy_ref_kv_k(const void* qkv, const int* pos, int f, int N,
                                                      int D, int el, void* dst) {
     const size_t per = (size_t)2 * D * el / 16;   // 16-byte pieces of a key/value row
     const size_t total = (size_t)N * per;
-    const size_t row0 = (size_t)qoff[f];
     for (size_t t = blockIdx.x * (size_t)blockDim.x + threadIdx.x; t < total;
          t += (size_t)gridDim.x * blockDim.x) {
         const size_t i = t / per, c = t % per;
-        const uint4* src = (const uint4*)((const char*)qkv + ((row0 + i) * 3 * D + D) * el);
+        const size_t row = (size_t)pos[(size_t)f * N + i];
+        const uint4* src = (const uint4*)((const char*)qkv + (row * 3 * D + D) * el);
         ((uint4*)dst)[t] = src[c];
+    }
+}
+
+// --- frame f's token rows to a dense [N, D] copy; with `root`, token i's row is that of frame
+// root[f*N + i] (reordered referencing: reused rows are aliases of the frame recomputing them)
+__global__ __launch_bounds__(256) void copy_rows_k(const float* x, const int* root, int f, int N,
+                                                   int D, float* dst) {
+    const int lane = threadIdx.x & 63;
+    for (int i = (blockIdx.x * blockDim.x + threadIdx.x) / 64; i < N;
+         i += gridDim.x * blockDim.x / 64) {
+        const int r = root ? root[(size_t)f * N + i] : f;
+        const float4* s = (const float4*)(x + ((size_t)r * N + i) * D);
+        float4* d = (float4*)(dst + (size_t)i * D);
+        for (int c = lane; c < D / 4; c += 64) d[c] = s[c];
     }
 }
 
@@ -671,10 +685,16 @@ void launch_restore_chain(float* x, const float* rbuf, const int* ridx, const in
                        rbuf, ridx, rslot, cur, src, Mdev, F, N, D, G);
 }
 
-void launch_copy_ref_kv(const void* qkv, const int* qoff, int f, int N, int D, int el, void* dst,
+void launch_copy_ref_kv(const void* qkv, const int* pos, int f, int N, int D, int el, void* dst,
                         hipStream_t s) {
     hipLaunchKernelGGL(copy_ref_kv_k, dim3(grid_for((size_t)N * 2 * D * el / 16, 256)), dim3(256),
-                       0, s, qkv, qoff, f, N, D, el, dst);
+                       0, s, qkv, pos, f, N, D, el, dst);
+}
+
+void launch_copy_rows(const float* x, const int* root, int f, int N, int D, float* dst,
+                      hipStream_t s) {
+    hipLaunchKernelGGL(copy_rows_k, dim3(grid_for((size_t)N, 4)), dim3(256), 0, s, x, root, f, N,
+                       D, dst);
 }
 
 void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* Mdev, int Mmax,

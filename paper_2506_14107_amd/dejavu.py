@@ -66,6 +66,8 @@ def load(path=None):
         "dv_stream_encode": (ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                             _P, _P, _P, _P, _P]),
         "dv_stream_reset": (ctypes.c_int, [_P]),
+        "dv_stream_held": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int)]),
+        "dv_stream_flush": (ctypes.c_int, [_P, _P, _P, _P, _P]),
         "dv_profile": (ctypes.c_int, [_P, ctypes.c_uint]),
         "dv_profile_read": (ctypes.c_int, [_P, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_longlong)]),
@@ -140,6 +142,16 @@ def dv_stream_encode(handle, frames, n_frames, group_size, tau, masks, out_embed
 
 def dv_stream_reset(handle):
     _check(load().dv_stream_reset(handle))
+
+
+def dv_stream_held(handle):
+    n = ctypes.c_int(0)
+    _check(load().dv_stream_held(handle, ctypes.byref(n)))
+    return n.value
+
+
+def dv_stream_flush(handle, out_embeddings, out_masks, out_tokens, stream):
+    _check(load().dv_stream_flush(handle, out_embeddings, out_masks, out_tokens, stream))
 
 
 def dv_compact(masks, n_frames, n_tokens, group_size, idx, pos, qoff, count, stream):
@@ -243,13 +255,26 @@ class Encoder:
 
     def stream_encode(self, frames, group_size, tau=0.0, masks_in=None, want_masks=True,
                       want_tokens=False, stream=None):
-        """The next frames of a stream (gate mode with tau, or injected masks_in)."""
+        """The next frames of a stream (gate mode with tau, or injected masks_in).  Returns the
+        outputs of the frames the call completes: its own frames, except that a reordered
+        stream first completes the frames it held and then holds back those after its last
+        anchor."""
         self._check_frames(frames)
         n = frames.shape[0]
-        emb, masks, toks = self._outs(n, want_masks, want_tokens)
+        held = dv_stream_held(self.handle)
+        emb, masks, toks = self._outs(n + held, want_masks, want_tokens)
         dv_stream_encode(self.handle, _ptr(frames), n, group_size, float(tau),
                          _ptr(masks_in) if masks_in is not None else 0, _ptr(emb), _ptr(masks),
                          _ptr(toks), _stream(stream))
+        k = n + held - dv_stream_held(self.handle)
+        return tuple(o[:k] if o is not None else None for o in (emb, masks, toks))
+
+    def stream_flush(self, want_masks=True, want_tokens=False, stream=None):
+        """End the stream: the outputs of the frames it still held (none without reordering)."""
+        held = dv_stream_held(self.handle)
+        emb, masks, toks = self._outs(held, want_masks, want_tokens)
+        dv_stream_flush(self.handle, _ptr(emb) if held else 0, _ptr(masks) if held else 0,
+                        _ptr(toks) if held else 0, _stream(stream))
         return emb, masks, toks
 
     def stream_reset(self):

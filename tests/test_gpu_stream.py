@@ -2,7 +2,8 @@
 the reference of an open group is carried between calls in the handle's cache.  The stream's
 outputs must equal, bit for bit, one encode over all frames (whose parity with the CPU oracle
 the other tests establish), in every mode; one group spanning calls is also checked against
-the oracle directly."""
+the oracle directly.  Reordered streams hold the frames after the last anchor received until it
+arrives (or the stream is flushed) and must meet the same bar."""
 import dataclasses
 
 import numpy as np
@@ -124,11 +125,108 @@ def test_stream_group_size_and_reset():
     assert np.array_equal(np.concatenate([host(a), host(b)]), want)
 
 
-def test_stream_with_reordering_is_rejected():
+# --- reordered streams: frames after the last anchor are held until it arrives ---------------
+
+TINY_O = dataclasses.replace(TINY.model, reorder=True)
+SMALL_O = dataclasses.replace(SMALL, reorder=True)
+MID_O = dataclasses.replace(MID, reorder=True)
+MID_OR = dataclasses.replace(MID_O, restore=True)
+MID_OD = dataclasses.replace(MID_O, decision=True)
+MID_ORD = dataclasses.replace(MID_OR, decision=True)
+
+
+def _streamed_reordered(m, blob, fr, G, tau, masks, batch, chunks):
+    """Stream the frames in calls of the given sizes, then flush; checks each call's output count
+    against the anchors it brings."""
+    torch = require_gpu()
+    enc = encoder(m, blob, batch)
+    outs, k = [], 0
+    for c in chunks:
+        mk = dev(masks[k:k + c]) if masks is not None else None
+        o = enc.stream_encode(dev(fr[k:k + c]), G, tau, masks_in=mk, want_tokens=True)
+        k += c
+        done = (k - 1) // 4 * 4 + 1          # frames 0 .. the last anchor received
+        got = sum(x[0].shape[0] for x in outs) + o[0].shape[0]
+        assert got == done, f"after {k} frames {got} are output, want {done}"
+        outs.append(o)
+    outs.append(enc.stream_flush(want_tokens=True))
+    torch.cuda.synchronize()
+    assert k == fr.shape[0]
+    assert sum(o[0].shape[0] for o in outs) == k
+    return [np.concatenate([host(o[j]) for o in outs if o[0].shape[0]]) for j in range(3)]
+
+
+RCASES = [
+    # model, group, frames, internal batch, call sizes, tau (None: injected masks)
+    ("tiny", TINY_O, 4, 14, 8, [3, 5, 1, 5], 0.95),
+    ("small", SMALL_O, 8, 30, 16, [3, 5, 1, 8, 13], 0.9),
+    ("small-batch-g+1", SMALL_O, 8, 30, 9, [13, 10, 7], 0.9),
+    ("small-g12-chains", SMALL_O, 12, 31, 16, [2, 2, 2, 20, 5], 0.9),
+    ("small-inf", SMALL_O, 8, 20, 16, [6, 7, 7], float("inf")),
+    ("small-dense", SMALL_O, 8, 20, 16, [6, 7, 7], float("-inf")),
+    ("mid-injected", MID_O, 8, 22, 16, [5, 2, 9, 6], None),
+    ("mid-restore", MID_OR, 8, 26, 16, [11, 4, 11], 0.9),
+    ("mid-decision", MID_OD, 8, 26, 16, [11, 4, 11], 0.0),
+    ("mid-full-method", MID_ORD, 8, 23, 16, [7, 1, 1, 14], 0.0),
+]
+
+
+@pytest.mark.parametrize("name,m,G,F,batch,chunks,tau", RCASES, ids=[c[0] for c in RCASES])
+def test_reordered_stream_equals_one_shot_bitwise(name, m, G, F, batch, chunks, tau):
+    blob = synth.make_blob(m, 66, perturb_ln=True)
+    fr = _frames(m, F, 66)
+    masks = None
+    if tau is None:
+        masks = (np.random.default_rng(67).random((F, m.depth, m.n_tokens)) < 0.6).astype(np.uint8)
+        tau = 0.0
+    tau = float(np.float32(tau))
+    want = _one_shot(m, blob, fr, G, tau, masks, batch)
+    got = _streamed_reordered(m, blob, fr, G, tau, masks, batch, chunks)
+    if np.isfinite(tau) or masks is not None:
+        assert 0.05 < oracle.reuse_rate(want[1], G) < 0.99, "want a mixed map"
+        assert (want[1] == 2).any(), "want tokens reused from future anchors"
+    for a, b, what in zip(got, want, ("embeddings", "masks", "tokens")):
+        assert np.array_equal(a, b), f"{what} differ from one encode over all frames"
+
+
+def test_reordered_stream_one_frame_per_call_against_oracle():
+    """One frame per call: every B frame waits for its later anchor; the stream's outputs are
+    checked against the oracle replaying the GPU's map and sources."""
+    from .test_gpu_reorder import reorder_parity
+    m = SMALL_O
+    blob = synth.make_blob(m, 68)
+    G, F = 8, 19
+    fr = _frames(m, F, 68)
+    tau = float(np.float32(0.9))
+    emb, mk, toks = _streamed_reordered(m, blob, fr, G, tau, None, 16, [1] * F)
+    r = oracle.encode(fr, blob, m.as_dict(), G, masks=(mk != 0), sources=(mk == 2))
+    bad, bad_src, _ = reorder_parity(mk, r, tau)
+    assert bad == 0 and bad_src == 0
+    check_close(emb, r["emb"], "bf16", "embeddings")
+    check_close(toks, r["tokens"], "bf16", "tokens")
+
+
+def test_reordered_stream_rules():
     from paper_2506_14107_amd import dejavu as dj
     require_gpu()
-    m = dataclasses.replace(SMALL, reorder=True)
-    enc = encoder(m, synth.make_blob(m, 65), 8)
-    with pytest.raises(dj.DejaVuError) as e:
-        enc.stream_encode(dev(_frames(m, 4, 65)), 4, 0.9)
-    assert e.value.code == dj.DV_EUNSUPPORTED
+    m = SMALL_O
+    blob = synth.make_blob(m, 69)
+    fr = _frames(m, 12, 69)
+    enc = encoder(m, blob, 8)
+    with pytest.raises(dj.DejaVuError) as e:   # the batch must exceed the group
+        enc.stream_encode(dev(fr[:4]), 8, 0.9)
+    assert e.value.code == dj.DV_EINVAL and "max_batch_frames" in dj.dv_last_error()
+    enc = encoder(m, blob, 16)
+    out = enc.stream_encode(dev(fr[:7]), 8, 0.9)   # frames 5, 6 are held
+    assert out[0].shape[0] == 5 and dj.dv_stream_held(enc.handle) == 2
+    mk = np.zeros((3, m.depth, m.n_tokens), np.uint8)
+    with pytest.raises(dj.DejaVuError) as e:   # no switch to injected maps while holding
+        enc.stream_encode(dev(fr[7:10]), 8, 0.9, masks_in=dev(mk))
+    assert e.value.code == dj.DV_EINVAL and "injected maps" in dj.dv_last_error()
+    out = enc.stream_flush()
+    assert out[0].shape[0] == 2 and dj.dv_stream_held(enc.handle) == 0
+    # a flush ends the stream: the next call starts a new one at frame 0
+    a = enc.stream_encode(dev(fr[:9]), 8, 0.9)[0]
+    b = enc.stream_flush()[0]
+    want = _one_shot(m, blob, fr[:9], 8, float(np.float32(0.9)), None, 16)[0]
+    assert np.array_equal(np.concatenate([host(a), host(b)]), want)
