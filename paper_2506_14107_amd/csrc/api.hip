@@ -465,6 +465,7 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         // per-group blocks assume the star with the reference's rows packed in the batch
         at.G = (dense || reord || skip > 0) ? 0 : G;
         at.skip = skip;
+        at.sparse = !dense;
         at.cus = h->cus;
         {
             Scope sc(h, DV_STAGE_ATTN, s);

@@ -22,6 +22,7 @@
 //
 // fp32 path: scalar scores, softmax and P.V (small fp32 models).
 #include <algorithm>
+#include <cstdlib>
 #include <type_traits>
 
 #include "dv_internal.h"
@@ -110,14 +111,16 @@ constexpr int UW = 16;   // wavefronts of a per-unit attention block
 
 // Online-softmax attention of one query tile (fragments qf, one query per lane) against the
 // staged K/V: key blocks taken two at a time in order (kb, kb + 1) -- two independent MFMA
-// chains and one rescale per step.  krow maps a key to its LDS row.  On
-// return (m, l, o) hold the tile's running max (raw score units), sum and unnormalised output.
-// The arithmetic and its order depend only on the key values, never on where the rows sit.
-template <int DH, class KRow>
+// chains and one rescale per step.  krow maps a key to its LDS row; stage(kb) runs before the
+// step of blocks kb, kb + 1 reads them (a kernel streaming K/V through LDS loads them there).
+// On return (m, l, o) hold the tile's running max (raw score units), sum and unnormalised
+// output.  The arithmetic and its order depend only on the key values, never on where the rows
+// sit.
+template <int DH, class KRow, class Stage>
 __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, const uint16_t* Vs,
                                             int N, int lane, const bf16x8 (&qf)[DH / 16],
                                             KRow krow, float& m, float& l,
-                                            f32x16 (&o)[(DH + 31) / 32]) {
+                                            f32x16 (&o)[(DH + 31) / 32], Stage stage) {
     constexpr int KS = DH / 16;          // k-steps of S^T
     constexpr int DB = (DH + 31) / 32;   // 32-row blocks of O^T
     const int hl = lane >> 5, lr = lane & 31;
@@ -180,6 +183,7 @@ __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, co
     m = -INFINITY;
     l = 0.f;
     for (int kb = 0; kb < nkb; kb += 2) {
+        stage(kb);
         const int kb1 = kb + 1;
         const bool two = kb1 < nkb;
         const f32x16 s0 = scores(kb);
@@ -251,7 +255,9 @@ void attn_mfma_k(AttnArgs a) {
     // The grid holds as many blocks as are resident at once (a multiple of 8, one share per
     // XCD) and each block walks a list of work items (frame f, head h): one item per launch slot
     // would leave the compute units waiting on workgroup dispatch when items are short.
-    // Without reuse the items are striped over the blocks, frames fastest.  With reuse, a unit
+    // Without groups the items are striped over the blocks, heads fastest, so that the items of a
+    // frame land on all 8 XCDs (block i runs on XCD i % 8; with frames fastest, every I frame of
+    // a reordered batch, one frame in 8, would fall on the same XCD).  With groups, a unit
     // (a group's frames, one head) lives on XCD unit % 8, whose L2 then serves the reference
     // rows all of its frames read; the units of XCD x are dealt to its R blocks
     // frame-index-major (entry e = unit e % U, frame e / U of the group), so that every block
@@ -268,7 +274,7 @@ void attn_mfma_k(AttnArgs a) {
         }
     } else {
         for (int item = blockIdx.x; item < a.F * a.H; item += gridDim.x) {
-            attn_item<DH>(a, item % a.F, item / a.F, smem);
+            attn_item<DH>(a, item / a.H, item % a.H, smem);
             lds_barrier();
         }
     }
@@ -295,7 +301,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char*
     const uint16_t* qkv = (const uint16_t*)a.qkv;
     const int q0 = a.qoff[f], q1 = a.qoff[f + 1];
     const int ntile = (q1 - q0 + 31) / 32;
-    if (ntile == 0) return;
+    if (ntile <= a.tile_cut) return;   // none, or taken by per-tile wavefronts
 
     // stage K and V rows (row-major, 16-byte chunks); keys past N repeat key N-1 (finite data
     // whose scores are masked).  Up to four chunks per thread are gathered before any store.
@@ -335,7 +341,101 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char*
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
             qf[ks] = *(const bf16x8*)(qkv + (size_t)qrow * ld3 + h * DH + ks * 16 + hl * 8);
-        attend_tile<DH>(g, Ks, Vs, N, lane, qf, [](int k) { return k; }, m, l, o);
+        attend_tile<DH>(g, Ks, Vs, N, lane, qf, [](int k) { return k; }, m, l, o, [](int) {});
+        if (myq < q1) store_row<DH>((uint16_t*)a.out + (size_t)myq * D + h * DH, lane, l, o);
+    }
+}
+
+// ---- per-wavefront items (reuse on: frames with few query tiles) ------------------------------
+// A work item is one query tile (frame f, head h, tile t), taken by one wavefront on its own:
+// the frame's keys and values stream through a wavefront-private LDS buffer, 64 keys (one step
+// of attend_tile) at a time, fetched by buffer_load ... lds through pos (one instruction writes
+// 1 KiB: lane i at 16 i, so each lane fetches the chunk that belongs at its slot of the
+// swizzled layout).  Nothing is shared between wavefronts -- no barrier -- so a compute unit
+// keeps as many tiles in flight as buffers fit, where a per-frame block stages a whole frame
+// for what is mostly a single tile.  The arithmetic is attend_tile's: results equal the other
+// kernels' bit for bit.
+constexpr int SW = 4;   // wavefronts of a per-wavefront attention block
+
+template <int DH>
+struct WaveBuf {   // 64 rows of K and 64 of V, with Geo's strides
+    static constexpr int LDK = (DH == 64 || DH == 128) ? DH : DH + 8;
+    static constexpr int LDV = (DH == 64 || DH == 128) ? DH : 96;
+    static constexpr size_t ELEMS = (size_t)64 * (LDK + LDV);
+};
+
+template <int DH>
+__global__ __launch_bounds__(SW * 64) void attn_wave_k(AttnArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    constexpr int KS = DH / 16;
+    constexpr int DB = (DH + 31) / 32;
+    const int N = a.N, D = a.D;
+    const Geo g(N, DH);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int hl = lane >> 5, lr = lane & 31;
+    using WB = WaveBuf<DH>;
+    uint16_t* Ks = (uint16_t*)smem + (size_t)wave * WB::ELEMS;
+    uint16_t* Vs = Ks + (size_t)64 * WB::LDK;
+    const size_t ld3 = 3 * (size_t)D;
+    const uint16_t* qkv = (const uint16_t*)a.qkv;
+    // the packed K/V rows (and the cached reference's rows past them) are below 2^32 bytes
+    const __amdgpu_buffer_rsrc_t rq =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.qkv), (short)0, (int)0xFFFFFFF0u,
+                                          0x00020000);
+    static_assert(DH == 64, "rows of 8 16-byte slots, K and V alike");
+    constexpr int KI = 8;   // copy instructions per step for K, and as many for V
+    const int tmax = (N + 31) / 32;
+    const int items = a.F * a.H * tmax;
+    for (int item = blockIdx.x * SW + wave; item < items; item += gridDim.x * SW) {
+        const int t = item % tmax, fh = item / tmax;
+        const int f = fh / a.H, h = fh % a.H;
+        const int q0 = a.qoff[f], q1 = a.qoff[f + 1];
+        if (t * 32 >= q1 - q0 || q1 - q0 > a.tile_cut * 32) continue;   // none, or a per-frame block
+        const int* pf = a.pos + (size_t)f * N;
+        const uint32_t hoff = (uint32_t)(h * DH) * 2;
+        // Lane l fetches row r = u*8 + l/8 of instruction u, slot l%8 (K and V rows have the same
+        // 8 slots); prow holds those rows' byte offsets for the coming step, loaded one step
+        // ahead so that a step waits for one memory round trip (the copy), not two.
+        uint32_t prow[KI];
+        auto rows = [&](int kb, uint32_t (&dst)[KI]) {
+#pragma unroll
+            for (int u = 0; u < KI; ++u)
+                dst[u] = (uint32_t)pf[min(kb * 32 + u * 8 + (lane >> 3), N - 1)] *
+                             (uint32_t)(ld3 * 2) + hoff;
+        };
+        rows(0, prow);
+        // keys kb*32 .. kb*32 + 63 (past N: key N-1, finite data whose scores are masked) into
+        // the buffer; LDS row = key - kb*32, the low bits of the key as attend_tile's krow needs
+        auto stage = [&](int kb) {
+            uint32_t next[KI];
+            rows(kb + 2, next);
+            __builtin_amdgcn_s_waitcnt(0xc07f);   // this wave's reads of the last step are done
+            asm volatile("" ::: "memory");
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                const int r = u * 8 + (lane >> 3), sl = lane & 7;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rq, (__attribute__((address_space(3))) void*)(Ks + u * 512), 16,
+                    (int)(prow[u] + (uint32_t)D * 2 + (sl ^ ((r >> 1) & 7)) * 16), 0, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rq, (__attribute__((address_space(3))) void*)(Vs + u * 512), 16,
+                    (int)(prow[u] + (uint32_t)D * 4 + (sl ^ (2 * ((r >> 1) & 3))) * 16), 0, 0,
+                    0);
+            }
+            __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0): the step has landed
+            asm volatile("" ::: "memory");
+#pragma unroll
+            for (int u = 0; u < KI; ++u) prow[u] = next[u];
+        };
+        const int myq = q0 + t * 32 + lr;
+        const int qrow = myq < q1 ? myq : q1 - 1;   // tail lanes compute on a valid row
+        bf16x8 qf[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            qf[ks] = *(const bf16x8*)(qkv + (size_t)qrow * ld3 + h * DH + ks * 16 + hl * 8);
+        float m, l;
+        f32x16 o[DB];
+        attend_tile<DH>(g, Ks, Vs, N, lane, qf, [](int k) { return k & 63; }, m, l, o, stage);
         if (myq < q1) store_row<DH>((uint16_t*)a.out + (size_t)myq * D + h * DH, lane, l, o);
     }
 }
@@ -461,11 +561,12 @@ void attn_unit_k(AttnArgs a, int pcap) {
                 float m, l;
                 f32x16 o[DB];
                 if (jj < 0) {
-                    attend_tile<DH>(g, Ks, Vs, N, lane, qf, [](int k) { return k; }, m, l, o);
+                    attend_tile<DH>(g, Ks, Vs, N, lane, qf, [](int k) { return k; }, m, l, o,
+                                    [](int) {});
                 } else {
                     const uint16_t* km = kmap + jj * g.npad;
                     attend_tile<DH>(g, Ks, Vs, N, lane, qf, [=](int k) { return (int)km[k]; },
-                                    m, l, o);
+                                    m, l, o, [](int) {});
                 }
                 if (myq < q1) store_row<DH>((uint16_t*)a.out + (size_t)myq * D + h * DH, lane, l, o);
             }
@@ -635,7 +736,9 @@ size_t f32_lds_bytes(int N, int dh) {
 }
 
 template <int DH>
-void launch_bf16(const AttnArgs& a, hipStream_t s) {
+void launch_bf16(const AttnArgs& a0, hipStream_t s) {
+    AttnArgs a = a0;
+    a.tile_cut = 0;
     static bool raised = false;
     if (!raised) {  // allow more than the default dynamic LDS (gfx950 has 160 KiB per CU)
         (void)hipFuncSetAttribute((const void*)attn_mfma_k<DH>,
@@ -659,6 +762,44 @@ void launch_bf16(const AttnArgs& a, hipStream_t s) {
             }
         }
     }
+    // Reuse on without per-group blocks (head dim 64): frames with at most `cut` query tiles go
+    // to per-tile wavefronts streaming K/V (one pass over the keys per tile), the others to
+    // per-frame blocks (one staging of the keys for all tiles); of the cuts 2, 3, 4 and 5,
+    // 2 gave the shortest attention at 50, 70 and 90 % reuse (ViT-L/14, reordered groups of 8).
+    // DV_ATTN_CFG (measurements): 1 per-frame blocks only, 2 per-tile wavefronts only, also
+    // without reuse; DV_ATTN_CUT overrides the cut.
+    static int cfg = -1, cut = 2;
+    if (cfg < 0) {
+        const char* e = getenv("DV_ATTN_CFG");
+        cfg = e ? atoi(e) : 0;
+        const char* c = getenv("DV_ATTN_CUT");
+        if (c) cut = std::max(0, atoi(c));
+    }
+    if constexpr (DH == 64) {
+        if (a.G == 0 && cfg != 1 && (a.sparse || cfg == 2)) {
+            a.tile_cut = cfg == 2 ? (a.N + 31) / 32 : cut;
+            static bool wraised = false;
+            constexpr size_t wlds = (size_t)SW * WaveBuf<DH>::ELEMS * 2;
+            if (!wraised) {
+                (void)hipFuncSetAttribute((const void*)attn_wave_k<DH>,
+                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)wlds);
+                wraised = true;
+            }
+            static int wper_cu = -1;
+            if (wper_cu < 0) {
+                int v = 0;
+                if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, (const void*)attn_wave_k<DH>,
+                                                                 SW * 64, wlds) != hipSuccess)
+                    v = 0;
+                wper_cu = v;
+            }
+            const int tiles = a.F * a.H * ((a.N + 31) / 32);
+            int grid = (tiles + SW - 1) / SW;
+            if (a.cus > 0 && wper_cu > 0) grid = std::min(grid, a.cus * wper_cu);
+            hipLaunchKernelGGL(attn_wave_k<DH>, dim3(grid), dim3(SW * 64), wlds, s, a);
+            if (a.tile_cut >= (a.N + 31) / 32) return;   // no frame left for per-frame blocks
+        }
+    }
     const size_t lds = Geo(a.N, DH).bytes();
     // work items: (frame, head) pairs; with reuse, the slots of whole units on each of 8 XCDs
     const int items = a.G > 0 ? xcd_unit_grid((a.F + a.G - 1) / a.G * a.H, a.G) : a.F * a.H;
@@ -670,9 +811,13 @@ void launch_bf16(const AttnArgs& a, hipStream_t s) {
             v = 0;
         per_cu = v;
     }
-    // a multiple of 8 blocks keeps item i on XCD i % 8, as the placement of a group's items assumes
+    // a multiple of 8 blocks keeps item i on XCD i % 8, as the placement of a group's items assumes.
+    // After per-tile wavefronts took the small frames, one block per item: the frames left (I
+    // frames and others with many recomputed tokens) are spread by the dispatcher, where resident
+    // blocks striding over the items would give all of them to a few blocks.
     int grid = items;
-    if (a.cus > 0 && per_cu > 0) grid = std::min(grid, (a.cus * per_cu + 7) / 8 * 8);
+    if (a.cus > 0 && per_cu > 0 && a.tile_cut == 0)
+        grid = std::min(grid, (a.cus * per_cu + 7) / 8 * 8);
     hipLaunchKernelGGL(attn_mfma_k<DH>, dim3(grid), dim3(AW * 64), lds, s, a);
 }
 

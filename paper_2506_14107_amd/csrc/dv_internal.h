@@ -106,6 +106,9 @@ struct AttnArgs {
     int G;             // group size, 0 without reuse (block placement only)
     int cus;           // compute units of the device (0: one block per work item)
     int skip;          // leading frames carried over from an earlier call (no rows, no queries)
+    int sparse;        // reuse on with G == 0: frames hold few query tiles (per-tile wavefronts)
+    int tile_cut;      // set by launch_attention: frames with at most this many query tiles go to
+                       // per-tile wavefronts, the others to per-frame blocks
 };
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
 // Class-token attention weights of every non-reference frame (G > 0: frames f % G == 0 are
