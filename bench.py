@@ -85,8 +85,26 @@ def attn_bytes(m, Ml, F):
     return Ml * D * 2 * 2 + F * N * 2 * D * 2
 
 
+def row_stage_bytes(stage, m, Ml_prev, Ml, F):
+    """Algorithmic HBM bytes of one launch of a row kernel at layer l (Ml active rows, Ml_prev at
+    the layer before; the whole batch at the first layer).  gate: the fp32 rows of every token not
+    reused at the layer before (a token reused there holds its reference's row: cosine 1 without
+    a read; reference frames are among the rows read), its LN1 row (bf16) for every recomputed
+    token, and the map.  ln2: fp32 rows in, bf16 rows out.  compact: the map in, the packed row
+    list and every token's packed slot out."""
+    D, N = m.width, m.n_tokens
+    if stage == "gate":
+        return Ml_prev * D * 4 + Ml * D * 2 + F * N
+    if stage == "ln2":
+        return Ml * D * 4 + Ml * D * 2
+    if stage == "compact":
+        return F * N + Ml * 4 + F * N * 4 + (F + 1) * 4
+    return 0.0
+
+
 KERNEL_SOURCE = {"qkv": "gemm.hip", "oproj": "gemm.hip", "fc1": "gemm.hip", "fc2": "gemm.hip",
-                 "attn": "attention.hip"}
+                 "attn": "attention.hip", "gate": "rowops.hip", "ln2": "rowops.hip",
+                 "compact": "rowops.hip"}
 
 
 def measured_traffic(stage):
@@ -105,7 +123,8 @@ def measured_traffic(stage):
 
 
 STAGE_KERNEL = {"qkv": ("Epi)1",), "oproj": ("Epi)2",), "fc1": ("Epi)3",), "fc2": ("Epi)4",),
-                "attn": ("attn_unit_k", "attn_mfma_k")}   # name fragments of each stage's kernels
+                "attn": ("attn_unit_k", "attn_mfma_k"), "gate": ("gate_k",),
+                "ln2": ("ln_rows_k",), "compact": ("compact_k",)}   # name fragments per stage
 
 
 def traffic_record(fetch_csv, write_csv, bench_json, cmds):
@@ -404,6 +423,11 @@ def main():
     for stg in ("qkv", "oproj", "fc1", "fc2", "attn"):
         tot = sum((attn_bytes(m, Ml, F) if stg == "attn" else stage_bytes(stg, m, Ml))
                   for lv in levels for Ml in lv["Ml"]) * args.steps
+        stages[stg] = {"launches": launches_per_stage,
+                       "algo_bytes_per_launch": round(tot / launches_per_stage)}
+    for stg in ("gate", "ln2", "compact"):
+        tot = sum(row_stage_bytes(stg, m, (lv["Ml"][l - 1] if l else F * N), lv["Ml"][l], F)
+                  for lv in levels for l in range(m.depth)) * args.steps
         stages[stg] = {"launches": launches_per_stage,
                        "algo_bytes_per_launch": round(tot / launches_per_stage)}
 
