@@ -8,7 +8,8 @@ namespace dv {
 namespace {
 
 constexpr int WAVE = 64;
-constexpr int MAX_CHUNKS = 8;  // float4 chunks per lane: D <= 2048
+// float4 chunks of a row held per lane by the row kernels (template CK): 4 for D <= 1024, 8 for
+// D <= 2048
 
 // Sum over the 64 lanes, in every lane: DPP steps within rows of 16 lanes (quad swaps, then the
 // half-row and row mirrors), one LDS shuffle across rows, and the permlane32 swap across the two
@@ -70,7 +71,7 @@ __global__ void cls_init_k(float* x, const float* cls, const float* pos, int F, 
 // Under reordered referencing a frame has up to two references: the similarity is the larger
 // cosine, `src` records which reference gave it (1: the future one; a tie keeps the past one),
 // and the cosines are taken in every mode but reuse-off, since they choose the source.
-template <bool BF, bool DEC, bool REORD>
+template <bool BF, bool DEC, bool REORD, int CK>
 __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     const int N = a.N, D = a.D;
     const int chunks = (N + GATE_TOK - 1) / GATE_TOK;
@@ -137,13 +138,13 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
         const float4* xo = xf;   // the token's current row (reordered: through its root)
         int reuse = 0, from_fut = 0;
         bool loaded = false;
-        float4 v[MAX_CHUNKS];
+        float4 v[CK];
         // cosine of this token's row (loaded into v on the first call) with reference row xr
         auto cosine = [&](const float4* xr) {
             float dot = 0.f, na = 0.f, nb = 0.f;
             int eq = 1;
 #pragma unroll
-            for (int k = 0; k < MAX_CHUNKS; ++k) {
+            for (int k = 0; k < CK; ++k) {
                 const int c = lane + k * WAVE;
                 if (c < nchunk) {
                     if (!loaded) v[k] = xo[c];
@@ -176,7 +177,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
                         if (!reuse) {   // recomputed again: its row becomes the reference's
                             const float4* xr = (const float4*)(a.x + ((size_t)r * N + i) * D);
 #pragma unroll
-                            for (int k = 0; k < MAX_CHUNKS; ++k) {
+                            for (int k = 0; k < CK; ++k) {
                                 const int c = lane + k * WAVE;
                                 if (c < nchunk) {
                                     v[k] = xr[c];
@@ -219,7 +220,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
                     }
                     if (REORD && !reuse && own != f) {   // recomputed after being reused: the
 #pragma unroll                                           // token gets its root's row back
-                        for (int k = 0; k < MAX_CHUNKS; ++k) {
+                        for (int k = 0; k < CK; ++k) {
                             const int c = lane + k * WAVE;
                             if (c < nchunk) {
                                 if (!loaded) v[k] = xo[c];
@@ -235,7 +236,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
             const int rs = from_fut ? rfut : r;   // the reference that supplies the token
             const float4* xr = (const float4*)(a.x + ((size_t)rs * N + i) * D);
 #pragma unroll
-            for (int k = 0; k < MAX_CHUNKS; ++k) {
+            for (int k = 0; k < CK; ++k) {
                 const int c = lane + k * WAVE;
                 if (c < nchunk) {
                     const float4 u = loaded ? v[k] : xf[c], w = xr[c];
@@ -254,19 +255,19 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
         if (!reuse && a.ln_out) {   // recomputed: LN1 of the row into the token-indexed buffer
             if (!loaded) {
 #pragma unroll
-                for (int k = 0; k < MAX_CHUNKS; ++k) {
+                for (int k = 0; k < CK; ++k) {
                     const int c = lane + k * WAVE;
                     if (c < nchunk) v[k] = xo[c];
                 }
             }
             float sum = 0.f;
 #pragma unroll
-            for (int k = 0; k < MAX_CHUNKS; ++k)
+            for (int k = 0; k < CK; ++k)
                 if (lane + k * WAVE < nchunk) sum += (v[k].x + v[k].y) + (v[k].z + v[k].w);
             const float mean = wave_sum(sum) / (float)D;
             float sq = 0.f;
 #pragma unroll
-            for (int k = 0; k < MAX_CHUNKS; ++k) {
+            for (int k = 0; k < CK; ++k) {
                 if (lane + k * WAVE < nchunk) {
                     const float a0 = v[k].x - mean, a1 = v[k].y - mean, a2 = v[k].z - mean,
                                 a3 = v[k].w - mean;
@@ -275,7 +276,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
             }
             const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + 1e-5f);
 #pragma unroll
-            for (int k = 0; k < MAX_CHUNKS; ++k) {
+            for (int k = 0; k < CK; ++k) {
                 const int c = lane + k * WAVE;
                 if (c < nchunk) {
                     const float4 gg = g4[c], bb = b4[c];
@@ -415,7 +416,7 @@ __global__ __launch_bounds__(256) void compact_k(const uint8_t* cur, const int* 
 }
 
 // --- LayerNorm of (gathered) rows -> elem rows ------------------------------------------------
-template <bool BF>
+template <bool BF, int CK>
 __global__ __launch_bounds__(256) void ln_rows_k(const float* __restrict__ src,
                                                  const int* __restrict__ gather,
                                                  const int* __restrict__ Mdev, int Mmax, int D,
@@ -430,10 +431,10 @@ __global__ __launch_bounds__(256) void ln_rows_k(const float* __restrict__ src,
          row += gridDim.x * blockDim.x / 64) {
         const int srow = gather ? gather[row] : row;
         const float4* s4 = (const float4*)(src + (size_t)srow * D);
-        float4 v[MAX_CHUNKS];
+        float4 v[CK];
         float sum = 0.f;
 #pragma unroll
-        for (int k = 0; k < MAX_CHUNKS; ++k) {
+        for (int k = 0; k < CK; ++k) {
             const int c = lane + k * 64;
             if (c < nchunk) {
                 v[k] = s4[c];
@@ -443,7 +444,7 @@ __global__ __launch_bounds__(256) void ln_rows_k(const float* __restrict__ src,
         const float mean = wave_sum(sum) / (float)D;
         float sq = 0.f;
 #pragma unroll
-        for (int k = 0; k < MAX_CHUNKS; ++k) {
+        for (int k = 0; k < CK; ++k) {
             const int c = lane + k * 64;
             if (c < nchunk) {
                 const float a0 = v[k].x - mean, a1 = v[k].y - mean, a2 = v[k].z - mean,
@@ -453,7 +454,7 @@ __global__ __launch_bounds__(256) void ln_rows_k(const float* __restrict__ src,
         }
         const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + 1e-5f);
 #pragma unroll
-        for (int k = 0; k < MAX_CHUNKS; ++k) {
+        for (int k = 0; k < CK; ++k) {
             const int c = lane + k * 64;
             if (c < nchunk) {
                 const float4 gg = g4[c], bb = b4[c];
@@ -651,15 +652,28 @@ void launch_gate(bool bf16, const GateArgs& a, hipStream_t s) {
     const dim3 grid(a.F * gate_chunks(a.N)), block(256);
     const bool dec = a.dec != nullptr && a.mode == GATE_COS;
     const int v = (bf16 ? 4 : 0) + (dec ? 2 : 0) + (a.reorder ? 1 : 0);
+    if (a.D <= 1024) {   // at most 4 float4 chunks per lane: half the registers, twice the waves
+        switch (v) {
+            case 0: hipLaunchKernelGGL((gate_k<false, false, false, 4>), grid, block, 0, s, a); break;
+            case 1: hipLaunchKernelGGL((gate_k<false, false, true, 4>), grid, block, 0, s, a); break;
+            case 2: hipLaunchKernelGGL((gate_k<false, true, false, 4>), grid, block, 0, s, a); break;
+            case 3: hipLaunchKernelGGL((gate_k<false, true, true, 4>), grid, block, 0, s, a); break;
+            case 4: hipLaunchKernelGGL((gate_k<true, false, false, 4>), grid, block, 0, s, a); break;
+            case 5: hipLaunchKernelGGL((gate_k<true, false, true, 4>), grid, block, 0, s, a); break;
+            case 6: hipLaunchKernelGGL((gate_k<true, true, false, 4>), grid, block, 0, s, a); break;
+            default: hipLaunchKernelGGL((gate_k<true, true, true, 4>), grid, block, 0, s, a); break;
+        }
+        return;
+    }
     switch (v) {
-        case 0: hipLaunchKernelGGL((gate_k<false, false, false>), grid, block, 0, s, a); break;
-        case 1: hipLaunchKernelGGL((gate_k<false, false, true>), grid, block, 0, s, a); break;
-        case 2: hipLaunchKernelGGL((gate_k<false, true, false>), grid, block, 0, s, a); break;
-        case 3: hipLaunchKernelGGL((gate_k<false, true, true>), grid, block, 0, s, a); break;
-        case 4: hipLaunchKernelGGL((gate_k<true, false, false>), grid, block, 0, s, a); break;
-        case 5: hipLaunchKernelGGL((gate_k<true, false, true>), grid, block, 0, s, a); break;
-        case 6: hipLaunchKernelGGL((gate_k<true, true, false>), grid, block, 0, s, a); break;
-        default: hipLaunchKernelGGL((gate_k<true, true, true>), grid, block, 0, s, a); break;
+        case 0: hipLaunchKernelGGL((gate_k<false, false, false, 8>), grid, block, 0, s, a); break;
+        case 1: hipLaunchKernelGGL((gate_k<false, false, true, 8>), grid, block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((gate_k<false, true, false, 8>), grid, block, 0, s, a); break;
+        case 3: hipLaunchKernelGGL((gate_k<false, true, true, 8>), grid, block, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((gate_k<true, false, false, 8>), grid, block, 0, s, a); break;
+        case 5: hipLaunchKernelGGL((gate_k<true, false, true, 8>), grid, block, 0, s, a); break;
+        case 6: hipLaunchKernelGGL((gate_k<true, true, false, 8>), grid, block, 0, s, a); break;
+        default: hipLaunchKernelGGL((gate_k<true, true, true, 8>), grid, block, 0, s, a); break;
     }
 }
 
@@ -700,12 +714,10 @@ void launch_copy_rows(const float* x, const int* root, int f, int N, int D, floa
 void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* Mdev, int Mmax,
                     int D, const float* g, const float* b, void* dst, hipStream_t s) {
     const int grid = grid_for((size_t)Mmax, 4, 65536);
-    if (bf16)
-        hipLaunchKernelGGL(ln_rows_k<true>, dim3(grid), dim3(256), 0, s, src, gather, Mdev, Mmax,
-                           D, g, b, dst);
-    else
-        hipLaunchKernelGGL(ln_rows_k<false>, dim3(grid), dim3(256), 0, s, src, gather, Mdev, Mmax,
-                           D, g, b, dst);
+    // rows of at most 1024 values: 4 float4 chunks per lane in registers, else up to 8
+    auto k = bf16 ? (D <= 1024 ? ln_rows_k<true, 4> : ln_rows_k<true, 8>)
+                  : (D <= 1024 ? ln_rows_k<false, 4> : ln_rows_k<false, 8>);
+    hipLaunchKernelGGL(k, dim3(grid), dim3(256), 0, s, src, gather, Mdev, Mmax, D, g, b, dst);
 }
 
 void launch_merge(float* x, const uint8_t* cur, const int* root, int F, int N, int D, int G,
