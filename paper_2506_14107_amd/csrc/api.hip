@@ -27,7 +27,9 @@
 //    call's first batch starts with that reference as local frame 0 (rows copied from the
 //    cache, not recomputed), then gap frames standing for the group's frames of earlier calls,
 //    then the call's own frames, so that groups keep their positions (frame f's reference is
-//    frame G * floor(f / G) of the batch).]
+//    frame G * floor(f / G) of the batch).  Reordered: the frames after the last anchor are
+//    held until it arrives; a batch starts at a group boundary with gap frames up to the cached
+//    anchor (their last), then the held and new frames, and ends on an anchor, which is cached.]
 //   final LayerNorm of the class tokens.
 // Nothing is read back to the host inside an encode call.
 //

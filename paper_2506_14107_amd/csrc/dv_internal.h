@@ -149,9 +149,10 @@ struct GateArgs {
     uint8_t* src;         // [F*N] reordered: 1 where the future reference supplies the token
     const int* root;      // [F*N] reordered: the previous layer's root map (nullptr: every token
                           // holds its own row); a recomputed token gets its root's row copied in
-    int skip;             // leading frames carried over from an earlier call of a stream: frame 0
-                          // is the cached reference (its rows already in x), the others gaps;
-                          // none is gated, and inj / out_masks start at frame skip
+    int skip;             // leading frames carried over from an earlier call of a stream: one is
+                          // the cached reference (the first in the star, the last under
+                          // reordering; its rows already in x), the others gaps; none is gated,
+                          // and inj / out_masks start at frame skip
 };
 // Reordering with restoration: a reused row is built along its chain of sources; a group of G
 // frames has chains of at most G/4 + 1 reused links (B_dist1, B_dist2, then the P frames back
