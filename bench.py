@@ -244,6 +244,10 @@ def main():
                          "threshold on its output is calibrated like tau)")
     ap.add_argument("--reorder", action="store_true",
                     help="reordered I/P/B referencing with past and future references")
+    ap.add_argument("--streams", type=int, default=1,
+                    help="with --stream-chunk: this many independent streams, one handle and one "
+                         "HIP stream each, every one encoding the whole batch; calls are issued "
+                         "round-robin (frames/s count all streams' frames; no roofline)")
     ap.add_argument("--stream-chunk", type=int, default=0,
                     help="deliver each batch to the timed encodes as a stream of calls of this "
                          "many frames (dv_stream_encode; groups span calls; a reordered stream "
@@ -334,8 +338,29 @@ def main():
     dominant = max(prof, key=lambda s: prof[s][0])
     log("[bench] stage ms per sweep: " + ", ".join(f"{k} {v[0]:.2f}" for k, v in prof.items() if v[1]))
 
+    S = max(1, args.streams) if args.stream_chunk else 1
+    if S > 1:   # small handles: one call's frames plus a group of carried-over frames
+        encs = [Encoder(m, blob, min(F, args.stream_chunk + G)) for _ in range(S)]
+        hs = [torch.cuda.Stream() for _ in range(S)]
+
     def encode_all(tau):
-        """One encode of the batch: one call, or a stream of calls of --stream-chunk frames."""
+        """One encode of the batch: one call, or a stream of calls of --stream-chunk frames (of
+        --streams concurrent streams)."""
+        if S > 1:
+            cur = torch.cuda.current_stream()
+            for e, st in zip(encs, hs):
+                st.wait_stream(cur)
+                e.stream_reset()
+            for k in range(0, F, args.stream_chunk):
+                for e, st in zip(encs, hs):
+                    with torch.cuda.stream(st):
+                        e.stream_encode(x[k:k + args.stream_chunk], G, tau, want_masks=False,
+                                        stream=st)
+            for e, st in zip(encs, hs):
+                with torch.cuda.stream(st):
+                    e.stream_flush(want_masks=False, stream=st)
+                cur.wait_stream(st)
+            return
         if not args.stream_chunk:
             enc.encode(x, G, tau, want_masks=False)
             return
@@ -369,19 +394,22 @@ def main():
     per_level = []
     for lv in levels:
         ms, _ = time_calls([lv["tau"]], max(2, args.steps), 1)
-        per_level.append(F * max(2, args.steps) / ms * 1e3)
+        per_level.append(S * F * max(2, args.steps) / ms * 1e3)
     dense_ms, _ = time_calls([float("-inf")], max(2, args.steps), 1)
-    dense_fps = F * max(2, args.steps) / dense_ms * 1e3
+    dense_fps = S * F * max(2, args.steps) / dense_ms * 1e3
 
     # the timed region: K steps of the whole sweep, dominant stage timed with HIP events
-    total_ms, st = time_calls(taus, args.steps, args.warmup, profile_stage=dominant)
-    frames_done = F * len(taus) * args.steps
+    total_ms, st = time_calls(taus, args.steps, args.warmup,
+                              profile_stage=dominant if S == 1 else None)
+    frames_done = S * F * len(taus) * args.steps
     value = frames_done / total_ms * 1e3
 
     # roofline of the dominant kernel
     flops = args.steps * sum(stage_flops(dominant, m, Ml) for lv in levels for Ml in lv["Ml"])
-    stage_ms, launches = st
-    if flops > 0:
+    stage_ms, launches = st if st is not None else (0.0, 0)
+    if S > 1:   # concurrent streams: no single kernel's launches to time
+        roof = None
+    elif flops > 0:
         achieved = flops / (stage_ms * 1e-3) / 1e12
         peak = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_FP32_TFLOPS
         algo_b = args.steps * sum(stage_bytes(dominant, m, Ml) for lv in levels for Ml in lv["Ml"])
@@ -452,9 +480,11 @@ def main():
                                   if m.reorder else "")
                                + (f"streamed in calls of {args.stream_chunk} frames; "
                                   if args.stream_chunk else "")
+                               + (f"{S} concurrent streams (one handle and HIP stream each, "
+                                  f"each encoding the batch); " if S > 1 else "")
                                + "reuse levels "
                                + "/".join(f"{t:.0%}" for t in targets if t is not None),
-                   "frames_per_step": F * len(taus), "group_size": G},
+                   "frames_per_step": S * F * len(taus), "group_size": G},
         "sweep": sweep,
         "dense_frames_per_s": round(dense_fps, 1),
         "roofline": roof,
