@@ -151,3 +151,31 @@ def test_full_size_reordered_referencing():
               f"{r_t:.2e}", flush=True)
         assert bad == 0 and bad_src == 0
     enc.close()
+
+
+@pytest.mark.parametrize("reorder", [False, True], ids=["star", "reordered"])
+def test_full_size_stream_equals_one_shot(reorder):
+    """ViT-L/14 (257 tokens, head dim 64) delivered as a stream of uneven calls: bit-equal to one
+    encode over all frames, so the stream path (carried-over reference, held frames, per-tile
+    attention) meets the bar the one-shot parity tests establish."""
+    torch = require_gpu()
+    w = synth.get_config("vit_l14")
+    m, G = dataclasses.replace(w.model, reorder=reorder), w.group_size
+    tau = float(np.float32(0.93))
+    blob = synth.make_blob(m, w.weight_seed)
+    F = 45
+    fr = synth.render_frames(w.video, m.image_size, 0, F)
+    want = encoder(m, blob, 32).encode(dev(fr), G, tau, want_tokens=True)
+    enc = encoder(m, blob, 32)
+    outs, k = [], 0
+    for c in (13, 7, 1, 20, 4):
+        outs.append(enc.stream_encode(dev(fr[k:k + c]), G, tau, want_tokens=True))
+        k += c
+    outs.append(enc.stream_flush(want_tokens=True))
+    torch.cuda.synchronize()
+    assert k == F
+    for j, what in enumerate(("embeddings", "masks", "tokens")):
+        got = np.concatenate([host(o[j]) for o in outs if o[0].shape[0]])
+        assert np.array_equal(got, host(want[j])), f"{what} differ from one encode"
+    rho = oracle.reuse_rate(host(want[1]), G)
+    assert 0.05 < rho < 0.99, f"threshold gives degenerate reuse {rho}"
