@@ -441,8 +441,9 @@ constexpr size_t pipe_lds_bytes() {
     return ring > slabs ? ring : slabs;
 }
 
-// Tail tiles of a split launch: 64 x 64, 3-stage ring, one per group of four wavefronts.
-constexpr int TBM = 64, TBN = 64, TS = 3;
+// Tail tiles of a split launch: 64 x 64, 8-stage ring (seven k-slices in flight: a tail tile is
+// bound by the latency of its k-loop), one per group of four wavefronts.
+constexpr int TBM = 64, TBN = 64, TS = 8;
 constexpr size_t TAIL_LDS = pipe_lds_bytes<TBM, TBN, 32, TS, 2, 2>();
 
 // Block tiles BM x BN of WGM x WGN wavefronts.  With a.slots set, the launch is split: blocks
