@@ -441,10 +441,11 @@ constexpr size_t pipe_lds_bytes() {
     return ring > slabs ? ring : slabs;
 }
 
-// Tail tiles of a split launch: 64 x 64, 8-stage ring (seven k-slices in flight: a tail tile is
-// bound by the latency of its k-loop), one per group of four wavefronts.
-constexpr int TBM = 64, TBN = 64, TS = 8;
-constexpr size_t TAIL_LDS = pipe_lds_bytes<TBM, TBN, 32, TS, 2, 2>();
+// Tail tiles of a split launch: 64 x 64, 64-deep k-slices in a 4-stage ring (three in flight: a
+// tail tile is bound by the latency of its k-loop, so few barriers and deep prefetch pay; 32-deep
+// slices in 3 or 8 stages measured slower), one per group of four wavefronts.
+constexpr int TBM = 64, TBN = 64, TBK = 64, TS = 4;
+constexpr size_t TAIL_LDS = pipe_lds_bytes<TBM, TBN, TBK, TS, 2, 2>();
 
 // Block tiles BM x BN of WGM x WGN wavefronts.  With a.slots set, the launch is split: blocks
 // below a.head_grid take the rows [0, head) that fill whole rounds of the grid
@@ -469,7 +470,7 @@ void gemm_bf16_pipe_k(GemmArgs a) {
     static_assert(NW % 4 == 0, "tail tiles take groups of four wavefronts");
     const int grp = wave / 4;
     const int tb = ((int)blockIdx.x - a.head_grid) * (NW / 4) + grp;
-    pipe_tile<E, TBM, TBN, 32, TS, 2, 2>(a, (uint16_t*)(smem + grp * TAIL_LDS), tb, head, M,
+    pipe_tile<E, TBM, TBN, TBK, TS, 2, 2>(a, (uint16_t*)(smem + grp * TAIL_LDS), tb, head, M,
                                          wave % 4);
 }
 
