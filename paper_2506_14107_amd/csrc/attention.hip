@@ -225,6 +225,125 @@ __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, co
     }
 }
 
+// attend_tile for up to NQ query tiles of one frame at once (nq of them present): every step's
+// keys and values are staged once for all of them; each tile's arithmetic, in its order, is
+// attend_tile's, so its results are the same bit for bit.
+template <int DH, int NQ, class KRow, class Stage>
+__device__ __forceinline__ void attend_tiles(const Geo& g, const uint16_t* Ks, const uint16_t* Vs,
+                                             int N, int lane, const bf16x8 (&qf)[NQ][DH / 16],
+                                             int nq, KRow krow, float (&m)[NQ], float (&l)[NQ],
+                                             f32x16 (&o)[NQ][(DH + 31) / 32], Stage stage) {
+    constexpr int KS = DH / 16;          // k-steps of S^T
+    constexpr int DB = (DH + 31) / 32;   // 32-row blocks of O^T
+    const int hl = lane >> 5, lr = lane & 31;
+    const float sl2 = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(dh)
+    const int nkb = g.npad / 32;
+    const int grp = lane >> 4, gi = lane & 15;    // 16-lane group of the transposing read
+    const int tr_key = hl * 4 + (gi >> 2);
+    const int tr_dim = (grp & 1) * 16 + (gi & 3) * 4;
+
+    // scores of key block kb against the query tile (raw, unscaled)
+    auto scores = [&](int q, int kb) {
+        f32x16 sc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[r] = 0.f;
+        const int row = krow(kb * 32 + lr);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8 kf = *(const bf16x8*)(Ks + g.kofs(row, ks * 2 + hl));
+            sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[q][ks], sc, 0, 0, 0);
+        }
+        if ((kb + 1) * 32 > N) {   // ragged last block: keys past N get -inf
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int key = kb * 32 + (r >> 2) * 8 + hl * 4 + (r & 3);
+                sc[r] = key < N ? sc[r] : -INFINITY;
+            }
+        }
+        return sc;
+    };
+    // O^T += V^T(kb) . P^T(kb)
+    auto accumulate = [&](int q, int kb, const bf16x8 (&pf)[2]) {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            // lane (group grp, index gi) names key kb*32 + ks*16 + hl*4 + gi/4 (+8) and dims
+            // b*32 + (grp&1)*16 + 4*(gi%4); it receives dim b*32 + (grp&1)*16 + gi of the 4
+            // keys named by lanes 4e + gi/4 of its group
+            const int key = kb * 32 + ks * 16 + tr_key;
+            const int r0 = krow(key), r1 = krow(key + 8);
+#pragma unroll
+            for (int b = 0; b < DB; ++b) {
+                int d = b * 32 + tr_dim;
+                d = d < DH ? d : DH - 4;   // head dims past DH: any finite row data
+                const uint16_t* p0 = Vs + g.vofs(r0, d >> 3) + (d & 7);
+                const uint16_t* p1 = Vs + g.vofs(r1, d >> 3) + (d & 7);
+                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4*)p0);
+                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4*)p1);
+                const s16x4 both[2] = {lo, hi};
+                const bf16x8 vf = __builtin_bit_cast(bf16x8, both);
+                o[q][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[q][b], 0, 0, 0);
+            }
+        }
+    };
+
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+#pragma unroll
+        for (int b = 0; b < DB; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) o[q][b][r] = 0.f;
+        m[q] = -INFINITY;
+        l[q] = 0.f;
+    }
+    for (int kb = 0; kb < nkb; kb += 2) {
+        stage(kb);
+        const int kb1 = kb + 1;
+        const bool two = kb1 < nkb;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            if (q >= nq) break;   // wave-uniform: the tile does not exist
+            const f32x16 s0 = scores(q, kb);
+            f32x16 s1;
+            if (two) {
+                s1 = scores(q, kb1);
+            } else {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) s1[r] = -INFINITY;
+            }
+            float bm = -INFINITY;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) bm = fmaxf(bm, fmaxf(s0[r], s1[r]));
+            bm = fmaxf(bm, other_half(bm));
+            if (__any(bm > m[q])) {   // rescale only when some lane's running max moved
+                const float mn = fmaxf(m[q], bm);
+                const float alpha = __builtin_amdgcn_exp2f((m[q] - mn) * sl2);
+                l[q] *= alpha;
+#pragma unroll
+                for (int b = 0; b < DB; ++b)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) o[q][b][r] *= alpha;
+                m[q] = mn;
+            }
+            const float nm = -m[q] * sl2;
+            float ps = 0.f;
+            bf16x8 p0[2], p1[2];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], sl2, nm));
+                const float e1 = __builtin_amdgcn_exp2f(fmaf(s1[r], sl2, nm));
+                ps += e0 + e1;
+                p0[r >> 3][r & 7] = (__bf16)e0;
+                p1[r >> 3][r & 7] = (__bf16)e1;
+            }
+            l[q] += ps + other_half(ps);
+            accumulate(q, kb, p0);
+            if (two) accumulate(q, kb1, p1);
+        }
+    }
+}
+
 // o / l of a lane's query as bf16 to its output row (dims of this lane's register groups)
 template <int DH>
 __device__ __forceinline__ void store_row(uint16_t* dst, int lane, float l,
@@ -364,8 +483,9 @@ struct WaveBuf {   // 64 rows of K and 64 of V, with Geo's strides
     static constexpr size_t ELEMS = (size_t)64 * (LDK + LDV);
 };
 
-template <int DH>
-__global__ __launch_bounds__(SW * 64) void attn_wave_k(AttnArgs a) {
+template <int DH, int NQ>
+__global__ __launch_bounds__(SW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_wave_k(AttnArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     constexpr int KS = DH / 16;
     constexpr int DB = (DH + 31) / 32;
@@ -384,13 +504,15 @@ __global__ __launch_bounds__(SW * 64) void attn_wave_k(AttnArgs a) {
                                           0x00020000);
     static_assert(DH == 64, "rows of 8 16-byte slots, K and V alike");
     constexpr int KI = 8;   // copy instructions per step for K, and as many for V
-    const int tmax = (N + 31) / 32;
+    // an item is NQ consecutive query tiles of a frame, t .. t + nq - 1
+    const int tmax = ((N + 31) / 32 + NQ - 1) / NQ;
     const int items = a.F * a.H * tmax;
     for (int item = blockIdx.x * SW + wave; item < items; item += gridDim.x * SW) {
-        const int t = item % tmax, fh = item / tmax;
+        const int t = item % tmax * NQ, fh = item / tmax;
         const int f = fh / a.H, h = fh % a.H;
         const int q0 = a.qoff[f], q1 = a.qoff[f + 1];
         if (t * 32 >= q1 - q0 || q1 - q0 > a.tile_cut * 32) continue;   // none, or a per-frame block
+        const int nq = min(NQ, (q1 - q0 + 31) / 32 - t);
         const int* pf = a.pos + (size_t)f * N;
         const uint32_t hoff = (uint32_t)(h * DH) * 2;
         // Lane l fetches row r = u*8 + l/8 of instruction u, slot l%8 (K and V rows have the same
@@ -427,16 +549,25 @@ __global__ __launch_bounds__(SW * 64) void attn_wave_k(AttnArgs a) {
 #pragma unroll
             for (int u = 0; u < KI; ++u) prow[u] = next[u];
         };
-        const int myq = q0 + t * 32 + lr;
-        const int qrow = myq < q1 ? myq : q1 - 1;   // tail lanes compute on a valid row
-        bf16x8 qf[KS];
+        bf16x8 qf[NQ][KS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            qf[ks] = *(const bf16x8*)(qkv + (size_t)qrow * ld3 + h * DH + ks * 16 + hl * 8);
-        float m, l;
-        f32x16 o[DB];
-        attend_tile<DH>(g, Ks, Vs, N, lane, qf, [](int k) { return k & 63; }, m, l, o, stage);
-        if (myq < q1) store_row<DH>((uint16_t*)a.out + (size_t)myq * D + h * DH, lane, l, o);
+        for (int q = 0; q < NQ; ++q) {
+            const int myq = q0 + (t + q) * 32 + lr;
+            const int qrow = myq < q1 ? myq : q1 - 1;   // tail lanes compute on a valid row
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                qf[q][ks] = *(const bf16x8*)(qkv + (size_t)qrow * ld3 + h * DH + ks * 16 + hl * 8);
+        }
+        float m[NQ], l[NQ];
+        f32x16 o[NQ][DB];
+        attend_tiles<DH, NQ>(g, Ks, Vs, N, lane, qf, nq, [](int k) { return k & 63; }, m, l, o,
+                             stage);
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int myq = q0 + (t + q) * 32 + lr;
+            if (q < nq && myq < q1)
+                store_row<DH>((uint16_t*)a.out + (size_t)myq * D + h * DH, lane, l[q], o[q]);
+        }
     }
 }
 
@@ -735,6 +866,25 @@ size_t f32_lds_bytes(int N, int dh) {
     return ((size_t)N * (dh + 1) + (size_t)N * dh + (size_t)NWAVE * dh + (size_t)NWAVE * N) * 4;
 }
 
+template <int DH, int NQ>
+void launch_wave(const AttnArgs& a, hipStream_t s) {
+    constexpr size_t lds = (size_t)SW * WaveBuf<DH>::ELEMS * 2;
+    static int per_cu = -1;
+    if (per_cu < 0) {
+        (void)hipFuncSetAttribute((const void*)attn_wave_k<DH, NQ>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        int v = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, (const void*)attn_wave_k<DH, NQ>,
+                                                         SW * 64, lds) != hipSuccess)
+            v = 0;
+        per_cu = v;
+    }
+    const int items = a.F * a.H * (((a.N + 31) / 32 + NQ - 1) / NQ);
+    int grid = (items + SW - 1) / SW;
+    if (a.cus > 0 && per_cu > 0) grid = std::min(grid, a.cus * per_cu);
+    hipLaunchKernelGGL((attn_wave_k<DH, NQ>), dim3(grid), dim3(SW * 64), lds, s, a);
+}
+
 template <int DH>
 void launch_bf16(const AttnArgs& a0, hipStream_t s) {
     AttnArgs a = a0;
@@ -766,37 +916,25 @@ void launch_bf16(const AttnArgs& a0, hipStream_t s) {
     // to per-tile wavefronts streaming K/V (one pass over the keys per tile), the others to
     // per-frame blocks (one staging of the keys for all tiles); of the cuts 2, 3, 4 and 5,
     // 2 gave the shortest attention at 50, 70 and 90 % reuse (ViT-L/14, reordered groups of 8).
-    // DV_ATTN_CFG (measurements): 1 per-frame blocks only, 2 per-tile wavefronts only, also
-    // without reuse; DV_ATTN_CUT overrides the cut.
-    static int cfg = -1, cut = 2;
+    // A wavefront takes two consecutive tiles of a frame at a time, so that a two-tile frame
+    // streams its keys once (attention 3.73 / 3.57 / 2.57 ms against 3.75 / 3.67 / 2.70 with
+    // one tile per wavefront).  DV_ATTN_CFG (measurements): 1 per-frame blocks only, 2 per-tile
+    // wavefronts only, also without reuse; DV_ATTN_CUT overrides the cut, DV_ATTN_PAIR=0 takes
+    // one tile per wavefront.
+    static int cfg = -1, cut = 2, pair = 1;
     if (cfg < 0) {
         const char* e = getenv("DV_ATTN_CFG");
         cfg = e ? atoi(e) : 0;
         const char* c = getenv("DV_ATTN_CUT");
         if (c) cut = std::max(0, atoi(c));
+        const char* pp = getenv("DV_ATTN_PAIR");
+        if (pp) pair = atoi(pp);
     }
     if constexpr (DH == 64) {
         if (a.G == 0 && cfg != 1 && (a.sparse || cfg == 2)) {
             a.tile_cut = cfg == 2 ? (a.N + 31) / 32 : cut;
-            static bool wraised = false;
-            constexpr size_t wlds = (size_t)SW * WaveBuf<DH>::ELEMS * 2;
-            if (!wraised) {
-                (void)hipFuncSetAttribute((const void*)attn_wave_k<DH>,
-                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)wlds);
-                wraised = true;
-            }
-            static int wper_cu = -1;
-            if (wper_cu < 0) {
-                int v = 0;
-                if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, (const void*)attn_wave_k<DH>,
-                                                                 SW * 64, wlds) != hipSuccess)
-                    v = 0;
-                wper_cu = v;
-            }
-            const int tiles = a.F * a.H * ((a.N + 31) / 32);
-            int grid = (tiles + SW - 1) / SW;
-            if (a.cus > 0 && wper_cu > 0) grid = std::min(grid, a.cus * wper_cu);
-            hipLaunchKernelGGL(attn_wave_k<DH>, dim3(grid), dim3(SW * 64), wlds, s, a);
+            if (pair) launch_wave<DH, 2>(a, s);
+            else launch_wave<DH, 1>(a, s);
             if (a.tile_cut >= (a.N + 31) / 32) return;   // no frame left for per-frame blocks
         }
     }
