@@ -202,7 +202,10 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
                     }
                     float cs = own == rp ? 1.0f
                                          : cosine((const float4*)(a.x + ((size_t)rp * N + i) * D));
-                    if (REORD && rfut >= 0) {   // the better of the two references
+                    // the better of the two references; a past cosine of exactly 1 (the same
+                    // root) already wins, a tie going to the past one, so the future one is
+                    // not needed
+                    if (REORD && rfut >= 0 && own != rp) {
                         const float c2 =
                             own == rq ? 1.0f
                                       : cosine((const float4*)(a.x + ((size_t)rq * N + i) * D));
