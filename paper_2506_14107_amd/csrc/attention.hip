@@ -107,7 +107,7 @@ __device__ inline float other_half(float x) {
 }
 
 constexpr int AW = 8;    // wavefronts of a per-frame attention block
-constexpr int UW = 16;   // wavefronts of a per-unit attention block
+constexpr int UW = 12;   // wavefronts of a per-unit attention block
 
 // Online-softmax attention of one query tile (fragments qf, one query per lane) against the
 // staged K/V: key blocks taken two at a time in order (kb, kb + 1) -- two independent MFMA
@@ -628,7 +628,7 @@ __device__ __forceinline__ void stage_rows(const Geo& g, uint16_t* Ks, uint16_t*
 }
 
 template <int DH>
-__global__ __launch_bounds__(UW * 64) __attribute__((amdgpu_waves_per_eu(4, 4)))
+__global__ __launch_bounds__(UW * 64) __attribute__((amdgpu_waves_per_eu(3, 3)))
 void attn_unit_k(AttnArgs a, int pcap) {
     constexpr int KS = DH / 16;
     constexpr int DB = (DH + 31) / 32;
