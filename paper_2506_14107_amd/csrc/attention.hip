@@ -1,10 +1,13 @@
 // Attention over mixed fresh and reference K/V.
 //
-// One block per (frame f, head h).  The block stages the frame's N keys and values of
-// head h in LDS, reading each key row through pos[]: a recomputed token's own packed row,
-// or -- for a reused token -- the packed row of the same token of the reference frame.
+// Per-frame kernel: one block per (frame f, head h).  The block stages the frame's N keys and
+// values of head h in LDS, reading each key row through pos[]: a recomputed token's own packed
+// row, or -- for a reused token -- the packed row of the same token of the reference frame.
 // The frame's packed query rows qoff[f] .. qoff[f+1] are cut into tiles of 32 that the
-// block's wavefronts take in turn.
+// block's wavefronts take in turn.  Per-unit kernel (star groups): the reference's keys are
+// staged once for all frames of a group.  Per-tile kernel (reuse without groups: reordering,
+// stream calls): a wavefront takes one or two query tiles of a frame and streams the keys
+// through its own LDS buffer.
 //
 // bf16 path (MFMA 32x32x16, fp32 accumulate), every quantity kept with one query per lane:
 //   S^T = K . Q^T      A = K rows from LDS, B = the query tile (registers); lane l holds the
