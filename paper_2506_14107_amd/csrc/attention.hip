@@ -803,14 +803,26 @@ __global__ __launch_bounds__(256) void cls_attn_k(AttnArgs a, float* __restrict_
         }
     const float scale = 1.0f / sqrtf((float)dh);
     typedef typename std::conditional<BF, uint4, float4>::type chunk_t;
+    // key rows' packed indices of the steps at j0, loaded one iteration ahead so that an
+    // iteration waits for one memory round trip (the key rows), not two
+    int pr[KB];
+    auto rows_at = [&](int j0, int (&dst)[KB]) {
+#pragma unroll
+        for (int t = 0; t < KB; ++t) {
+            const int j = j0 + 8 * t + kq;
+            dst[t] = j < N ? a.pos[(size_t)f * N + j] : 0;
+        }
+    };
+    rows_at(0, pr);
     for (int j0 = 0; j0 < N; j0 += 8 * KB) {
         // KB steps of eight keys at once: every row offset, then every chunk, then the sums
         size_t kr[KB];
 #pragma unroll
         for (int t = 0; t < KB; ++t) {
             const int j = j0 + 8 * t + kq;
-            kr[t] = j < N ? (size_t)a.pos[(size_t)f * N + j] * ld3 + D + (size_t)h * dh : 0;
+            kr[t] = j < N ? (size_t)pr[t] * ld3 + D + (size_t)h * dh : 0;
         }
+        if (j0 + 8 * KB < N) rows_at(j0 + 8 * KB, pr);
         chunk_t kv[KB][U];
 #pragma unroll
         for (int t = 0; t < KB; ++t)
