@@ -132,7 +132,17 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     };
     int active = 0;
     const int i_end = min(N, (ch + 1) * GATE_TOK);
-    for (int i = ch * GATE_TOK + wave; i < i_end; i += nwaves) {
+    // the previous layer's map for all of this wavefront's tokens, loaded together up front
+    // (blocks of 256 threads: GATE_TOK / 4 tokens per wavefront)
+    constexpr int TPW = GATE_TOK / 4;
+    uint8_t pv[TPW];
+#pragma unroll
+    for (int k = 0; k < TPW; ++k) {
+        const int i = ch * GATE_TOK + wave + k * nwaves;
+        pv[k] = (a.prev && i < i_end) ? a.prev[(size_t)f * N + i] : 0;
+    }
+    int k = 0;
+    for (int i = ch * GATE_TOK + wave; i < i_end; i += nwaves, ++k) {
         const size_t row = (size_t)f * N + i;
         float4* xf = (float4*)(a.x + row * D);
         const float4* xo = xf;   // the token's current row (reordered: through its root)
@@ -170,7 +180,7 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
             } else if (a.mode == GATE_ALL && !REORD) {
                 reuse = 1;
             } else if (a.mode != GATE_NONE) {
-                if (a.prev && a.prev[row]) {
+                if (a.prev && pv[k]) {
                     // a reused token stands for the reference's row: cosine exactly 1
                     if constexpr (DEC) {
                         reuse = decision(1.0f, i) > a.tau;
