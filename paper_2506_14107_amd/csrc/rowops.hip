@@ -136,10 +136,20 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
     // (blocks of 256 threads: GATE_TOK / 4 tokens per wavefront)
     constexpr int TPW = GATE_TOK / 4;
     uint8_t pv[TPW];
+    int own_k[TPW], rp_k[TPW], rq_k[TPW];   // reordered: the tokens' roots and their anchors'
 #pragma unroll
     for (int k = 0; k < TPW; ++k) {
         const int i = ch * GATE_TOK + wave + k * nwaves;
-        pv[k] = (a.prev && i < i_end) ? a.prev[(size_t)f * N + i] : 0;
+        const bool in = i < i_end;
+        pv[k] = (a.prev && in) ? a.prev[(size_t)f * N + i] : 0;
+        own_k[k] = f;
+        rp_k[k] = r;
+        rq_k[k] = rfut;
+        if (REORD && a.root && in && r >= 0) {
+            own_k[k] = a.root[(size_t)f * N + i];
+            rp_k[k] = a.root[(size_t)r * N + i];
+            if (rfut >= 0) rq_k[k] = a.root[(size_t)rfut * N + i];
+        }
     }
     int k = 0;
     for (int i = ch * GATE_TOK + wave; i < i_end; i += nwaves, ++k) {
@@ -203,13 +213,8 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
                     // reordered: rows are read through the previous layer's roots (a token reused
                     // there is the row of the frame that recomputed it); one root, one row, and
                     // a cosine of exactly 1 without reading it
-                    int own = f, rp = r, rq = rfut;
-                    if (REORD && a.root) {
-                        own = a.root[row];
-                        rp = a.root[(size_t)r * N + i];
-                        if (rfut >= 0) rq = a.root[(size_t)rfut * N + i];
-                        xo = (const float4*)(a.x + ((size_t)own * N + i) * D);
-                    }
+                    const int own = own_k[k], rp = rp_k[k], rq = rq_k[k];
+                    if (REORD && a.root) xo = (const float4*)(a.x + ((size_t)own * N + i) * D);
                     float cs = own == rp ? 1.0f
                                          : cosine((const float4*)(a.x + ((size_t)rp * N + i) * D));
                     // the better of the two references; a past cosine of exactly 1 (the same
