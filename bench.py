@@ -205,8 +205,10 @@ def calibrate(enc, x, G, target, iters=24, lo=-1.0, hi=1.0):
     return best
 
 
-def cpu_baseline(w, blob, frames, taus, groups_per_level=2, budget_s=30.0):
-    """The CPU oracle (fp64) on whole groups of the same frames, two groups per reuse level."""
+def cpu_baseline(w, blob, frames, taus, groups_per_level=2):
+    """The CPU oracle on whole groups of the same frames: fp64 at each level's threshold
+    (`groups_per_level` groups per level), its fp32 variant (one group per level) and reuse off
+    (tau = -inf, fp64, two groups)."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -214,20 +216,59 @@ def cpu_baseline(w, blob, frames, taus, groups_per_level=2, budget_s=30.0):
     except Exception:
         threads = len(os.sched_getaffinity(0))
     G = w.group_size
-    done, t0 = 0, time.time()
     ngroups = frames.shape[0] // G
-    for k, tau in enumerate(taus):
-        for gsel in range(groups_per_level):
-            g0 = ((k * groups_per_level + gsel) % ngroups) * G
-            oracle.encode(frames[g0:g0 + G], blob, w.model.as_dict(), G, tau=tau)
-            done += G
-        if time.time() - t0 > budget_s:
-            break
-    dt = time.time() - t0
-    return {"value": round(done / dt, 3), "unit": "frames/s", "cores": int(threads),
+
+    def run(levels, per, dtype):
+        done, t0 = 0, time.time()
+        for k, tau in enumerate(levels):
+            for gsel in range(per):
+                g0 = ((k * per + gsel) * 5 % ngroups) * G   # groups spread over the input
+                oracle.encode(frames[g0:g0 + G], blob, w.model.as_dict(), G, tau=tau, dtype=dtype)
+                done += G
+        dt = time.time() - t0
+        return done, dt
+
+    n64, t64 = run(taus, groups_per_level, np.float64)
+    n32, t32 = run(taus, 1, np.float32)
+    nd, td = run([float("-inf")], 2, np.float64)
+    return {"value": round(n64 / t64, 3), "unit": "frames/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"{done} frames ({done // G} groups of {G}: {groups_per_level} per reuse level "
-                      f"at the calibrated thresholds), fp64 NumPy, {dt:.1f} s"}
+            "sample": f"{n64} frames ({n64 // G} groups of {G}: {groups_per_level} per reuse level "
+                      f"at the bench's thresholds), fp64 NumPy, {t64:.1f} s",
+            "fp32": {"value": round(n32 / t32, 3), "unit": "frames/s",
+                     "sample": f"{n32} frames (one group per reuse level), the oracle in fp32, "
+                               f"{t32:.1f} s"},
+            "dense": {"value": round(nd / td, 3), "unit": "frames/s",
+                      "sample": f"{nd} frames (two groups) with reuse off (tau = -inf), fp64, "
+                                f"{td:.1f} s"}}
+
+
+def operating_points(name):
+    """Thresholds of the workload's reuse levels from the fixture the parity tests use
+    (calibrated with the CPU oracle by tests/golden/make_operating_points.py), or None."""
+    path = os.path.join(ROOT, "tests", "golden", "operating_points.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        ops = json.load(fh)["workloads"].get(name)
+    return {lv["target"]: lv["tau"] for lv in ops["levels"]} if ops else None
+
+
+def render(video, S, n, workers=8):
+    """Frames 0 .. n-1 of a recipe, rendered in parallel chunks (each frame depends only on the
+    recipe and its index)."""
+    if n <= 256:
+        return synth.render_frames(video, S, 0, n)
+    from concurrent.futures import ProcessPoolExecutor
+    chunk = (n + workers - 1) // workers
+    starts = list(range(0, n, chunk))
+    out = np.empty((n, 3, S, S), np.float32)
+    with ProcessPoolExecutor(workers) as ex:
+        for s0, fr in zip(starts, ex.map(synth.render_frames, [video] * len(starts),
+                                         [S] * len(starts), starts,
+                                         [min(chunk, n - s0) for s0 in starts])):
+            out[s0:s0 + fr.shape[0]] = fr
+    return out
 
 
 def main():
@@ -237,6 +278,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="vit_l14")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--frames", type=int, default=0,
+                    help="frames per encode (default: the workload's whole clip; the handle "
+                         "keeps the workload's batch size)")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="bisect each level's threshold on the GPU instead of taking the "
+                         "oracle-calibrated operating points (always done with --restore, "
+                         "--decision, --reorder)")
     ap.add_argument("--restore", action="store_true",
                     help="with the restoration layer on reused tokens (random restoration weights)")
     ap.add_argument("--decision", action="store_true",
@@ -289,24 +337,31 @@ def main():
         import dataclasses
         m = dataclasses.replace(m, reorder=True)
         w = dataclasses.replace(w, model=m)
-    G, F = w.group_size, w.batch_frames
+    G, B = w.group_size, w.batch_frames
+    F = args.frames or w.n_frames           # frames per encode
+    batches = -(-F // ((B // G) * G))        # internal batches per encode
     t0 = time.time()
     blob = synth.make_blob(m, w.weight_seed)
-    frames = synth.render_frames(w.video, m.image_size, 0, F)
-    log(f"[bench] {w.name}: inputs ready in {time.time() - t0:.1f} s")
-    enc = Encoder(m, blob, F)
+    frames = render(w.video, m.image_size, F)
+    log(f"[bench] {w.name}: {F} frames in {batches} batches of <= {B}, inputs ready in "
+        f"{time.time() - t0:.1f} s")
+    enc = Encoder(m, blob, B)
     x = torch.from_numpy(frames).cuda()
     targets = w.reuse_targets or (None,)
-    taus, rhos = [], []
+    ops = None if (args.calibrate or m.restore or m.decision or m.reorder) else \
+        operating_points(w.name)
+    taus = []
     for tgt in targets:
         if tgt is None:
-            tau, rho = float(np.float32(w.tau)), None
+            tau, how = float(np.float32(w.tau)), "fixed"
+        elif ops is not None:
+            tau, how = ops[tgt], "operating point"
         else:
             bracket = {"lo": -16.0, "hi": 16.0} if m.decision else {}
-            tau, rho = calibrate(enc, x, G, tgt, **bracket)
+            tau, _ = calibrate(enc, x[:B], G, tgt, **bracket)
+            how = "GPU bisection on the first batch"
         taus.append(float(np.float32(tau)))
-        rhos.append(rho)
-        log(f"[bench] target reuse {tgt}: tau {tau:.6f} -> reuse {rho}")
+        log(f"[bench] target reuse {tgt}: tau {tau!r} ({how})")
 
     # per-level reuse maps and active rows (deterministic: same as in the timed region), and the
     # embeddings' cosine to those of the same kernels with reuse off (the paper's accuracy proxy)
@@ -445,19 +500,38 @@ def main():
         log("[bench] copy calibration: 1 GiB device-to-device copy done")
         del src, dst
 
-    # per-stage launches and algorithmic bytes per launch in the timed region
-    launches_per_stage = args.steps * len(levels) * m.depth
+    # per stage: launches and algorithmic bytes per launch in the timed region, and from the
+    # profiled pass over the sweep (one encode per level, HIP events around every launch) the
+    # time per sweep and the achieved fractions of the MFMA and HBM peaks
+    launches_per_stage = args.steps * len(levels) * m.depth * batches
+    peak_f = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_FP32_TFLOPS
     stages = {}
+
+    def account(stg, flops_sweep, bytes_sweep, launches):
+        ms = prof.get(stg, (0.0, 0))[0]
+        rec = {"launches": launches, "algo_bytes_per_launch":
+               round(bytes_sweep * args.steps / launches) if launches else 0,
+               "ms_per_sweep": round(ms, 3)}
+        if ms > 0:
+            if flops_sweep:
+                rec["tflops"] = round(flops_sweep / ms * 1e-9, 1)
+                rec["mfma_frac"] = round(flops_sweep / ms * 1e-9 / peak_f, 4)
+            rec["gbs"] = round(bytes_sweep / ms * 1e-6, 1)
+            rec["hbm_frac"] = round(bytes_sweep / ms * 1e-6 / PEAK_HBM_GBS, 4)
+        stages[stg] = rec
+
     for stg in ("qkv", "oproj", "fc1", "fc2", "attn"):
-        tot = sum((attn_bytes(m, Ml, F) if stg == "attn" else stage_bytes(stg, m, Ml))
-                  for lv in levels for Ml in lv["Ml"]) * args.steps
-        stages[stg] = {"launches": launches_per_stage,
-                       "algo_bytes_per_launch": round(tot / launches_per_stage)}
+        fl = sum(stage_flops(stg, m, Ml) for lv in levels for Ml in lv["Ml"])
+        by = sum((attn_bytes(m, Ml, F) if stg == "attn" else stage_bytes(stg, m, Ml))
+                 for lv in levels for Ml in lv["Ml"])
+        account(stg, fl, by, launches_per_stage)
     for stg in ("gate", "ln2", "compact"):
-        tot = sum(row_stage_bytes(stg, m, (lv["Ml"][l - 1] if l else F * N), lv["Ml"][l], F)
-                  for lv in levels for l in range(m.depth)) * args.steps
-        stages[stg] = {"launches": launches_per_stage,
-                       "algo_bytes_per_launch": round(tot / launches_per_stage)}
+        by = sum(row_stage_bytes(stg, m, (lv["Ml"][l - 1] if l else F * N), lv["Ml"][l], F)
+                 for lv in levels for l in range(m.depth))
+        account(stg, 0.0, by, launches_per_stage)
+    img = 3 * m.image_size * m.image_size
+    account("patch", 2.0 * P * 3 * m.patch * m.patch * D * F * len(levels),
+            (F * img * 4 + F * N * D * 4) * len(levels), args.steps * len(levels) * batches)
 
     cpu = None
     if not args.no_cpu:
@@ -471,7 +545,7 @@ def main():
         "dtype": "bf16" if m.dtype == "bf16" else "f32", "data": "synthetic",
         "config": {"workload": f"{w.name}: {m.image_size}px patch {m.patch} ({N} tokens), depth "
                                f"{m.depth}, width {D}, {m.heads} heads, MLP {m.mlp}; {F} frames "
-                               f"per batch, groups of {G}; "
+                               f"per encode in batches of {B}, groups of {G}; "
                                + ("restoration MLP (hidden 128) on reused tokens; " if m.restore
                                   else "")
                                + ("learned decision MLP gate (hidden 64); " if m.decision

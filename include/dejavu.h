@@ -128,6 +128,7 @@ typedef struct dv_config {
 typedef struct dv_handle dv_handle;
 
 /* Number of floats the weight blob of `cfg` must hold (0 if cfg is NULL or invalid).
+ * The blob holds the ViT backbone of Section 2.3 (and the Section 3.3 MLPs when flagged).
  * Blob layout (fp32, tensors back to back):
  *   W_pe [D,3,p,p], b_pe [D], cls [D], pos [N,D]
  *   per layer: ln1_g [D], ln1_b [D], W_qkv [3D,D], b_qkv [3D], W_o [D,D], b_o [D],
@@ -141,10 +142,13 @@ typedef struct dv_handle dv_handle;
  * contiguous slices of D/H rows within each.  LayerNorm eps is 1e-5. */
 size_t dv_weights_floats(const dv_config* cfg);
 
-/* Create a handle: validates cfg, copies the weight blob (`weights`, host,
+/* Create a handle for the encoder of Section 2.3 (plus the Section 3.3 layers when flagged):
+ * validates cfg, copies the weight blob (`weights`, host,
  * `weights_bytes` bytes, the caller may free it on return) to the device,
  * rounds the matrices to bf16 (nearest, ties to even) when dtype is
- * DV_BF16, and allocates the workspace for max_batch_frames frames.
+ * DV_BF16, and allocates the workspace for max_batch_frames frames together with the stream
+ * state of dv_stream_encode (the cached reference, and under DV_FLAG_REORDER the held frames),
+ * so that no encode or stream call allocates.  dv_workspace_bytes reports the total.
  * Synchronous.  Errors: DV_EINVAL (null pointer, wrong blob size, sizes < 1),
  * DV_EUNSUPPORTED (S % p, D % H, head dim, unknown flag bits), DV_ENOMEM (an allocation
  * failed, or the weights and workspace exceed the environment variable DV_MAX_DEVICE_BYTES when
@@ -152,17 +156,23 @@ size_t dv_weights_floats(const dv_config* cfg);
  * On error *out is set to NULL. */
 int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, dv_handle** out);
 
-/* Release a handle and its device memory (synchronises the device first).
- * A NULL handle is accepted. */
+/* Release a handle and its device memory (synchronises the device first; the lifetime end of
+ * the state dv_create made for Section 2.3's encoder).  A NULL handle is accepted. */
 int dv_destroy(dv_handle* h);
 
-/* Message of the last error raised on the calling thread ("" if none). */
+/* Message of the last error raised on the calling thread ("" if none).  Host-side bookkeeping;
+ * no passage of the paper defines it. */
 const char* dv_last_error(void);
 
-/* Bytes of device workspace the handle holds (weights excluded). */
+/* Bytes of device workspace the handle holds (weights excluded): the per-layer batch buffers
+ * of layer-wise scheduling and cached memory compaction (Sections 5.1, 5.2) and the stream
+ * state (Section 6.3). */
 int dv_workspace_bytes(const dv_handle* h, size_t* bytes);
 
-/* Gate mode.  frames: device fp32 [n_frames, 3, S, S], already normalised.
+/* Gate mode: the reuse-aware forward of Section 3.3 (similarity cue, Eq. 1; hard gate; token
+ * filtration; recompute; token reconstruction) over layer-wise scheduled batches (Section 5.1)
+ * with sparse computation compaction (Section 5.3).
+ * frames: device fp32 [n_frames, 3, S, S], already normalised.
  * out_embeddings: device fp32 [n_frames, D] (final LayerNorm of the class token).
  * out_masks: device u8 [n_frames, depth, N] (1 = reused; with DV_FLAG_REORDER, 2 = reused
  * from the future reference) or NULL.
@@ -181,7 +191,8 @@ int dv_workspace_bytes(const dv_handle* h, size_t* bytes);
 int dv_encode(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
               float* out_embeddings, uint8_t* out_masks, hipStream_t stream);
 
-/* Mask-injection mode: the reuse map comes from `masks`, device u8
+/* Mask-injection mode (Section 3.3 with the hard gate's map M supplied by the caller instead of
+ * computed): the reuse map comes from `masks`, device u8
  * [n_frames, depth, N] (nonzero = reuse), instead of the gate.  Entries of
  * class tokens and of reference frames are forced to 0; out_masks (optional)
  * receives the effective map.  Masks need not be monotone over layers: a
@@ -192,7 +203,7 @@ int dv_encode_masked(dv_handle* h, const float* frames, int n_frames, int group_
                      hipStream_t stream);
 
 /* Either mode (masks != NULL selects injection and ignores tau), plus the
- * last layer's full token buffer: out_tokens device fp32 [n_frames, N, D]
+ * last layer's full token buffer (the reconstructed tokens of Section 3.3): out_tokens device fp32 [n_frames, N, D]
  * (NULL allowed).  Used to check whole outputs, not only embeddings. */
 int dv_encode_tokens(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
                      const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,
@@ -203,7 +214,7 @@ int dv_encode_tokens(dv_handle* h, const float* frames, int n_frames, int group_
  * dv_stream_encode calls g = 0, 1, ... since the last dv_stream_reset (or creation); frame g's
  * reference is frame G * floor(g / G), which may have come in an earlier call: the handle then
  * keeps that reference's per-layer input rows and keys/values in a cache ((L+1) N D fp32 plus
- * L N 2D dtype elements, allocated by the first stream call) instead of recomputing it.  Results
+ * L N 2D dtype elements, part of the workspace dv_create allocates) instead of recomputing it.  Results
  * are those of one dv_encode_tokens call over all frames of the stream.  frames, masks (NULL:
  * gate mode with tau), out_embeddings, out_masks and out_tokens (both may be NULL) cover this
  * call's frames, with the layouts of dv_encode_tokens.  group_size must stay the same until the
@@ -223,17 +234,19 @@ int dv_encode_tokens(dv_handle* h, const float* frames, int n_frames, int group_
  * maps (3 frames of pixels, (3 + max_batch_frames) L N bytes).
  * Errors as dv_encode_tokens, plus DV_EINVAL for a changed group_size, a stream left
  * inconsistent by a failed call (reset it), a reordered stream switching between gate mode and
- * injected maps while frames are held, or max_batch_frames <= group_size under reordering;
- * DV_ENOMEM for the cache. */
+ * injected maps while frames are held, or max_batch_frames <= group_size under reordering.
+ * Allocates nothing. */
 int dv_stream_encode(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
                      const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,
                      float* out_tokens, hipStream_t stream);
-/* Forget the stream position, the cached reference and any held frames (the memory is kept). */
+/* Forget the stream position, the cached reference and any held frames (the memory is kept;
+ * Section 6.3's reset of the reference chain). */
 int dv_stream_reset(dv_handle* h);
-/* Number of frames a reordered stream holds (0 .. 3; always 0 without DV_FLAG_REORDER), a host
+/* Number of frames a reordered stream holds (Section 6, frame reordering in streaming use
+ * buffers frames until their later anchor; 0 .. 3; always 0 without DV_FLAG_REORDER), a host
  * value known when the last call returned.  Errors: DV_EINVAL (null handle or n_held). */
 int dv_stream_held(const dv_handle* h, int* n_held);
-/* End a stream: encode the held frames (DV_FLAG_REORDER) as its last frames, whose later anchor
+/* End a stream (Section 6.3): encode the held frames (DV_FLAG_REORDER) as its last frames, whose later anchor
  * is absent, with the mode and tau of the last dv_stream_encode call, write their results to
  * out_embeddings, out_masks and out_tokens (the latter two may be NULL; layouts as
  * dv_stream_encode), then reset the stream.  With no held frames only the reset happens.
@@ -255,7 +268,8 @@ int dv_stream_flush(dv_handle* h, float* out_embeddings, uint8_t* out_masks, flo
 int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size, int32_t* idx,
                int32_t* pos, int32_t* qoff, int32_t* count, hipStream_t stream);
 
-/* Stage timing with HIP events recorded on the encode stream around every
+/* Stage timing (measurement support; the stages are the steps of Sections 2.3 and 3.3) with
+ * HIP events recorded on the encode stream around every
  * launch of the selected stages.  stage_mask: bit s selects stage s (0 = off,
  * DV_PROFILE_ALL = every stage).  While on, every dv_encode* call records;
  * read the totals after synchronising the stream.  dv_profile resets them. */

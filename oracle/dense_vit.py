@@ -27,8 +27,11 @@ def _read_layout(blob, cfg):
         cnt = int(np.prod(sh))
         out[nm] = flat[pos:pos + cnt].reshape(sh)
         pos += cnt
-    # a restoration section (cfg["restore"]) may follow; the dense forward has no reused rows
+    # the restoration MLP (cfg["restore"]: W_r1 [128, D], b_r1, W_r2 [D, 128], b_r2) and then the
+    # decision MLP (cfg["decision"]: W_d1 [64, 6], b_d1, W_d2 [1, 64], b_d2) may follow, one set
+    # per layer; the dense forward reuses nothing, so it reads neither
     extra = L * (128 * D + 128 + D * 128 + D) if cfg.get("restore") else 0
+    extra += L * (64 * 6 + 64 + 64 + 1) if cfg.get("decision") else 0
     assert pos + extra == flat.size, "weight blob size does not match the configuration"
     return out
 

@@ -136,10 +136,23 @@ int check_config(const dv_config* c, Dims* d) {
     if (!attention_supported(bf, d->N, dh))
         return fail(DV_EUNSUPPORTED, "attention for N=%d tokens, head dim %d is not supported "
                     "(bf16: head dim 64/80/96/128; keys and values of a head must fit in LDS)", d->N, dh);
-    const size_t T = (size_t)d->Bw * d->N;
-    const size_t widest = (size_t)std::max(std::max(3 * d->D, d->Dm), d->Kp);
-    if (round_up(T, ROW_PAD) * widest >= (1ull << 31) || T >= (1ull << 30))
-        return fail(DV_EUNSUPPORTED, "max_batch_frames * tokens too large for 32-bit row indices");
+    // kernels address each workspace buffer with 32-bit byte offsets (buffer descriptors) and
+    // token rows with int indices: every buffer stays below 2^32 bytes, the qkv rows including
+    // a stream's cached reference rows after the batch's
+    const size_t T = (size_t)d->Bw * d->N, Tp = round_up(T, ROW_PAD);
+    const size_t el = bf ? 2 : 4, D = d->D;
+    const size_t bufs[] = {T * D * 4,                                         // x
+                           Tp * std::max(D, (size_t)d->Kp) * el,              // A
+                           (Tp + round_up(d->N, ROW_PAD)) * 3 * D * el,       // qkv
+                           Tp * D * 4,                                        // Z (O is smaller)
+                           Tp * (size_t)d->Dm * el,                           // MLP hidden
+                           d->restore ? Tp * (size_t)RH * el : 0,             // restoration hidden
+                           (d->restore && d->reorder) ? Tp * D * 4 : 0};      // restoration outputs
+    size_t largest = 0;
+    for (size_t b : bufs) largest = std::max(largest, b);
+    if (largest >= (1ull << 32) || T >= (1ull << 30))
+        return fail(DV_EUNSUPPORTED, "max_batch_frames %d: a workspace buffer of %zu bytes is "
+                    "too large for 32-bit offsets", d->B, largest);
     return DV_OK;
 }
 
@@ -151,43 +164,97 @@ size_t blob_floats(const Dims& d) {
     return D * 3 * p * p + D + D + N * D + (size_t)d.L * per_layer + 2 * D + restore + decision;
 }
 
-// Bytes of workspace a handle of these dimensions allocates (the order of dv_create's carving).
-size_t workspace_need(const Dims& d) {
-    const size_t N = d.N, D = d.D, Dm = d.Dm, el = d.bf16 ? 2 : 4;
+// Workspace of one internal batch size: the buffers every launch of an encode reads and writes.
+// A handle carves one from its own allocation, with the stream state.
+struct Work {
+    float* x = nullptr;         // [T, D] fp32 token rows
+    void* A = nullptr;          // [Tp, max(D, Kp)] elem: LN output / patch rows
+    void* qkv = nullptr;        // [Tp (+ Np with the stream state), 3D] elem
+    int ext_row = 0;            // packed row of the cached reference's first key/value row
+    void* O = nullptr;          // [Tp, D] elem: attention output
+    float* Z = nullptr;         // [Tp, D] fp32: after attention residual
+    void* Hb = nullptr;         // [Tp, Dm] elem: MLP hidden
+    uint8_t* mask[2] = {nullptr, nullptr};   // [T] per-layer maps (ping-pong)
+    int *idx = nullptr, *pos_ = nullptr, *qoff = nullptr, *cnt = nullptr;
+    int* M = nullptr;           // M[0]: recomputed rows, M[1]: reused tokens
+    int *idx_id = nullptr, *pos_id = nullptr, *qoff_id = nullptr;   // identity lists (reuse off)
+    int id_frames = -1;         // frames the identity lists were built for
+    int* ridx = nullptr;        // [T] reused tokens (restoration)
+    void* Hr = nullptr;         // [Tp, 128] elem: restoration hidden rows
+    float* tcls = nullptr;      // [Bw, H, N] class-token attention weights per head (decision MLP)
+    uint8_t* srcmap = nullptr;  // [T] reordered: 1 where the future anchor supplies the token
+    int* root = nullptr;        // [T] reordered: frame that recomputes a reused token
+    int* rslot = nullptr;       // [T] reordered restoration: a reused token's slot in ridx
+    float* rbuf = nullptr;      // [Tp, D] reordered restoration: restoration outputs
+    // stream state (handles only): the cached reference's layer inputs x^0 .. x^L [L+1, N, D]
+    // fp32 and keys/values [L, N, 2D] elem; under reordering the held frames' pixels
+    // [3, 3, S, S], their maps [3, L, N] and a staging area for a batch's maps [B, L, N]
+    float* xc = nullptr;
+    void* kvc = nullptr;
+    float* hold = nullptr;
+    uint8_t* holdm = nullptr;
+    uint8_t* injs = nullptr;
+};
+
+// The one layout of a workspace for dimensions d (d.Bw frames): returns its bytes and, with a
+// base, the views into it.  stream: also the stream state and the spare key/value rows of a
+// stream's cached reference.
+size_t carve_work(const Dims& d, char* base, Work* out, bool stream) {
+    const size_t N = d.N, D = d.D, Dm = d.Dm, L = d.L, el = d.bf16 ? 2 : 4;
     const size_t T = (size_t)d.Bw * N, Tp = round_up(T, ROW_PAD);
     const size_t Awide = std::max((size_t)D, (size_t)d.Kp);
-    size_t need = 0;
-    auto sz = [&](size_t bytes) { need += round_up(bytes, 256); };
-    sz(T * D * 4);        // x
-    sz(Tp * Awide * el);  // A
-    sz((Tp + round_up(N, ROW_PAD)) * 3 * D * el);  // qkv (+ a stream's cached reference rows)
-    sz(Tp * D * el);      // O
-    sz(Tp * D * 4);       // Z
-    sz(Tp * Dm * el);     // H
-    sz(T);
-    sz(T);                // masks
-    for (int i = 0; i < 2; ++i) {
-        sz(T * 4);
-        sz(T * 4);
-        sz((d.Bw + 1) * 4);
-    }
-    sz((size_t)d.Bw * gate_chunks(d.N) * 4);
-    sz(4 * 4);
+    size_t off = 0;
+    auto take = [&](size_t bytes) -> char* {
+        char* r = base ? base + off : nullptr;
+        off += round_up(bytes, 256);
+        return r;
+    };
+    Work w;
+    w.x = (float*)take(T * D * 4);
+    w.A = take(Tp * Awide * el);
+    w.qkv = take((Tp + (stream ? round_up(N, ROW_PAD) : 0)) * 3 * D * el);
+    w.ext_row = (int)Tp;
+    w.O = take(Tp * D * el);
+    w.Z = (float*)take(Tp * D * 4);
+    w.Hb = take(Tp * Dm * el);
+    w.mask[0] = (uint8_t*)take(T);
+    w.mask[1] = (uint8_t*)take(T);
+    w.idx = (int*)take(T * 4);
+    w.pos_ = (int*)take(T * 4);
+    w.qoff = (int*)take((d.Bw + 1) * 4);
+    w.idx_id = (int*)take(T * 4);
+    w.pos_id = (int*)take(T * 4);
+    w.qoff_id = (int*)take((d.Bw + 1) * 4);
+    w.cnt = (int*)take((size_t)d.Bw * gate_chunks(d.N) * 4);
+    w.M = (int*)take(4 * 4);
     if (d.restore) {
-        sz(T * 4);             // ridx
-        sz(Tp * RH * el);      // Hr
+        w.ridx = (int*)take(T * 4);
+        w.Hr = take(Tp * RH * el);
     }
-    if (d.decision) sz(T * d.H * 4);   // tcls
+    if (d.decision) w.tcls = (float*)take(T * d.H * 4);
     if (d.reorder) {
-        sz(T);       // srcmap
-        sz(T * 4);   // root
+        w.srcmap = (uint8_t*)take(T);
+        w.root = (int*)take(T * 4);
     }
     if (d.reorder && d.restore) {
-        sz(T * 4);         // rslot
-        sz(Tp * D * 4);    // rbuf: restoration outputs of reused tokens
+        w.rslot = (int*)take(T * 4);
+        w.rbuf = (float*)take(Tp * D * 4);
     }
-    return need;
+    if (stream) {
+        w.xc = (float*)take((L + 1) * N * D * 4);
+        w.kvc = take(L * N * 2 * D * el);
+        if (d.reorder) {
+            w.hold = (float*)take((size_t)3 * 3 * d.S * d.S * 4);
+            w.holdm = (uint8_t*)take(3 * L * N);
+            w.injs = (uint8_t*)take((size_t)d.B * L * N);
+        }
+    }
+    if (out) *out = w;
+    return off;
 }
+
+// Bytes of workspace a handle of these dimensions allocates.
+size_t workspace_need(const Dims& d) { return carve_work(d, nullptr, nullptr, true); }
 
 struct Stage {
     double ms = 0;
@@ -207,43 +274,17 @@ struct dv_handle {
     const void* W_pe;
     const float *b_pe, *cls, *pos, *lnf_g, *lnf_b;
     std::vector<LayerW> layers;
-    // workspace views
-    float* x;         // [T, D] fp32 token rows
-    void* A;          // [Tp, max(D, Kp)] elem: LN output / patch rows
-    void* qkv;        // [Tp, 3D] elem
-    void* O;          // [Tp, D] elem: attention output
-    float* Z;         // [Tp, D] fp32: after attention residual
-    void* Hb;         // [Tp, Dm] elem: MLP hidden
-    uint8_t* mask[2]; // [T] per-layer maps (ping-pong)
-    int *idx, *pos_, *qoff, *cnt, *M;   // M[0]: recomputed rows, M[1]: reused tokens
-    int* ridx = nullptr;   // [T] reused tokens (restoration)
-    int* rslot = nullptr;  // [T] reordered restoration: a reused token's slot in ridx
-    float* rbuf = nullptr; // [Tp, D] reordered restoration: restoration outputs, in ridx order
-    float* tcls = nullptr; // [B, H, N] class-token attention weights of the last layer, per head
-                           // (decision MLP)
-    uint8_t* srcmap = nullptr;   // [T] reordered: 1 where the future anchor supplies the token
-    int* root = nullptr;         // [T] reordered: frame that recomputes a reused token
-    int ext_row = 0;             // packed row of the cached reference's first key/value row
+    Work w;                 // views into ws
     // stream state: frames seen since the last reset, their group size, and the cached
-    // reference (stream frame index, -1 none) with its rows
+    // reference (stream frame index, -1 none); under reordering the number of held frames
+    // (stream frames st_pos - st_hold .. st_pos - 1) and the mode and tau of the last call
     long long st_pos = 0;
     int st_G = 0;
     long long st_ref = -1;
-    float* xc = nullptr;   // [L+1, N, D] the cached reference's layer inputs x^0 .. x^L
-    void* kvc = nullptr;   // [L, N, 2D] elem: its keys and values per layer
-    // reordered streams: frames held until their later anchor arrives (stream frames
-    // st_pos - st_hold .. st_pos - 1), with the pixels, the maps of a mask-injection stream, a
-    // staging area for a batch's maps, and the mode and tau of the last call
     int st_hold = 0;
-    float* hold = nullptr;     // [3, 3, S, S]
-    uint8_t* holdm = nullptr;  // [3, L, N]
-    uint8_t* injs = nullptr;   // [B, L, N]
     int st_masks = -1;         // -1: no frame yet, 0: gate mode, 1: injected maps
     int st_mode = 0;
     float st_tau = 0.f;
-    void* Hr = nullptr;    // [Tp, 128] elem: restoration hidden rows
-    int *idx_id, *pos_id, *qoff_id;  // identity lists (reuse off)
-    int id_frames = -1;              // frames the identity lists were built for
     // profiling
     unsigned prof = 0;  // bit s: time stage s
     Stage stages[DV_NUM_STAGES];
@@ -306,7 +347,7 @@ int collect(dv_handle* h) {
 // for frames already returned).  fill >= 0: cache local frame fill, a reference needed by frames
 // of the next call.  npend > 0: the first npend computed frames' pixels are at `pend`, the rest
 // at `frames`.
-int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float tau,
+int run_batch(dv_handle* h, Work& wk, const float* frames, int F, int G, int mode, float tau,
               const uint8_t* inj, float* emb, uint8_t* om, float* tokens, hipStream_t s,
               int skip = 0, int fill = -1, int cached = 0, const float* pend = nullptr,
               int npend = 0) {
@@ -317,28 +358,28 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
     const bool dense = mode == GATE_NONE;
 
     // identity row lists for the dense pass (built once per batch size)
-    if (dense && h->id_frames != F) {
-        launch_compact(nullptr, nullptr, F, N, 1, h->idx_id, h->pos_id, h->qoff_id, nullptr, s);
-        h->id_frames = F;
+    if (dense && wk.id_frames != F) {
+        launch_compact(nullptr, nullptr, F, N, 1, wk.idx_id, wk.pos_id, wk.qoff_id, nullptr, s);
+        wk.id_frames = F;
     }
 
     const size_t row_bytes = (size_t)N * D * sizeof(float);   // one frame's token rows
     const size_t el = bf ? 2 : 4;
     const size_t kv_bytes = (size_t)N * 2 * D * el;           // one frame's keys and values
-    float* xs = h->x + (size_t)skip * N * D;                  // the first computed frame's rows
-    float* xcached = h->x + (size_t)cached * N * D;
+    float* xs = wk.x + (size_t)skip * N * D;                  // the first computed frame's rows
+    float* xcached = wk.x + (size_t)cached * N * D;
     if (skip > 0)   // the cached reference's layer-0 rows
-        HIP_TRY(hipMemcpyAsync(xcached, h->xc, row_bytes, hipMemcpyDeviceToDevice, s));
+        HIP_TRY(hipMemcpyAsync(xcached, wk.xc, row_bytes, hipMemcpyDeviceToDevice, s));
     {   // patch embedding + class-token rows
         Scope sc(h, DV_STAGE_PATCH, s);
         if (npend > 0)
-            launch_im2col(bf, pend, npend, d.S, d.p, d.Kp, h->A, s);
+            launch_im2col(bf, pend, npend, d.S, d.p, d.Kp, wk.A, s);
         if (F - skip > npend)
             launch_im2col(bf, frames, F - skip - npend, d.S, d.p, d.Kp,
-                          (char*)h->A + (size_t)npend * d.P * d.Kp * el, s);
+                          (char*)wk.A + (size_t)npend * d.P * d.Kp * el, s);
         launch_cls_init(xs, h->cls, h->pos, F - skip, N, D, s);
         GemmArgs g{};
-        g.A = h->A;
+        g.A = wk.A;
         g.W = h->W_pe;
         g.bias = h->b_pe;
         g.K = d.Kp;
@@ -354,10 +395,10 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         launch_gemm(Epi::Patch, bf, g, s);
     }
 
-    const int* idx = dense ? h->idx_id : h->idx;
-    const int* pos = dense ? h->pos_id : h->pos_;
-    const int* qoff = dense ? h->qoff_id : h->qoff;
-    const int* Mdev = dense ? nullptr : h->M;
+    const int* idx = dense ? wk.idx_id : wk.idx;
+    const int* pos = dense ? wk.pos_id : wk.pos_;
+    const int* qoff = dense ? wk.qoff_id : wk.qoff;
+    const int* Mdev = dense ? nullptr : wk.M;
     // restoration of reused rows: on whenever tokens can be reused
     const bool restore = d.restore && !dense;
     // learned decision gate: gate mode only (injected maps and the sentinels bypass it)
@@ -368,15 +409,15 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
 
     for (int l = 0; l < L; ++l) {
         const LayerW& w = h->layers[l];
-        uint8_t* cur = h->mask[l & 1];
-        uint8_t* prev = l > 0 ? h->mask[(l - 1) & 1] : nullptr;
+        uint8_t* cur = wk.mask[l & 1];
+        uint8_t* prev = l > 0 ? wk.mask[(l - 1) & 1] : nullptr;
         if (fill >= 0)   // the layer input of a reference carried to the next call
-            launch_copy_rows(h->x, (alias && l > 0) ? h->root : nullptr, fill, N, D,
-                             h->xc + (size_t)l * N * D, s);
+            launch_copy_rows(wk.x, (alias && l > 0) ? wk.root : nullptr, fill, N, D,
+                             wk.xc + (size_t)l * N * D, s);
         {   // reuse gate + LN1 of every recomputed token (reuse off: LN1 of every token)
             Scope sc(h, DV_STAGE_GATE, s);
             GateArgs ga{};
-            ga.x = h->x;
+            ga.x = wk.x;
             ga.F = F;
             ga.N = N;
             ga.D = D;
@@ -391,43 +432,43 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             ga.inj = inj;
             ga.cur = dense ? nullptr : cur;
             ga.out_masks = om;
-            ga.cnt = dense ? nullptr : h->cnt;
+            ga.cnt = dense ? nullptr : wk.cnt;
             ga.ln_g = w.ln1_g;
             ga.ln_b = w.ln1_b;
-            ga.ln_out = h->A;   // token-indexed LN1 rows; the QKV GEMM gathers them through idx
-            ga.d_out = restore ? h->A : nullptr;   // reused tokens' differences, same buffer
+            ga.ln_out = wk.A;   // token-indexed LN1 rows; the QKV GEMM gathers them through idx
+            ga.d_out = restore ? wk.A : nullptr;   // reused tokens' differences, same buffer
             ga.dec = decide ? w.dec : nullptr;
-            ga.tcls = (decide && l > 0) ? h->tcls : nullptr;
+            ga.tcls = (decide && l > 0) ? wk.tcls : nullptr;
             ga.H = d.H;
             ga.reorder = reord;
-            ga.src = reord ? h->srcmap : nullptr;
+            ga.src = reord ? wk.srcmap : nullptr;
             // restored rows are written out every layer; otherwise reused rows alias their root
-            ga.root = (alias && l > 0) ? h->root : nullptr;
+            ga.root = (alias && l > 0) ? wk.root : nullptr;
             ga.skip = skip;
             launch_gate(bf, ga, s);
         }
         if (!dense) {
             Scope sc(h, DV_STAGE_COMPACT, s);
-            launch_scan(h->cnt, gate_chunks(N), F, restore ? (F - skip) * N : 0, h->qoff, h->M, s);
-            launch_compact(cur, h->qoff, F, N, G, h->idx, h->pos_, nullptr,
-                           restore ? h->ridx : nullptr, s, skip, h->ext_row,
-                           restore && reord ? h->rslot : nullptr);
-            if (reord) launch_resolve(cur, h->srcmap, F, N, G, h->pos_, h->root, s);
+            launch_scan(wk.cnt, gate_chunks(N), F, restore ? (F - skip) * N : 0, wk.qoff, wk.M, s);
+            launch_compact(cur, wk.qoff, F, N, G, wk.idx, wk.pos_, nullptr,
+                           restore ? wk.ridx : nullptr, s, skip, wk.ext_row,
+                           restore && reord ? wk.rslot : nullptr);
+            if (reord) launch_resolve(cur, wk.srcmap, F, N, G, wk.pos_, wk.root, s);
         }
         if (restore) {   // restoration hidden rows: GELU(dx W_r1^T + b_r1), before LN2 reuses A
             Scope sc(h, DV_STAGE_RESTORE, s);
             GemmArgs r{};
-            r.A = h->A;
-            r.a_idx = h->ridx;
+            r.A = wk.A;
+            r.a_idx = wk.ridx;
             r.W = w.W_r1;
             r.bias = w.b_r1;
             r.K = D;
             r.Nout = RH;
-            r.Mdev = h->M + 1;
+            r.Mdev = wk.M + 1;
             r.Mconst = T;
             r.Mmax = T;
             r.cus = h->cus;
-            r.out = h->Hr;
+            r.out = wk.Hr;
             launch_gemm(Epi::Fc1, bf, r, s);
         }
         GemmArgs g{};
@@ -438,28 +479,28 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
         g.idx = idx;
         {
             Scope sc(h, DV_STAGE_QKV, s);
-            g.A = h->A;
+            g.A = wk.A;
             g.a_idx = idx;   // packed row m is token row idx[m] of the LN1 buffer
             g.W = w.W_qkv;
             g.bias = w.b_qkv;
             g.K = D;
             g.Nout = 3 * D;
-            g.out = h->qkv;
+            g.out = wk.qkv;
             launch_gemm(Epi::Qkv, bf, g, s);
         }
         if (skip > 0)   // the cached reference's keys and values, at packed rows ext_row ..
-            HIP_TRY(hipMemcpy2DAsync((char*)h->qkv + ((size_t)h->ext_row * 3 * D + D) * el,
-                                     3 * D * el, (const char*)h->kvc + (size_t)l * kv_bytes,
+            HIP_TRY(hipMemcpy2DAsync((char*)wk.qkv + ((size_t)wk.ext_row * 3 * D + D) * el,
+                                     3 * D * el, (const char*)wk.kvc + (size_t)l * kv_bytes,
                                      2 * D * el, 2 * D * el, N, hipMemcpyDeviceToDevice, s));
         if (fill >= 0)
-            launch_copy_ref_kv(h->qkv, pos, fill, N, D, (int)el,
-                               (char*)h->kvc + (size_t)l * kv_bytes, s);
+            launch_copy_ref_kv(wk.qkv, pos, fill, N, D, (int)el,
+                               (char*)wk.kvc + (size_t)l * kv_bytes, s);
         g.a_idx = nullptr;
         AttnArgs at{};
-        at.qkv = h->qkv;
+        at.qkv = wk.qkv;
         at.pos = pos;
         at.qoff = qoff;
-        at.out = h->O;
+        at.out = wk.O;
         at.F = F;
         at.N = N;
         at.D = D;
@@ -477,79 +518,79 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             Scope sc(h, DV_STAGE_CLS, s);
             AttnArgs ac = at;
             ac.G = G;   // I frames are not gated
-            launch_cls_attention(bf, ac, h->tcls, s);
+            launch_cls_attention(bf, ac, wk.tcls, s);
         }
         {
             Scope sc(h, DV_STAGE_OPROJ, s);
-            g.A = h->O;
+            g.A = wk.O;
             g.W = w.W_o;
             g.bias = w.b_o;
             g.K = D;
             g.Nout = D;
-            g.out = h->Z;
-            g.resid = h->x;
+            g.out = wk.Z;
+            g.resid = wk.x;
             launch_gemm(Epi::OProj, bf, g, s);
         }
         {
             Scope sc(h, DV_STAGE_LN2, s);
-            launch_ln_rows(bf, h->Z, nullptr, Mdev, T, D, w.ln2_g, w.ln2_b, h->A, s);
+            launch_ln_rows(bf, wk.Z, nullptr, Mdev, T, D, w.ln2_g, w.ln2_b, wk.A, s);
         }
         {
             Scope sc(h, DV_STAGE_FC1, s);
-            g.A = h->A;
+            g.A = wk.A;
             g.W = w.W_1;
             g.bias = w.b_1;
             g.K = D;
             g.Nout = d.Dm;
-            g.out = h->Hb;
+            g.out = wk.Hb;
             g.resid = nullptr;
             launch_gemm(Epi::Fc1, bf, g, s);
         }
         {
             Scope sc(h, DV_STAGE_FC2, s);
-            g.A = h->Hb;
+            g.A = wk.Hb;
             g.W = w.W_2;
             g.bias = w.b_2;
             g.K = d.Dm;
             g.Nout = D;
-            g.out = h->x;
-            g.resid = h->Z;
+            g.out = wk.x;
+            g.resid = wk.Z;
             launch_gemm(Epi::Fc2, bf, g, s);
         }
         if (skip > 0)   // the cached reference's new rows, for the restoration, merges, next gate
-            HIP_TRY(hipMemcpyAsync(xcached, h->xc + (size_t)(l + 1) * N * D, row_bytes,
+            HIP_TRY(hipMemcpyAsync(xcached, wk.xc + (size_t)(l + 1) * N * D, row_bytes,
                                    hipMemcpyDeviceToDevice, s));
         if (restore && reord) {   // restoration outputs, then each reused row along its chain
             Scope sc(h, DV_STAGE_RESTORE, s);
             GemmArgs r{};
-            r.A = h->Hr;
+            r.A = wk.Hr;
             r.W = w.W_r2;
             r.bias = w.b_r2;
             r.K = RH;
             r.Nout = D;
-            r.Mdev = h->M + 1;
+            r.Mdev = wk.M + 1;
             r.Mconst = T;
             r.Mmax = T;
             r.cus = h->cus;
-            r.out = h->rbuf;
+            r.out = wk.rbuf;
             launch_gemm(Epi::Delta, bf, r, s);
-            launch_restore_chain(h->x, h->rbuf, h->ridx, h->rslot, cur, h->srcmap, h->M + 1, T, F,
+            launch_restore_chain(wk.x, wk.rbuf, wk.ridx, wk.rslot, cur, wk.srcmap, wk.M + 1, T, F,
                                  N, D, G, s);
         } else if (restore) {   // reused rows: the reference token's new row + Hr W_r2^T + b_r2
             Scope sc(h, DV_STAGE_RESTORE, s);
             GemmArgs r{};
-            r.A = h->Hr;
+            r.A = wk.Hr;
             r.W = w.W_r2;
             r.bias = w.b_r2;
             r.K = RH;
             r.Nout = D;
-            r.Mdev = h->M + 1;
+            r.Mdev = wk.M + 1;
             r.Mconst = T;
             r.Mmax = T;
             r.cus = h->cus;
-            r.idx = h->ridx;
-            r.resid = h->x;
-            r.out = h->x;
+            r.idx = wk.ridx;
+            r.resid = wk.x;
+            r.out = wk.x;
             r.N = N;
             r.G = G;
             launch_gemm(Epi::Restore, bf, r, s);
@@ -558,17 +599,17 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
             // are filled in only to hand out the tokens
             if (tokens && l == L - 1) {
                 Scope sc(h, DV_STAGE_MERGE, s);
-                launch_merge(h->x, cur, h->root, F, N, D, G, s);
+                launch_merge(wk.x, cur, wk.root, F, N, D, G, s);
             }
         } else if (mode == GATE_INJECT || mode == GATE_ALL ||
                    (mode == GATE_COS && tokens && l == L - 1)) {
             // reused rows take the reference's new row (gate mode: only to hand out tokens)
             Scope sc(h, DV_STAGE_MERGE, s);
-            launch_merge(h->x, cur, nullptr, F, N, D, G, s);
+            launch_merge(wk.x, cur, nullptr, F, N, D, G, s);
         }
         if (fill >= 0 && l == L - 1)   // the reference's last-layer rows (restored ones included)
-            launch_copy_rows(h->x, alias ? h->root : nullptr, fill, N, D,
-                             h->xc + (size_t)L * N * D, s);
+            launch_copy_rows(wk.x, alias ? wk.root : nullptr, fill, N, D,
+                             wk.xc + (size_t)L * N * D, s);
     }
     {
         Scope sc(h, DV_STAGE_FINAL, s);
@@ -580,19 +621,19 @@ int run_batch(dv_handle* h, const float* frames, int F, int G, int mode, float t
     return DV_OK;
 }
 
-int encode_impl(dv_handle* h, const float* frames, int n, int G, float tau, const uint8_t* masks,
-                float* emb, uint8_t* om, float* tokens, hipStream_t s) {
+// Validates the arguments of an encode call; sets *mode.
+int check_encode(const dv_handle* h, const float* frames, int n, int G, float tau,
+                 const uint8_t* masks, const float* emb, int* mode) {
     if (!h) return fail(DV_EINVAL, "handle is NULL");
     if (!frames || !emb) return fail(DV_EINVAL, "frames and out_embeddings must not be NULL");
     if (n < 1) return fail(DV_EINVAL, "n_frames must be >= 1 (got %d)", n);
     if (G < 1) return fail(DV_EINVAL, "group_size must be >= 1 (got %d)", G);
     if (G > h->d.B) return fail(DV_EINVAL, "group_size %d exceeds max_batch_frames %d", G, h->d.B);
-    int mode;
     if (masks) {
-        mode = GATE_INJECT;
+        *mode = GATE_INJECT;
     } else {
         if (std::isnan(tau)) return fail(DV_EINVAL, "tau is NaN");
-        mode = (tau == -INFINITY) ? GATE_NONE : (tau == INFINITY) ? GATE_ALL : GATE_COS;
+        *mode = (tau == -INFINITY) ? GATE_NONE : (tau == INFINITY) ? GATE_ALL : GATE_COS;
     }
     const Dims& d = h->d;
     if (d.reorder && G % 4)
@@ -601,7 +642,16 @@ int encode_impl(dv_handle* h, const float* frames, int n, int G, float tau, cons
     if (d.reorder && d.restore && G / 4 + 1 > CHAIN_MAX)
         return fail(DV_EINVAL, "reordered referencing with restoration supports group_size <= %d "
                     "(got %d)", 4 * (CHAIN_MAX - 1), G);
-    const int per = (d.B / G) * G;
+    return DV_OK;
+}
+
+// An encode call over internal batches of at most `batch` frames (whole groups) with workspace
+// w, laid out for that many frames.  Arguments already checked.
+int encode_batches(dv_handle* h, Work& w, int batch, const float* frames, int n, int G, int mode,
+                   float tau, const uint8_t* masks, float* emb, uint8_t* om, float* tokens,
+                   hipStream_t s) {
+    const Dims& d = h->d;
+    const int per = (batch / G) * G;
     const size_t img = (size_t)3 * d.S * d.S;
     HIP_TRY(hipSetDevice(h->device));
     for (int f0 = 0; f0 < n; f0 += per) {
@@ -610,7 +660,7 @@ int encode_impl(dv_handle* h, const float* frames, int n, int G, float tau, cons
         // (its results are computed again, identically, as part of the next batch)
         const int F = F0 + (d.reorder && f0 + F0 < n ? 1 : 0);
         const size_t ml = (size_t)d.L * d.N;
-        int rc = run_batch(h, frames + (size_t)f0 * img, F, G, mode, tau,
+        int rc = run_batch(h, w, frames + (size_t)f0 * img, F, G, mode, tau,
                            masks ? masks + (size_t)f0 * ml : nullptr, emb + (size_t)f0 * d.D,
                            om ? om + (size_t)f0 * ml : nullptr,
                            tokens ? tokens + (size_t)f0 * d.N * d.D : nullptr, s);
@@ -620,24 +670,13 @@ int encode_impl(dv_handle* h, const float* frames, int n, int G, float tau, cons
     return DV_OK;
 }
 
-// The stream's device buffers, on its first call: the reference cache and, under reordering, the
-// held frames' pixels and maps and the map staging area.
-int stream_buffers(dv_handle* h) {
-    const Dims& d = h->d;
-    const size_t el = d.bf16 ? 2 : 4, N = d.N, D = d.D, L = d.L;
-    hipError_t e = hipSuccess;
-    if (!h->xc) e = hipMalloc((void**)&h->xc, (L + 1) * N * D * sizeof(float));
-    if (e == hipSuccess && !h->kvc) e = hipMalloc(&h->kvc, L * N * 2 * D * el);
-    if (d.reorder) {
-        if (e == hipSuccess && !h->hold)
-            e = hipMalloc((void**)&h->hold, (size_t)3 * 3 * d.S * d.S * sizeof(float));
-        if (e == hipSuccess && !h->holdm) e = hipMalloc((void**)&h->holdm, 3 * L * N);
-        if (e == hipSuccess && !h->injs) e = hipMalloc((void**)&h->injs, (size_t)d.B * L * N);
-    }
-    if (e != hipSuccess)
-        return fail(e == hipErrorOutOfMemory ? DV_ENOMEM : DV_EHIP, "stream buffers: %s",
-                    hipGetErrorString(e));
-    return DV_OK;
+// An encode call with the handle's own workspace.
+int encode_impl(dv_handle* h, const float* frames, int n, int G, float tau, const uint8_t* masks,
+                float* emb, uint8_t* om, float* tokens, hipStream_t s) {
+    int mode;
+    int rc = check_encode(h, frames, n, G, tau, masks, emb, &mode);
+    if (rc) return rc;
+    return encode_batches(h, h->w, h->d.B, frames, n, G, mode, tau, masks, emb, om, tokens, s);
 }
 
 // A reordered stream.  A frame between anchors a and a + 4 (stream indices that are multiples of
@@ -674,24 +713,25 @@ int stream_reorder_impl(dv_handle* h, const float* frames, int n, int G, int mod
         const long long e = u + cnt - 1;
         const int F = lead + (int)cnt;
         const int npend = (int)std::max<long long>(0, std::min(st, e + 1) - u);
-        const float* pend = npend ? h->hold + (size_t)(u - done) * img : nullptr;
+        const float* pend = npend ? h->w.hold + (size_t)(u - done) * img : nullptr;
         const float* fr = frames ? frames + (size_t)std::max<long long>(0, u - st) * img : nullptr;
         const uint8_t* inj = nullptr;
         if (masks || (flush && mode == GATE_INJECT)) {
             if (npend) {   // held frames' maps, then the call's own
-                HIP_TRY(hipMemcpyAsync(h->injs, h->holdm + (size_t)(u - done) * ml, npend * ml,
+                HIP_TRY(hipMemcpyAsync(h->w.injs, h->w.holdm + (size_t)(u - done) * ml, npend * ml,
                                        hipMemcpyDeviceToDevice, s));
                 if (cnt > npend)
-                    HIP_TRY(hipMemcpyAsync(h->injs + npend * ml, masks, (cnt - npend) * ml,
+                    HIP_TRY(hipMemcpyAsync(h->w.injs + npend * ml, masks, (cnt - npend) * ml,
                                            hipMemcpyDeviceToDevice, s));
-                inj = h->injs;
+                inj = h->w.injs;
             } else {
                 inj = masks + (size_t)(u - st) * ml;
             }
         }
         const size_t k = (size_t)(u - done);
         const int fill = flush ? -1 : F - 1;
-        int rc = run_batch(h, fr, F, G, mode, tau, inj, emb + k * D, om ? om + k * ml : nullptr,
+        int rc = run_batch(h, h->w, fr, F, G, mode, tau, inj, emb + k * D,
+                           om ? om + k * ml : nullptr,
                            tokens ? tokens + k * N * D : nullptr, s, lead, fill,
                            lead > 0 ? lead - 1 : 0, pend, npend);
         if (rc) return rc;
@@ -709,10 +749,10 @@ int stream_reorder_impl(dv_handle* h, const float* frames, int n, int G, int mod
     // (when this call completed nothing) or are all replaced by frames of this call
     const long long h0 = last + 1;
     for (long long g = std::max(h0, st); g < total; ++g) {
-        HIP_TRY(hipMemcpyAsync(h->hold + (size_t)(g - h0) * img, frames + (size_t)(g - st) * img,
+        HIP_TRY(hipMemcpyAsync(h->w.hold + (size_t)(g - h0) * img, frames + (size_t)(g - st) * img,
                                img * sizeof(float), hipMemcpyDeviceToDevice, s));
         if (masks)
-            HIP_TRY(hipMemcpyAsync(h->holdm + (size_t)(g - h0) * ml, masks + (size_t)(g - st) * ml,
+            HIP_TRY(hipMemcpyAsync(h->w.holdm + (size_t)(g - h0) * ml, masks + (size_t)(g - st) * ml,
                                    ml, hipMemcpyDeviceToDevice, s));
     }
     h->st_hold = (int)(total - h0);
@@ -754,7 +794,6 @@ int stream_impl(dv_handle* h, const float* frames, int n, int G, float tau, cons
         return fail(DV_EINVAL, "a reordered stream holding frames cannot switch between gate "
                     "mode and injected maps");
     HIP_TRY(hipSetDevice(h->device));
-    if (int rc = stream_buffers(h)) return rc;
     if (d.reorder) {
         int rc = stream_reorder_impl(h, frames, n, G, mode, tau, masks, emb, om, tokens, s, false);
         if (rc) return rc;
@@ -778,7 +817,7 @@ int stream_impl(dv_handle* h, const float* frames, int n, int G, float tau, cons
         int cnt = std::min(d.B - lead, n - k);
         if (k + cnt < n) cnt = (int)((gk + cnt) / G * G - gk);   // end on a group boundary
         const int fill = (open && last >= gk && last < gk + cnt) ? (int)(last - gk) + lead : -1;
-        int rc = run_batch(h, frames + (size_t)k * img, lead + cnt, G, mode, tau,
+        int rc = run_batch(h, h->w, frames + (size_t)k * img, lead + cnt, G, mode, tau,
                            masks ? masks + (size_t)k * ml : nullptr, emb + (size_t)k * D,
                            om ? om + (size_t)k * ml : nullptr,
                            tokens ? tokens + (size_t)k * N * D : nullptr, s, lead, fill);
@@ -979,9 +1018,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
         w.dec = d.decision ? (const float*)(wb + dco[l]) : nullptr;
     }
 
-    // --- workspace ----------------------------------------------------------------------------
-    const size_t T = (size_t)d.Bw * N, Tp = round_up(T, ROW_PAD);
-    const size_t Awide = std::max((size_t)D, (size_t)d.Kp);
+    // --- workspace (with the stream state, so that no encode call allocates) -----------------
     const size_t need = workspace_need(d);
     {
         hipError_t e = hipMalloc(&h->ws, need);
@@ -995,37 +1032,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
         if (e != hipSuccess) return cleanup(fail(DV_EHIP, "workspace clear: %s", hipGetErrorString(e)));
     }
     h->ws_bytes = need;
-    char* p = (char*)h->ws;
-    h->x = carve<float>(p, T * D);
-    h->A = carve<char>(p, Tp * Awide * el);
-    h->qkv = carve<char>(p, (Tp + round_up(N, ROW_PAD)) * 3 * D * el);
-    h->ext_row = (int)Tp;
-    h->O = carve<char>(p, Tp * D * el);
-    h->Z = carve<float>(p, Tp * D);
-    h->Hb = carve<char>(p, Tp * Dm * el);
-    h->mask[0] = carve<uint8_t>(p, T);
-    h->mask[1] = carve<uint8_t>(p, T);
-    h->idx = carve<int>(p, T);
-    h->pos_ = carve<int>(p, T);
-    h->qoff = carve<int>(p, d.Bw + 1);
-    h->idx_id = carve<int>(p, T);
-    h->pos_id = carve<int>(p, T);
-    h->qoff_id = carve<int>(p, d.Bw + 1);
-    h->cnt = carve<int>(p, (size_t)d.Bw * gate_chunks(d.N));
-    h->M = carve<int>(p, 4);
-    if (d.restore) {
-        h->ridx = carve<int>(p, T);
-        h->Hr = carve<char>(p, Tp * RH * el);
-    }
-    if (d.decision) h->tcls = carve<float>(p, T * d.H);
-    if (d.reorder) {
-        h->srcmap = carve<uint8_t>(p, T);
-        h->root = carve<int>(p, T);
-    }
-    if (d.reorder && d.restore) {
-        h->rslot = carve<int>(p, T);
-        h->rbuf = carve<float>(p, Tp * D);
-    }
+    carve_work(d, (char*)h->ws, &h->w, true);
     *out = h;
     return DV_OK;
 }
@@ -1041,11 +1048,6 @@ int dv_destroy(dv_handle* h) {
     for (auto e : h->pool) (void)hipEventDestroy(e);
     if (h->wmem) (void)hipFree(h->wmem);
     if (h->ws) (void)hipFree(h->ws);
-    if (h->xc) (void)hipFree(h->xc);
-    if (h->kvc) (void)hipFree(h->kvc);
-    if (h->hold) (void)hipFree(h->hold);
-    if (h->holdm) (void)hipFree(h->holdm);
-    if (h->injs) (void)hipFree(h->injs);
     delete h;
     return DV_OK;
 }
@@ -1061,6 +1063,7 @@ int dv_encode(dv_handle* h, const float* frames, int n_frames, int group_size, f
     return encode_impl(h, frames, n_frames, group_size, tau, nullptr, out_embeddings, out_masks,
                        nullptr, stream);
 }
+
 
 int dv_encode_masked(dv_handle* h, const float* frames, int n_frames, int group_size,
                      const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,

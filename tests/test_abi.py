@@ -150,3 +150,18 @@ def test_create_reports_enomem_above_the_device_memory_cap(monkeypatch):
     with pytest.raises(dj.DejaVuError) as e:
         dj.dv_create(_cfg(), blob)
     assert e.value.code == dj.DV_ENOMEM and "DV_MAX_DEVICE_BYTES" in dj.dv_last_error()
+
+
+@pytest.mark.parametrize("mlp,ok,bad", [
+    (4096, 2039, 2040),   # MLP hidden rows: round_up(257 B, 256) * 4096 * 2 bytes reach 2^32
+    (1024, 2717, 2718),   # MLP no wider than D: the qkv rows (batch + 512 spare) * 3072 * 2 do
+])
+def test_config_rejects_buffers_past_32_bit_offsets(mlp, ok, bad):
+    """ViT-L/14 geometry (257 tokens, width 1024, bf16): the largest batch whose every workspace
+    buffer stays below 2^32 bytes is accepted, one frame more is not.  With mlp 1024 the limit
+    comes from the qkv buffer and its spare rows for a stream's cached reference (2^32 / 6144 =
+    699050.7 rows; 2717 frames pad to 698368 rows + 512, 2718 to 698624 + 512)."""
+    def floats(b):
+        return dj.dv_weights_floats(dj.make_config(224, 14, 24, 1024, 16, mlp, "bf16", b))
+    assert floats(ok) > 0
+    assert floats(bad) == 0

@@ -26,6 +26,9 @@ N257_D = ModelConfig(224, 14, 2, 128, 2, 256, "bf16", decision=True)
 MID_RD = ModelConfig(112, 16, 3, 256, 4, 512, "bf16", restore=True, decision=True)
 
 GELU_SLOPE = 1.13   # max |GELU'(z)| over the reals (at z ~ 1.4)
+# Largest fraction of decisions the margin may leave unjudged: a wider band would let most
+# decisions pass unchecked (about 1 % lie inside at ViT-L/14).
+BAND_MAX = 0.05
 
 
 def feature_errors(m):
@@ -74,28 +77,52 @@ def _case(m, seed, F=16):
     return w, fr
 
 
+def judged_thresholds(w, m, fr, G, blob, k=2, sep=0.15):
+    """Operating points where the check has power: candidate thresholds at the 5 %, 10 %, ...,
+    95 % quantiles of the oracle's decision values at the paper's tau = 0, each scored by the
+    fraction of decisions inside the margin in the oracle's own run at that threshold; the k
+    lowest-scoring candidates at least `sep` apart in quantile.  (Reused tokens carry an exact
+    cosine of 1, so their d values cluster and a plain quartile can sit inside a cluster.)"""
+    r0 = oracle.encode(fr, blob, m.as_dict(), G, tau=0.0)
+    dv = r0["dec"][~np.isnan(r0["dec"])]
+    scored = []
+    for q in np.arange(0.05, 0.951, 0.05):
+        tau = float(np.float32(np.quantile(dv, q)))
+        r = oracle.encode(fr, blob, m.as_dict(), G, tau=tau)
+        d, ev = r["dec"], ~np.isnan(r["dec"])
+        inside = float(np.mean(np.abs(d[ev] - tau) < decision_band(w, m, r["t"])[ev]))
+        scored.append((inside, q, tau))
+    picked = []
+    for inside, q, tau in sorted(scored):
+        if all(abs(q - q2) >= sep for _, q2, _ in picked):
+            picked.append((inside, q, tau))
+        if len(picked) == k:
+            break
+    return [tau for _, _, tau in picked]
+
+
 @pytest.mark.parametrize("m,G", [(TINY_D, 4), (SMALL_D, 8), (MID_D, 8), (N257_D, 8)],
                          ids=["tiny", "small", "mid", "n257"])
 def test_decision_gate_parity(m, G):
     w, fr = _case(m, 41, F=8 if m is TINY_D else 16)
     blob = synth.pack_weights(w, m)
-    # operating points: the paper's tau = 0 and the quartiles of the oracle's decision values
-    r0 = oracle.encode(fr, blob, m.as_dict(), G, tau=0.0)
-    dv = r0["dec"][~np.isnan(r0["dec"])]
+    # operating points: the paper's tau = 0 and two judged thresholds apart in the range
     checked = 0
-    for tau in (0.0, *np.quantile(dv, [0.25, 0.5, 0.75])):
+    for tau in (0.0, *judged_thresholds(w, m, fr, G, blob)):
         tau = float(np.float32(tau))
         emb, mg, toks = _run(m, blob, fr, G, tau)
         r = oracle.encode(fr, blob, m.as_dict(), G, masks=mg)
         band = decision_band(w, m, r["t"])
         bad, inside = decision_parity(mg, r, band, tau)
+        print(f"[decision {m.width}] tau {tau:.4f}: reuse {oracle.reuse_rate(mg, G):.3f}, "
+              f"decisions off {bad}, in band {inside:.2%}", flush=True)
         assert bad == 0, f"tau={tau}: {bad} decisions differ outside the band ({inside:.1%} inside)"
-        assert inside < 0.5, f"tau={tau}: band too wide to check ({inside:.1%} inside)"
+        assert inside <= BAND_MAX, f"tau={tau}: band too wide to check ({inside:.1%} inside)"
         checked += 1
         dt = "f32" if m.dtype == "f32" else "bf16"
         check_close(emb, r["emb"], dt, f"embeddings tau={tau}")
         check_close(toks, r["tokens"], dt, f"tokens tau={tau}")
-    assert checked == 4
+    assert checked == 3
 
 
 @pytest.mark.parametrize("m,G,theta", [(TINY_D, 4, 0.95), (SMALL_D, 8, 0.9), (MID_D, 8, 0.75)],
@@ -149,8 +176,10 @@ def test_decision_attention_cue(m):
     _, et = feature_errors(m)
     band = a * (et * np.abs(r["t"]) + 1e-6)
     bad, inside = decision_parity(mg, r, band, 0.0)
+    print(f"[decision attention cue {m.n_tokens}] decisions off {bad}, in band {inside:.2%}",
+          flush=True)
     assert bad == 0, f"{bad} decisions differ outside the band ({inside:.1%} inside)"
-    assert inside < 0.5
+    assert inside <= BAND_MAX
     check_close(emb, r["emb"], "bf16", "embeddings")
 
 
@@ -159,12 +188,13 @@ def test_decision_with_restoration():
     w, fr = _case(m, 45)
     blob = synth.pack_weights(w, m)
     G = 8
-    r0 = oracle.encode(fr, blob, m.as_dict(), G, tau=0.0)
-    tau = float(np.float32(np.quantile(r0["dec"][~np.isnan(r0["dec"])], 0.4)))
+    tau = judged_thresholds(w, m, fr, G, blob, k=1)[0]
     emb, mg, toks = _run(m, blob, fr, G, tau)
     r = oracle.encode(fr, blob, m.as_dict(), G, masks=mg)
     bad, inside = decision_parity(mg, r, decision_band(w, m, r["t"]), tau)
+    print(f"[decision with restoration] decisions off {bad}, in band {inside:.2%}", flush=True)
     assert bad == 0, f"{bad} decisions differ outside the band ({inside:.1%} inside)"
+    assert inside <= BAND_MAX
     assert 0.1 < oracle.reuse_rate(mg, G) < 0.95
     check_close(emb, r["emb"], "bf16", "embeddings")
     check_close(toks, r["tokens"], "bf16", "tokens")
