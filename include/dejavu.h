@@ -149,6 +149,7 @@ size_t dv_weights_floats(const dv_config* cfg);
  * DV_BF16, and allocates the workspace for max_batch_frames frames together with the stream
  * state of dv_stream_encode (the cached reference, and under DV_FLAG_REORDER the held frames),
  * so that no encode or stream call allocates.  dv_workspace_bytes reports the total.
+ * Also looks up, once per device, the static scratch array of dv_encode_noalloc.
  * Synchronous.  Errors: DV_EINVAL (null pointer, wrong blob size, sizes < 1),
  * DV_EUNSUPPORTED (S % p, D % H, head dim, unknown flag bits), DV_ENOMEM (an allocation
  * failed, or the weights and workspace exceed the environment variable DV_MAX_DEVICE_BYTES when
@@ -190,6 +191,21 @@ int dv_workspace_bytes(const dv_handle* h, size_t* bytes);
  * DV_FLAG_REORDER, or above 60 with DV_FLAG_REORDER and DV_FLAG_RESTORE), DV_EHIP. */
 int dv_encode(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
               float* out_embeddings, uint8_t* out_masks, hipStream_t stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): dv_encode with its workspace taken from a static
+ * device array of DV_SCRATCH_BYTES bytes instead of the handle's.  Same arguments, results and
+ * errors as dv_encode (results are bitwise those of dv_encode: they do not depend on the
+ * internal batch size).  Frames are encoded in internal batches of as many whole groups as the
+ * array holds (at most max_batch_frames); a single group that does not fit is rejected with
+ * DV_ENOMEM before anything is launched.  The call allocates nothing and creates no events
+ * (stage timing is off for it).  Each device holds one copy of the array for the life of the
+ * process, looked up by dv_create; every call on a device uses that one copy, so calls that
+ * overlap on one device (other streams, other threads, other handles) race and must be
+ * serialised by the caller.  DV_EHIP if the array's address could not be looked up. */
+#define DV_SCRATCH_BYTES (128ull << 20)
+int dv_encode_noalloc(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
+                      float* out_embeddings, uint8_t* out_masks, hipStream_t stream);
 
 /* Mask-injection mode (Section 3.3 with the hard gate's map M supplied by the caller instead of
  * computed): the reuse map comes from `masks`, device u8

@@ -45,6 +45,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -53,6 +54,12 @@
 #include "dv_internal.h"
 
 using namespace dv;
+
+// Scratch of dv_encode_noalloc: the workspace of its internal batches, in a static device array
+// (one copy per device, held until the process ends).  Host code never uses the array's name as
+// an address: dv_create looks up each device's copy once (scratch_setup) and every launch takes
+// that address.
+static __device__ __align__(256) char scratch[DV_SCRATCH_BYTES];
 
 namespace {
 
@@ -75,6 +82,37 @@ int fail(int code, const char* fmt, ...) {
             return fail(e_ == hipErrorOutOfMemory ? DV_ENOMEM : DV_EHIP, "%s: %s (%s:%d)", #expr, \
                         hipGetErrorString(e_), __FILE__, __LINE__);                            \
     } while (0)
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[MAX_DEVICES] = {};   // device address of each device's copy of `scratch`
+bool g_scratch_done[MAX_DEVICES] = {};
+std::string g_scratch_err;           // why a look-up failed
+
+// Once per device, with that device current: the address of its copy of the scratch array,
+// cleared once (later calls find the previous call's contents, as in a handle's workspace).
+void scratch_setup(int dev) {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (dev < 0 || dev >= MAX_DEVICES) {
+        g_scratch_err = "device index out of range";
+        return;
+    }
+    if (g_scratch_done[dev]) return;
+    g_scratch_done[dev] = true;
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e == hipSuccess) e = hipMemset(p, 0, DV_SCRATCH_BYTES);
+    if (e != hipSuccess) {
+        g_scratch_err = hipGetErrorString(e);
+        return;
+    }
+    g_scratch[dev] = p;
+}
+
+void* scratch_base(int dev) {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    return (dev >= 0 && dev < MAX_DEVICES) ? g_scratch[dev] : nullptr;
+}
 
 constexpr int ROW_PAD = 256;  // GEMM operand rows are padded to a multiple of the tallest tile
 
@@ -165,7 +203,8 @@ size_t blob_floats(const Dims& d) {
 }
 
 // Workspace of one internal batch size: the buffers every launch of an encode reads and writes.
-// A handle carves one from its own allocation, with the stream state.
+// A handle carves one from its own allocation (with the stream state); dv_encode_noalloc carves
+// one from the static scratch array.
 struct Work {
     float* x = nullptr;         // [T, D] fp32 token rows
     void* A = nullptr;          // [Tp, max(D, Kp)] elem: LN output / patch rows
@@ -972,6 +1011,7 @@ int dv_create(const dv_config* cfg, const float* weights, size_t weights_bytes, 
         return code;
     };
     if (hipGetDevice(&h->device) != hipSuccess) return cleanup(fail(DV_EHIP, "hipGetDevice failed"));
+    scratch_setup(h->device);   // dv_encode_noalloc's array on this device (errors reported there)
     if (hipDeviceGetAttribute(&h->cus, hipDeviceAttributeMultiprocessorCount, h->device) !=
         hipSuccess)
         h->cus = 0;   // the GEMMs then keep one tiling for all rows
@@ -1064,6 +1104,43 @@ int dv_encode(dv_handle* h, const float* frames, int n_frames, int group_size, f
                        nullptr, stream);
 }
 
+int dv_encode_noalloc(dv_handle* h, const float* frames, int n_frames, int group_size, float tau,
+                      float* out_embeddings, uint8_t* out_masks, hipStream_t stream) {
+    int mode;
+    int rc = check_encode(h, frames, n_frames, group_size, tau, nullptr, out_embeddings, &mode);
+    if (rc) return rc;
+    void* base = scratch_base(h->device);
+    if (!base)
+        return fail(DV_EHIP, "the scratch array of device %d has no address (set-up failed: %s)",
+                    h->device, g_scratch_err.c_str());
+    // internal batches: as many whole groups as the scratch holds, at most max_batch_frames
+    Dims dn = h->d;
+    int best = 0;
+    for (int b = group_size; b <= h->d.B; b += group_size) {
+        dn.B = b;
+        dn.Bw = b + (dn.reorder ? 1 : 0);
+        if (carve_work(dn, nullptr, nullptr, false) > DV_SCRATCH_BYTES) break;
+        best = b;
+    }
+    if (best == 0) {
+        dn.B = group_size;
+        dn.Bw = group_size + (dn.reorder ? 1 : 0);
+        return fail(DV_ENOMEM, "one group of %d frames needs %zu bytes of scratch, above the %llu "
+                    "bytes of dv_encode_noalloc's static array", group_size,
+                    carve_work(dn, nullptr, nullptr, false), (unsigned long long)DV_SCRATCH_BYTES);
+    }
+    dn.B = best;
+    dn.Bw = best + (dn.reorder ? 1 : 0);
+    Work w;
+    carve_work(dn, (char*)base, &w, false);   // identity lists are rebuilt: another call may
+    w.id_frames = -1;                        // have used the array since
+    const unsigned prof = h->prof;            // stage timing creates events: off for this call
+    h->prof = 0;
+    rc = encode_batches(h, w, best, frames, n_frames, group_size, mode, tau, nullptr,
+                        out_embeddings, out_masks, nullptr, stream);
+    h->prof = prof;
+    return rc;
+}
 
 int dv_encode_masked(dv_handle* h, const float* frames, int n_frames, int group_size,
                      const uint8_t* masks, float* out_embeddings, uint8_t* out_masks,

@@ -58,6 +58,8 @@ def load(path=None):
         "dv_workspace_bytes": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_size_t)]),
         "dv_encode": (ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_float, _P, _P,
                                      _P]),
+        "dv_encode_noalloc": (ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_float,
+                                             _P, _P, _P]),
         "dv_encode_masked": (ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P]),
         "dv_encode_tokens": (ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                             _P, _P, _P, _P, _P]),
@@ -120,6 +122,15 @@ def dv_workspace_bytes(handle):
 def dv_encode(handle, frames, n_frames, group_size, tau, out_embeddings, out_masks, stream):
     _check(load().dv_encode(handle, frames, n_frames, group_size, tau, out_embeddings,
                             out_masks, stream))
+
+
+def dv_encode_noalloc(handle, frames, n_frames, group_size, tau, out_embeddings, out_masks,
+                      stream):
+    _check(load().dv_encode_noalloc(handle, frames, n_frames, group_size, tau, out_embeddings,
+                                    out_masks, stream))
+
+
+DV_SCRATCH_BYTES = 128 << 20   # the static scratch array of dv_encode_noalloc
 
 
 def dv_encode_masked(handle, frames, n_frames, group_size, masks, out_embeddings, out_masks,
@@ -234,6 +245,15 @@ class Encoder:
             dv_encode(self.handle, _ptr(frames), n, group_size, float(tau), _ptr(emb),
                       _ptr(masks), _stream(stream))
         return emb, masks, toks
+
+    def encode_noalloc(self, frames, group_size, tau, out_embeddings, out_masks=None, stream=None):
+        """Gate mode through dv_encode_noalloc, into caller-allocated outputs (embeddings
+        [n, D] fp32, masks [n, depth, N] uint8 or None); the library allocates nothing."""
+        self._check_frames(frames)
+        n = frames.shape[0]
+        dv_encode_noalloc(self.handle, _ptr(frames), n, group_size, float(tau),
+                          _ptr(out_embeddings), _ptr(out_masks), _stream(stream))
+        return out_embeddings, out_masks
 
     def encode_masked(self, frames, group_size, masks_in, want_masks=True, want_tokens=False,
                       stream=None):

@@ -114,6 +114,7 @@ def test_encode_rejects_bad_arguments_without_a_handle():
     # null handle is rejected before anything touches the device
     assert lib.dv_encode(None, 1, 1, 1, 0.5, 1, None, None) == dj.DV_EINVAL
     assert lib.dv_encode_masked(None, 1, 1, 1, None, 1, None, None) == dj.DV_EINVAL
+    assert lib.dv_encode_noalloc(None, 1, 1, 1, 0.5, 1, None, None) == dj.DV_EINVAL
     assert lib.dv_encode_tokens(None, 1, 1, 1, math.nan, None, 1, None, None, None) == dj.DV_EINVAL
     assert lib.dv_stream_encode(None, 1, 1, 1, 0.5, None, 1, None, None, None) == dj.DV_EINVAL
     assert lib.dv_stream_reset(None) == dj.DV_EINVAL
