@@ -913,30 +913,10 @@ void launch_bf16(const AttnArgs& a0, hipStream_t s) {
                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         raised = true;
     }
-    // groups of several frames (head dim 64): per-unit blocks, one per compute unit, when the
-    // reference rows, the maps and at least one other frame's rows fit in LDS
-    if constexpr (DH == 64) {
-        if (a.G > 1 && a.cus > 0) {
-            const int pcap = unit_pcap(a.N, DH, a.G, 160 * 1024);
-            if (pcap >= a.N) {
-                const size_t lds = UnitGeo(a.N, DH, a.G, pcap).bytes();
-                const int units = (a.F + a.G - 1) / a.G * a.H;
-                hipLaunchKernelGGL(attn_unit_k<DH>, dim3(std::min(units, a.cus)), dim3(UW * 64),
-                                   lds, s, a, pcap);
-                return;
-            }
-        }
-    }
-    // Reuse on without per-group blocks (head dim 64): frames with at most `cut` query tiles go
-    // to per-tile wavefronts streaming K/V (one pass over the keys per tile), the others to
-    // per-frame blocks (one staging of the keys for all tiles); of the cuts 2, 3, 4 and 5,
-    // 2 gave the shortest attention at 50, 70 and 90 % reuse (ViT-L/14, reordered groups of 8).
-    // A wavefront takes two consecutive tiles of a frame at a time, so that a two-tile frame
-    // streams its keys once (attention 3.73 / 3.57 / 2.57 ms against 3.75 / 3.67 / 2.70 with
-    // one tile per wavefront).  DV_ATTN_CFG (measurements): 1 per-frame blocks only, 2 per-tile
-    // wavefronts only, also without reuse; DV_ATTN_CUT overrides the cut, DV_ATTN_PAIR=0 takes
-    // one tile per wavefront.
-    static int cfg = -1, cut = 2, pair = 1;
+    // DV_ATTN_CFG (measurements): 1 per-frame blocks only, 2 per-tile wavefronts only, also
+    // without reuse, 3 groups too large for per-unit blocks on per-frame blocks placed by unit;
+    // DV_ATTN_CUT overrides the cuts below, DV_ATTN_PAIR=0 takes one tile per wavefront.
+    static int cfg = -1, cut = -1, pair = 1;
     if (cfg < 0) {
         const char* e = getenv("DV_ATTN_CFG");
         cfg = e ? atoi(e) : 0;
@@ -945,9 +925,45 @@ void launch_bf16(const AttnArgs& a0, hipStream_t s) {
         const char* pp = getenv("DV_ATTN_PAIR");
         if (pp) pair = atoi(pp);
     }
+    int tcut = cut >= 0 ? cut : 2;
+    if constexpr (DH == 64) {
+        if (a.G > 1 && a.cus > 0) {
+            // groups of several frames: per-unit blocks, one per compute unit, when the
+            // reference rows, the maps and at least one other frame's rows fit in LDS
+            const int pcap = unit_pcap(a.N, DH, a.G, 160 * 1024);
+            if (pcap >= a.N && cfg != 1 && cfg != 2) {
+                const size_t lds = UnitGeo(a.N, DH, a.G, pcap).bytes();
+                const int units = (a.F + a.G - 1) / a.G * a.H;
+                hipLaunchKernelGGL(attn_unit_k<DH>, dim3(std::min(units, a.cus)), dim3(UW * 64),
+                                   lds, s, a, pcap);
+                return;
+            }
+            // Otherwise (ViT-L/14 at 336 px: 577 keys) the frames go the way of ungrouped
+            // reuse: those with few query tiles to per-tile wavefronts, which read the
+            // reference's keys and values through L2 (every frame of a group reads the same
+            // rows), the others to per-frame blocks.  Measured at 0 / 34 / 62 / 90 % reuse
+            // (attention per 1024-frame encode): per-frame blocks placed by unit 74 / 64 / 56 /
+            // 46 ms; cut 2 76 / 63 / 50 / 37; cut 3 78 / 61 / 47 / 35; cut 5 78 / 61 / 51 / 35;
+            // every frame per tile 91 / 73 / 51 / 31.  A per-unit kernel over chunks of 64 keys
+            // (the reference's chunk rows staged once for the frames of a pass) took 125 / 105 /
+            // 89 / 66 ms: its per-chunk barriers serialise staging and the softmax.
+            if (cfg != 3) {
+                a.G = 0;
+                a.sparse = 1;
+                tcut = cut >= 0 ? cut : 3;
+            }
+        }
+    }
+    // Reuse on without per-group blocks (head dim 64): frames with at most `tcut` query tiles go
+    // to per-tile wavefronts streaming K/V (one pass over the keys per tile), the others to
+    // per-frame blocks (one staging of the keys for all tiles); of the cuts 2, 3, 4 and 5,
+    // 2 gave the shortest attention at 50, 70 and 90 % reuse (ViT-L/14, reordered groups of 8).
+    // A wavefront takes two consecutive tiles of a frame at a time, so that a two-tile frame
+    // streams its keys once (attention 3.73 / 3.57 / 2.57 ms against 3.75 / 3.67 / 2.70 with
+    // one tile per wavefront).
     if constexpr (DH == 64) {
         if (a.G == 0 && cfg != 1 && (a.sparse || cfg == 2)) {
-            a.tile_cut = cfg == 2 ? (a.N + 31) / 32 : cut;
+            a.tile_cut = cfg == 2 ? (a.N + 31) / 32 : tcut;
             if (pair) launch_wave<DH, 2>(a, s);
             else launch_wave<DH, 1>(a, s);
             if (a.tile_cut >= (a.N + 31) / 32) return;   // no frame left for per-frame blocks

@@ -109,8 +109,8 @@ def test_tiny_dense_matches_oracle():
     check_close(host(toks), r[1], "f32", "tokens")
 
 
-@pytest.mark.parametrize("m", [TINY.model, SMALL_BF16, MID_BF16, DH80_N50],
-                         ids=["tiny", "small", "mid", "dh80"])
+@pytest.mark.parametrize("m", [TINY.model, SMALL_BF16, MID_BF16, DH80_N50, N577_BF16],
+                         ids=["tiny", "small", "mid", "dh80", "n577"])
 def test_copy_at_plus_inf_is_bitwise(m):
     torch = require_gpu()
     blob = synth.make_blob(m, 21)
@@ -132,8 +132,8 @@ def test_copy_at_plus_inf_is_bitwise(m):
     assert np.array_equal(host(toks2), t) and np.array_equal(host(emb2), e)
 
 
-@pytest.mark.parametrize("m", [TINY.model, SMALL_BF16, MID_BF16, DH80_N50],
-                         ids=["tiny", "small", "mid", "dh80"])
+@pytest.mark.parametrize("m", [TINY.model, SMALL_BF16, MID_BF16, DH80_N50, N577_BF16],
+                         ids=["tiny", "small", "mid", "dh80", "n577"])
 def test_reuse_off_equivalences_bitwise(m):
     """tau=2 (gate runs, reuses nothing) == tau=-inf; G=1 == dense; reference frames of a
     reuse run == the same frames run densely (rows are independent of their packed slot)."""
@@ -229,3 +229,34 @@ def test_bf16_gate_mode_parity(m):
         assert np.all(mg[:, 1:] >= mg[:, :-1]), "gate-mode reuse must be monotone over layers"
         check_close(host(emb), r["emb"], "bf16", f"embeddings tau={tau}")
         check_close(host(toks), r["tokens"], "bf16", f"tokens tau={tau}")
+
+
+# N = 577 keys in two layers: a frame's keys do not fit in LDS next to another frame's, so a
+# group's frames take the per-tile wavefronts (few query tiles) or per-frame blocks
+N577_L2 = ModelConfig(336, 14, 2, 128, 2, 256, "bf16")
+
+
+@pytest.mark.parametrize("G,n", [(8, 21), (12, 24)], ids=["G8-ragged", "G12"])
+def test_large_frame_group_gate_mode_parity(G, n):
+    """Gate mode at 577 tokens over the reuse range (frames of every tile count, so both
+    kernels), groups of 8 with a short last group and of 12."""
+    torch = require_gpu()
+    m = N577_L2
+    blob = synth.make_blob(m, 27)
+    fr = _video(m, n, seed=9, sigma=0.02, n_obj=4, size=40)
+    enc = encoder(m, blob, 24)
+    for tau in (0.5, 0.95, 0.995, 2.0):
+        emb, masks, toks = enc.encode(dev(fr), G, tau, want_tokens=True)
+        torch.cuda.synchronize()
+        mg = host(masks)
+        r = oracle.encode(fr, blob, m.as_dict(), G, masks=mg)
+        bad, inside = mask_parity(mg, r["cos"], tau)
+        print(f"[n577 G{G}] tau {tau}: reuse {oracle.reuse_rate(mg, G):.3f}, decisions off {bad}, "
+              f"in band {inside:.2%}", flush=True)
+        assert bad == 0, f"tau={tau}: {bad} decisions differ outside the band ({inside:.3%} inside)"
+        check_close(host(emb), r["emb"], "bf16", f"embeddings tau={tau}")
+        check_close(host(toks), r["tokens"], "bf16", f"tokens tau={tau}")
+    d_emb, _, d_tok = enc.encode(dev(fr), G, float("-inf"), want_tokens=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(d_tok), host(toks)), "tau = 2 equals reuse off bit for bit"
+    assert np.array_equal(host(d_emb), host(emb))
