@@ -27,6 +27,7 @@ sys.path.insert(0, ROOT)
 
 import synth  # noqa: E402
 
+METRIC = "frames/s ViT-L/14 at 50/70/90% reuse; packed-GEMM MFMA util; speedup vs dense"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0
@@ -103,8 +104,8 @@ def row_stage_bytes(stage, m, Ml_prev, Ml, F):
 
 
 KERNEL_SOURCE = {"qkv": "gemm.hip", "oproj": "gemm.hip", "fc1": "gemm.hip", "fc2": "gemm.hip",
-                 "attn": "attention.hip", "gate": "rowops.hip", "ln2": "rowops.hip",
-                 "compact": "rowops.hip"}
+                 "patch": "gemm.hip", "attn": "attention.hip", "gate": "rowops.hip",
+                 "ln2": "rowops.hip", "compact": "rowops.hip"}
 
 
 def measured_traffic(stage):
@@ -123,7 +124,8 @@ def measured_traffic(stage):
 
 
 STAGE_KERNEL = {"qkv": ("Epi)1",), "oproj": ("Epi)2",), "fc1": ("Epi)3",), "fc2": ("Epi)4",),
-                "attn": ("attn_unit_k", "attn_mfma_k"), "gate": ("gate_k",),
+                "patch": ("Epi)0",),
+                "attn": ("attn_unit_k", "attn_mfma_k", "attn_wave_k"), "gate": ("gate_k",),
                 "ln2": ("ln_rows_k",), "compact": ("compact_k",)}   # name fragments per stage
 
 
@@ -180,6 +182,58 @@ def traffic_record(fetch_csv, write_csv, bench_json, cmds):
         with open(os.path.join(ROOT, "profiles", f"{stage}_hbm_traffic.json"), "w") as fh:
             json.dump(rec, fh, indent=1)
         out[stage] = rec
+    return out
+
+
+def mfma_record(csv_path, bench_json, cmds):
+    """Turns one rocprofv3 --pmc pass (SQ_VALU_MFMA_BUSY_CYCLES, SQ_BUSY_CYCLES,
+    GRBM_GUI_ACTIVE) over bench.py into profiles/mfma_busy.json.  Per stage, over the timed
+    region's launches (the last ones of the stage's kernels in the run): SQ_VALU_MFMA_BUSY_CYCLES
+    sums the matrix units' busy cycles over the 1024 SIMDs (a 32x32x16 bf16 MFMA keeps one busy
+    for 32 cycles, so it counts 1/1024 of the MFMA FLOPs); GRBM_GUI_ACTIVE sums the active cycles
+    of the 8 XCDs.  mfma_busy_frac = busy / (GRBM_GUI_ACTIVE / 8 x 1024): the share of the
+    launch the matrix units are busy at the clock they ran at; clock_ghz = (GRBM_GUI_ACTIVE / 8)
+    / duration; mfma_tflops = the MFMA FLOPs issued per second."""
+    import csv
+    import hashlib
+    with open(bench_json) as fh:
+        bench = [json.loads(ln) for ln in fh if ln.startswith("{")][-1]
+    with open(csv_path) as fh:
+        rows = list(csv.DictReader(fh))
+    by = {}
+    for r in rows:
+        d = by.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"],
+                                                    "ns": int(r["End_Timestamp"]) -
+                                                    int(r["Start_Timestamp"])})
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+    order = sorted(by)
+    xcd, simds = 8, 1024
+    out = {"commands": cmds,
+           "formula": {"mfma_busy_frac": "SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 * 1024)",
+                       "clock_ghz": "(GRBM_GUI_ACTIVE / 8) / duration",
+                       "mfma_tflops": "SQ_VALU_MFMA_BUSY_CYCLES * 1024 / duration (32768 FLOP "
+                                      "per 32 busy cycles of a 32x32x16 bf16 MFMA)"},
+           "stages": {}}
+    for stage, info in bench["stages"].items():
+        keys = STAGE_KERNEL.get(stage, ())
+        ds = [d for d in order if any(k in by[d]["name"] for k in keys)][-info["launches"]:]
+        if not ds:
+            continue
+        tot = {c: sum(by[d].get(c, 0.0) for d in ds) for c in
+               ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE")}
+        ns = sum(by[d]["ns"] for d in ds)
+        busy, act = tot["SQ_VALU_MFMA_BUSY_CYCLES"], tot["GRBM_GUI_ACTIVE"] / xcd
+        src = os.path.join("paper_2506_14107_amd", "csrc", KERNEL_SOURCE[stage])
+        out["stages"][stage] = {
+            "kernel": by[ds[0]]["name"], "launches": len(ds), "counters": tot,
+            "avg_launch_us": round(ns / len(ds) / 1e3, 2),
+            "source": src,
+            "source_sha256": hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest(),
+            "clock_ghz": round(act / ns, 3) if ns else None,
+            "mfma_busy_frac": round(busy / max(act * simds, 1.0), 4),
+            "mfma_tflops": round(busy * 1024 / ns * 1e-3, 1) if ns else None}
+    with open(os.path.join(ROOT, "profiles", "mfma_busy.json"), "w") as fh:
+        json.dump(out, fh, indent=1)
     return out
 
 
@@ -306,9 +360,19 @@ def main():
                     help="write profiles/<stage>_hbm_traffic.json from two rocprofv3 --pmc passes "
                          "(FETCH_SIZE, WRITE_SIZE) over bench.py --copy-calibration and that "
                          "run's output line; no GPU work")
+    ap.add_argument("--mfma-record", nargs=2, metavar=("PMC_CSV", "BENCH_OUT"),
+                    help="write profiles/mfma_busy.json from a rocprofv3 --pmc pass "
+                         "(SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES GRBM_GUI_ACTIVE) over bench.py "
+                         "and that run's output line; no GPU work")
     ap.add_argument("--command", action="append", default=[],
                     help="with --traffic-record: the profiling commands, kept in the record")
     args = ap.parse_args()
+    if args.mfma_record:
+        rec = mfma_record(*args.mfma_record, args.command)
+        for st, r in rec["stages"].items():
+            print(f"{st}: MFMA busy {r['mfma_busy_frac']} at {r['clock_ghz']} GHz, "
+                  f"{r['mfma_tflops']} TFLOP/s issued, {r['avg_launch_us']} us per launch")
+        return
     if args.traffic_record:
         recs = traffic_record(*args.traffic_record, args.command)
         for st, r in recs.items():
@@ -538,7 +602,9 @@ def main():
         cpu = cpu_baseline(w, blob, frames, taus)
 
     out = {
-        "metric": "frames/s ViT-L/14 at 50/70/90% reuse; packed-GEMM MFMA util; speedup vs dense",
+        "metric": METRIC if w.name == "vit_l14" else
+                  f"frames/s {w.name} at " + "/".join(f"{t:.0%}" for t in targets if t is not None)
+                  + " reuse; packed-GEMM MFMA util; speedup vs dense",
         "value": round(value, 2), "unit": "frames/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(total_ms / args.steps, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
