@@ -261,8 +261,8 @@ def calibrate(enc, x, G, target, iters=24, lo=-1.0, hi=1.0):
 
 def cpu_baseline(w, blob, frames, taus, groups_per_level=2):
     """The CPU oracle on whole groups of the same frames: fp64 at each level's threshold
-    (`groups_per_level` groups per level), its fp32 variant (one group per level) and reuse off
-    (tau = -inf, fp64, two groups)."""
+    (`groups_per_level` groups per level), its fp32 variant (one group at the last level) and
+    reuse off (tau = -inf, fp64, one group)."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -283,17 +283,17 @@ def cpu_baseline(w, blob, frames, taus, groups_per_level=2):
         return done, dt
 
     n64, t64 = run(taus, groups_per_level, np.float64)
-    n32, t32 = run(taus, 1, np.float32)
-    nd, td = run([float("-inf")], 2, np.float64)
+    n32, t32 = run(taus[-1:], 1, np.float32)
+    nd, td = run([float("-inf")], 1, np.float64)
     return {"value": round(n64 / t64, 3), "unit": "frames/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"{n64} frames ({n64 // G} groups of {G}: {groups_per_level} per reuse level "
                       f"at the bench's thresholds), fp64 NumPy, {t64:.1f} s",
             "fp32": {"value": round(n32 / t32, 3), "unit": "frames/s",
-                     "sample": f"{n32} frames (one group per reuse level), the oracle in fp32, "
-                               f"{t32:.1f} s"},
+                     "sample": f"{n32} frames (one group at the last reuse level), the oracle "
+                               f"in fp32, {t32:.1f} s"},
             "dense": {"value": round(nd / td, 3), "unit": "frames/s",
-                      "sample": f"{nd} frames (two groups) with reuse off (tau = -inf), fp64, "
+                      "sample": f"{nd} frames (one group) with reuse off (tau = -inf), fp64, "
                                 f"{td:.1f} s"}}
 
 
