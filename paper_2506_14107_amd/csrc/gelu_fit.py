@@ -26,25 +26,23 @@ def fit():
 
 
 def horner32(c, x):
-    """The kernel's operation order in fp32: m = min(|x|, 4), h = m P(m^2), 0.5 x + |x| h."""
+    """The kernel's operation order in fp32: y = clamp(x, -4, 4), p = P(y^2) by Horner (fused
+    multiply-adds), GELU(x) = x (y p + 1/2) with the inner multiply-add fused."""
     x = np.asarray(x, dtype=np.float32)
-    m = np.minimum(np.abs(x), np.float32(X))
-    s = m * m
+    y = np.clip(x, np.float32(-X), np.float32(X))
+    s = (y * y).astype(np.float32)
     p = np.float32(c[-1])
     for k in range(len(c) - 2, -1, -1):
-        p = (p * s + np.float32(c[k])).astype(np.float32)
-    h = (m * p).astype(np.float32)
-    return (np.float32(0.5) * x + np.abs(x) * h).astype(np.float32)
+        p = np.float32(np.float64(p) * np.float64(s) + np.float64(np.float32(c[k])))
+    inner = np.float32(np.float64(y) * np.float64(p) + 0.5)
+    return (x * inner).astype(np.float32)
 
 
 if __name__ == "__main__":
     c = fit()
-    xs = np.linspace(0, X, 400001)
-    cdf = 0.5 * erf(xs / np.sqrt(2))
-    m = xs.astype(np.float32)
-    p = np.float32(c[-1])
-    for k in range(DEG - 1, -1, -1):
-        p = (p * m * m + np.float32(c[k])).astype(np.float32)
-    print("max |Phi error| (fp32):", np.max(np.abs(m * p - cdf)))
+    xs = np.linspace(-X - 1, X + 1, 400001)
+    exact = xs * 0.5 * (1 + erf(xs / np.sqrt(2)))
+    got = np.array([horner32(c, v) for v in xs[::50]], dtype=np.float64)
+    print("max |GELU error| (fp32, kernel order):", np.max(np.abs(got - exact[::50])))
     for k, v in enumerate(c):
         print(f"c{k} = {np.float32(v)!r}")
