@@ -488,10 +488,9 @@ int run_batch(dv_handle* h, Work& wk, const float* frames, int F, int G, int mod
         }
         if (!dense) {
             Scope sc(h, DV_STAGE_COMPACT, s);
-            launch_scan(wk.cnt, gate_chunks(N), F, restore ? (F - skip) * N : 0, wk.qoff, wk.M, s);
-            launch_compact(cur, wk.qoff, F, N, G, wk.idx, wk.pos_, nullptr,
-                           restore ? wk.ridx : nullptr, s, skip, wk.ext_row,
-                           restore && reord ? wk.rslot : nullptr);
+            launch_scan_compact(wk.cnt, gate_chunks(N), restore ? (F - skip) * N : 0, cur, F, N, G,
+                                wk.idx, wk.pos_, wk.qoff, wk.M, restore ? wk.ridx : nullptr, s,
+                                skip, wk.ext_row, restore && reord ? wk.rslot : nullptr);
             if (reord) launch_resolve(cur, wk.srcmap, F, N, G, wk.pos_, wk.root, s);
         }
         if (restore) {   // restoration hidden rows: GELU(dx W_r1^T + b_r1), before LN2 reuses A

@@ -181,6 +181,11 @@ void launch_scan(const int* cnt, int per, int F, int tokens, int* qoff, int* M, 
 void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G, int* idx,
                     int* pos, int* qoff_out, int* ridx, hipStream_t s, int skip = 0,
                     int ext_row = 0, int* rslot = nullptr);
+// launch_scan then launch_compact in one launch: every block sums the per-block counts of the
+// frames before it (and before its reference) itself; qoff, M as launch_scan writes them
+void launch_scan_compact(const int* cnt, int per, int tokens, const uint8_t* cur, int F, int N,
+                         int G, int* idx, int* pos, int* qoff, int* M, int* ridx, hipStream_t s,
+                         int skip = 0, int ext_row = 0, int* rslot = nullptr);
 // dst[i, 0:2D] = K|V of packed row pos[f*N + i], el-byte elems
 void launch_copy_ref_kv(const void* qkv, const int* pos, int f, int N, int D, int el, void* dst,
                         hipStream_t s);

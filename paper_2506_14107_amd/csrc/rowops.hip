@@ -31,23 +31,59 @@ __device__ inline float wave_sum(float v) {
 }
 
 // --- patch gather: A[f*P + k, e] = frame[f][c][py*p+ky][px*p+kx], e = (c, ky, kx); zero pad to Kp
+// bf16: a thread writes 8 consecutive elements of a row with one 16-byte store (Kp is a multiple
+// of 64), walking (c, ky, kx) from the chunk's first element; 32-bit indices (F*P*Kp/8 < 2^31
+// for every batch the handle accepts)
 template <bool BF>
 __global__ void im2col_k(const float* __restrict__ frames, int F, int S, int p, int Kp, void* A) {
-    const int g = S / p, P = g * g, kk = 3 * p * p;
-    const size_t total = (size_t)F * P * Kp;
-    for (size_t t = blockIdx.x * (size_t)blockDim.x + threadIdx.x; t < total;
-         t += (size_t)gridDim.x * blockDim.x) {
-        const int e = (int)(t % Kp);
-        const size_t row = t / Kp;
-        const int f = (int)(row / P), k = (int)(row % P);
-        float v = 0.f;
-        if (e < kk) {
-            const int c = e / (p * p), ky = (e / p) % p, kx = e % p;
-            const int py = k / g, px = k % g;
-            v = frames[(((size_t)f * 3 + c) * S + (py * p + ky)) * S + px * p + kx];
+    const int g = S / p, P = g * g, kk = 3 * p * p, pp = p * p;
+    if constexpr (BF) {
+        const int cpr = Kp / 8;
+        const unsigned total = (unsigned)F * P * cpr;
+        for (unsigned t = blockIdx.x * blockDim.x + threadIdx.x; t < total;
+             t += gridDim.x * blockDim.x) {
+            const unsigned row = t / cpr;
+            const int e0 = (int)(t - row * cpr) * 8;
+            const unsigned f = row / P;
+            const int k = (int)(row - f * P);
+            const int py = k / g, px = k - (k / g) * g;
+            const float* base = frames + ((size_t)f * 3 * S + py * p) * S + px * p;
+            int c = e0 / pp, rem = e0 - (e0 / pp) * pp;
+            int ky = rem / p, kx = rem - (rem / p) * p;
+            uint32_t w[4];
+#pragma unroll
+            for (int q = 0; q < 8; q += 2) {
+                float v[2];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    v[h] = e0 + q + h < kk ? base[((size_t)c * S + ky) * S + kx] : 0.f;
+                    if (++kx == p) {
+                        kx = 0;
+                        if (++ky == p) {
+                            ky = 0;
+                            ++c;
+                        }
+                    }
+                }
+                w[q / 2] = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+            }
+            ((uint4*)A)[t] = uint4{w[0], w[1], w[2], w[3]};
         }
-        if (BF) ((uint16_t*)A)[t] = f32_to_bf16(v);
-        else ((float*)A)[t] = v;
+    } else {
+        const size_t total = (size_t)F * P * Kp;
+        for (size_t t = blockIdx.x * (size_t)blockDim.x + threadIdx.x; t < total;
+             t += (size_t)gridDim.x * blockDim.x) {
+            const int e = (int)(t % Kp);
+            const size_t row = t / Kp;
+            const int f = (int)(row / P), k = (int)(row % P);
+            float v = 0.f;
+            if (e < kk) {
+                const int c = e / pp, ky = (e / p) % p, kx = e % p;
+                const int py = k / g, px = k % g;
+                v = frames[(((size_t)f * 3 + c) * S + (py * p + ky)) * S + px * p + kx];
+            }
+            ((float*)A)[t] = v;
+        }
     }
 }
 
@@ -388,20 +424,57 @@ __global__ __launch_bounds__(1024) void scan_k(const int* cnt, int per, int F, i
 // (reference frames keep all their tokens, in order).  cur == nullptr: every token recomputed,
 // qoff ignored (identity lists).  ridx: the complement list of reused tokens, frame-major (a
 // reused token's rank is i minus the recomputed tokens of its frame before i).
+// With `cnt` (the gate's per-block counts, `per` of them per frame) the frame offsets come from
+// the counts themselves: each block sums the counts of the frames before it (and before its
+// reference) and writes qoff[f]; the last block writes qoff[F], M[0] = the recomputed rows and,
+// with tokens > 0, M[1] = tokens - M[0].  The offsets equal those of scan_k.
 __global__ __launch_bounds__(256) void compact_k(const uint8_t* cur, const int* qoff_in, int F,
                                                  int N, int G, int* idx, int* pos, int* qoff_out,
-                                                 int* ridx, int skip, int ext_row, int* rslot) {
+                                                 int* ridx, int skip, int ext_row, int* rslot,
+                                                 const int* cnt, int per, int* qoff_w, int* M,
+                                                 int tokens) {
     const int f = blockIdx.x;
     const int r = (f / G) * G;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __shared__ int wtot[4];
+    int pre_f = 0, pre_r = 0;   // counts of the frames before f and before r
+    if (cnt) {
+        int a = 0, b = 0;
+        for (int e = tid; e < f * per; e += 256) {
+            const int v = cnt[e];
+            a += v;
+            b += e < r * per ? v : 0;
+        }
+        for (int o = 32; o >= 1; o >>= 1) {
+            a += __shfl_xor(a, o, WAVE);
+            b += __shfl_xor(b, o, WAVE);
+        }
+        if (lane == 0) wtot[wave] = a;
+        __syncthreads();
+        pre_f = wtot[0] + wtot[1] + wtot[2] + wtot[3];
+        __syncthreads();
+        if (lane == 0) wtot[wave] = b;
+        __syncthreads();
+        pre_r = wtot[0] + wtot[1] + wtot[2] + wtot[3];
+        __syncthreads();
+        if (tid == 0) {
+            qoff_w[f] = pre_f;
+            if (f == F - 1) {
+                int last = 0;
+                for (int k = 0; k < per; ++k) last += cnt[(size_t)f * per + k];
+                qoff_w[F] = pre_f + last;
+                M[0] = pre_f + last;
+                if (tokens > 0) M[1] = tokens - (pre_f + last);
+            }
+        }
+    }
     if (f < skip) {   // carried over from an earlier call: no rows; the cached reference's
                       // keys/values are the rows at ext_row (the other such frames are never read)
         for (int i = tid; i < N; i += 256) pos[(size_t)f * N + i] = ext_row + i;
         return;
     }
-    __shared__ int wtot[4];
-    const int off = cur ? qoff_in[f] : f * N;
-    const int refoff = (skip > 0 && r == 0) ? ext_row : cur ? qoff_in[r] : r * N;
+    const int off = cnt ? pre_f : cur ? qoff_in[f] : f * N;
+    const int refoff = (skip > 0 && r == 0) ? ext_row : cnt ? pre_r : cur ? qoff_in[r] : r * N;
     int running = 0;
     for (int base = 0; base < N; base += 256) {
         const int i = base + tid;
@@ -654,7 +727,7 @@ inline int grid_for(size_t work, int per_block, int cap = 8192) {
 void launch_im2col(bool bf16, const float* frames, int F, int S, int p, int Kp, void* A,
                    hipStream_t s) {
     const int P = (S / p) * (S / p);
-    const size_t total = (size_t)F * P * Kp;
+    const size_t total = (size_t)F * P * Kp / (bf16 ? 8 : 1);   // elements, or 8-element chunks
     const int grid = grid_for(total, 256, 65536);
     if (bf16) hipLaunchKernelGGL(im2col_k<true>, dim3(grid), dim3(256), 0, s, frames, F, S, p, Kp, A);
     else hipLaunchKernelGGL(im2col_k<false>, dim3(grid), dim3(256), 0, s, frames, F, S, p, Kp, A);
@@ -707,7 +780,14 @@ void launch_compact(const uint8_t* cur, const int* qoff_in, int F, int N, int G,
                     int* pos, int* qoff_out, int* ridx, hipStream_t s, int skip, int ext_row,
                     int* rslot) {
     hipLaunchKernelGGL(compact_k, dim3(F), dim3(256), 0, s, cur, qoff_in, F, N, G, idx, pos,
-                       qoff_out, ridx, skip, ext_row, rslot);
+                       qoff_out, ridx, skip, ext_row, rslot, nullptr, 0, nullptr, nullptr, 0);
+}
+
+void launch_scan_compact(const int* cnt, int per, int tokens, const uint8_t* cur, int F, int N,
+                         int G, int* idx, int* pos, int* qoff, int* M, int* ridx, hipStream_t s,
+                         int skip, int ext_row, int* rslot) {
+    hipLaunchKernelGGL(compact_k, dim3(F), dim3(256), 0, s, cur, nullptr, F, N, G, idx, pos,
+                       nullptr, ridx, skip, ext_row, rslot, cnt, per, qoff, M, tokens);
 }
 
 void launch_restore_chain(float* x, const float* rbuf, const int* ridx, const int* rslot,
