@@ -354,6 +354,11 @@ def main():
                     help="deliver each batch to the timed encodes as a stream of calls of this "
                          "many frames (dv_stream_encode; groups span calls; a reordered stream "
                          "is flushed at the end)")
+    ap.add_argument("--split", type=int, default=1,
+                    help="encode the clip as this many contiguous parts of whole groups at the "
+                         "same time, one handle (batches of 1/K of the workload's) and one HIP "
+                         "stream each; bit-identical results; no roofline (the parts' kernels "
+                         "share the chip, so no launch's duration is its own)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device-to-device copy (HBM counter calibration)")
     ap.add_argument("--traffic-record", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_OUT"),
@@ -461,6 +466,15 @@ def main():
     if S > 1:   # small handles: one call's frames plus a group of carried-over frames
         encs = [Encoder(m, blob, min(F, args.stream_chunk + G)) for _ in range(S)]
         hs = [torch.cuda.Stream() for _ in range(S)]
+    K = max(1, args.split)
+    if K > 1:   # contiguous parts of whole groups, one handle and HIP stream each
+        if args.stream_chunk or F % (K * G):
+            raise SystemExit("--split needs whole calls and a frame count that splits into "
+                             f"{K} parts of whole groups of {G}")
+        part = F // K
+        part_cap = min(part, max(G, (B // K) // G * G))
+        kencs = [Encoder(m, blob, part_cap) for _ in range(K)]
+        khs = [torch.cuda.Stream() for _ in range(K)]
 
     def encode_all(tau):
         """One encode of the batch: one call, or a stream of calls of --stream-chunk frames (of
@@ -478,6 +492,15 @@ def main():
             for e, st in zip(encs, hs):
                 with torch.cuda.stream(st):
                     e.stream_flush(want_masks=False, stream=st)
+                cur.wait_stream(st)
+            return
+        if K > 1:
+            cur = torch.cuda.current_stream()
+            for k, (e, st) in enumerate(zip(kencs, khs)):
+                st.wait_stream(cur)
+                with torch.cuda.stream(st):
+                    e.encode(x[k * part:(k + 1) * part], G, tau, want_masks=False, stream=st)
+            for st in khs:
                 cur.wait_stream(st)
             return
         if not args.stream_chunk:
@@ -519,14 +542,14 @@ def main():
 
     # the timed region: K steps of the whole sweep, dominant stage timed with HIP events
     total_ms, st = time_calls(taus, args.steps, args.warmup,
-                              profile_stage=dominant if S == 1 else None)
+                              profile_stage=dominant if S == 1 and K == 1 else None)
     frames_done = S * F * len(taus) * args.steps
     value = frames_done / total_ms * 1e3
 
     # roofline of the dominant kernel
     flops = args.steps * sum(stage_flops(dominant, m, Ml) for lv in levels for Ml in lv["Ml"])
     stage_ms, launches = st if st is not None else (0.0, 0)
-    if S > 1:   # concurrent streams: no single kernel's launches to time
+    if S > 1 or K > 1:   # concurrent streams: no single kernel's launches to time
         roof = None
     elif flops > 0:
         achieved = flops / (stage_ms * 1e-3) / 1e12
@@ -622,6 +645,9 @@ def main():
                                   if args.stream_chunk else "")
                                + (f"{S} concurrent streams (one handle and HIP stream each, "
                                   f"each encoding the batch); " if S > 1 else "")
+                               + (f"split into {K} concurrent parts of {part} frames (one "
+                                  f"handle, batches of {part_cap}, and one HIP stream each); "
+                                  if K > 1 else "")
                                + "reuse levels "
                                + "/".join(f"{t:.0%}" for t in targets if t is not None),
                    "frames_per_step": S * F * len(taus), "group_size": G},

@@ -174,6 +174,34 @@ def test_batching_and_determinism_bitwise():
         assert np.array_equal(cat, ref[k])
 
 
+def test_concurrent_handles_on_two_streams_bitwise():
+    """Groups are independent: two handles encoding the two halves of a clip at the same time on
+    two HIP streams give, bit for bit, the tokens, masks and embeddings of one encode of the whole
+    clip (each handle owns its workspace; the kernels of the two streams overlap on the GPU)."""
+    torch = require_gpu()
+    m = N257_BF16
+    blob = synth.make_blob(m, 29)
+    fr = dev(_video(m, 32, seed=11, pan=0.5))
+    whole = encoder(m, blob, 32)
+    halves = [encoder(m, blob, 16), encoder(m, blob, 16)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    ref = [host(t) for t in whole.encode(fr, 4, 0.9, want_tokens=True)]
+    for _ in range(3):
+        cur = torch.cuda.current_stream()
+        outs = []
+        for k, (e, st) in enumerate(zip(halves, streams)):
+            st.wait_stream(cur)
+            with torch.cuda.stream(st):
+                outs.append(e.encode(fr[16 * k:16 * (k + 1)], 4, 0.9, want_tokens=True, stream=st))
+        for st in streams:
+            cur.wait_stream(st)
+        torch.cuda.synchronize()
+        for j in range(3):
+            cat = np.concatenate([host(outs[0][j]), host(outs[1][j])])
+            assert np.array_equal(cat, ref[j])
+    assert 0 < ref[1][4:].mean() < 1, "the clip should mix reused and recomputed tokens"
+
+
 @pytest.mark.parametrize("m,n,G", [(TINY.model, 7, 4), (SMALL_BF16, 9, 4), (SMALL_BF16, 1, 4),
                                    (MID_BF16, 10, 3), (N257_BF16, 6, 4), (N577_BF16, 3, 2),
                                    (DH80_BF16, 5, 4)],
