@@ -3,14 +3,16 @@
 Workload (default): ViT-L/14 at 224 px (257 tokens, depth 24, width 1024, 16 heads, MLP
 4096, bf16 operands, fp32 accumulate), a batch of 256 synthetic video frames (6 moving
 squares, 1 px/frame camera pan, pixel noise sigma 0.02) in groups of 8 frames.  The
-reuse threshold tau is calibrated on the batch to 50 %, 70 % and 90 % reuse.
+reuse thresholds are the operating points for 50 %, 70 % and 90 % reuse calibrated with the
+CPU oracle (tests/golden/operating_points.json).
 
 One step = one encode of the batch at each of the three reuse levels (768 frames),
 inputs already resident in device memory.  `value` = frames encoded per second over
 the timed steps.  The line also carries each level's frames/s, the same kernels with
 reuse off (tau = -inf) and the speedup over it, the roofline of the dominant kernel
-(timed with HIP events on the encode stream over the timed region), and the CPU oracle
-timed on a bounded sample of the same frames.
+(timed with HIP events on the encode stream over the timed region) against the nominal
+peak and against the MFMA rate measured on the chip, and the CPU oracle timed on a bounded
+sample of the same frames.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
 """
@@ -297,6 +299,44 @@ def cpu_baseline(w, blob, frames, taus, groups_per_level=2):
                                 f"{td:.1f} s"}}
 
 
+def measured_peaks():
+    """What this chip sustains, beside its nominal peaks: the library's MFMA-loop probe (four
+    independent v_mfma_f32_32x32x16_bf16 chains of random register operands per wavefront, two
+    blocks of four wavefronts per CU, all resident at once, no memory traffic) and a 1 GiB
+    device-to-device copy (bytes read + written), best of three timed launches each, outside
+    the timed region."""
+    import torch
+    from paper_2506_14107_amd.dejavu import dv_mfma_probe
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = 2 * cus
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    cur = torch.cuda.current_stream()
+
+    def best(fn, work):
+        fn()
+        torch.cuda.synchronize()
+        rates = []
+        for _ in range(3):
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record()
+            fn()
+            e.record()
+            torch.cuda.synchronize()
+            rates.append(work / (s.elapsed_time(e) * 1e-3))
+        return max(rates)
+
+    iters = 40000
+    flops = dv_mfma_probe(blocks, iters, sink.data_ptr(), cur.cuda_stream)
+    mfma = best(lambda: dv_mfma_probe(blocks, iters, sink.data_ptr(), cur.cuda_stream), flops)
+    src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    copy = best(lambda: dst.copy_(src), 2.0 * src.numel() * 4)
+    del src, dst, sink
+    return {"mfma_bf16_tflops": round(mfma / 1e12, 1), "hbm_copy_gbs": round(copy / 1e9, 1),
+            "how": f"MFMA-loop probe ({blocks} blocks x 4 wavefronts x {iters} rounds of 4 "
+                   "independent 32x32x16 bf16 chains of random operands) and a 1 GiB device copy, best of 3"}
+
+
 def operating_points(name):
     """Thresholds of the workload's reuse levels from the fixture the parity tests use
     (calibrated with the CPU oracle by tests/golden/make_operating_points.py), or None."""
@@ -546,6 +586,10 @@ def main():
     frames_done = S * F * len(taus) * args.steps
     value = frames_done / total_ms * 1e3
 
+    peaks = measured_peaks()
+    log(f"[bench] measured peaks: {peaks['mfma_bf16_tflops']} TFLOP/s bf16 MFMA loop, "
+        f"{peaks['hbm_copy_gbs']} GB/s device copy")
+
     # roofline of the dominant kernel
     flops = args.steps * sum(stage_flops(dominant, m, Ml) for lv in levels for Ml in lv["Ml"])
     stage_ms, launches = st if st is not None else (0.0, 0)
@@ -557,6 +601,9 @@ def main():
         algo_b = args.steps * sum(stage_bytes(dominant, m, Ml) for lv in levels for Ml in lv["Ml"])
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": measured_traffic(dominant),
+                "measured_peak": peaks["mfma_bf16_tflops"] if m.dtype == "bf16" else None,
+                "frac_of_measured_peak": round(achieved / peaks["mfma_bf16_tflops"], 4)
+                if m.dtype == "bf16" else None,
                 "kernel": dominant, "launches": launches,
                 "avg_launch_us": round(stage_ms / max(launches, 1) * 1e3, 2),
                 "algo_flops_per_launch": round(flops / max(launches, 1)),
@@ -656,6 +703,7 @@ def main():
         "roofline": roof,
         "stages": stages,
         "cpu_baseline": cpu,
+        "measured_peaks": peaks,
         "workspace_bytes": dv_workspace_bytes(enc.handle),
     }
     print(json.dumps(out), flush=True)

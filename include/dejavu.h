@@ -309,6 +309,17 @@ int dv_profile(dv_handle* h, unsigned stage_mask);
 /* total_ms: summed event time of the stage's launches; launches: how many. */
 int dv_profile_read(dv_handle* h, int stage, double* total_ms, long long* launches);
 
+/* Measured MFMA ceiling (measurement support: the roofline of the packed GEMMs of Section 3.3 is
+ * also quoted against what the matrix cores sustain on this chip, not only the nominal peak).
+ * Enqueues on `stream` one launch of `blocks` blocks of four wavefronts; each wavefront runs
+ * `iters` rounds of four independent chains of v_mfma_f32_32x32x16_bf16 on random register
+ * operands, with no memory traffic, and stores one float per lane to `sink` (device,
+ * blocks*256 floats, caller-owned; the values are meaningless).  *flops (host) receives the
+ * FLOPs of the launch; time it with events on `stream`.  Two blocks per compute unit (two
+ * wavefronts per SIMD) are resident at once.
+ * Errors: DV_EINVAL (NULL sink or flops, blocks outside [1, 2^20], iters < 1), DV_EHIP. */
+int dv_mfma_probe(int blocks, int iters, float* sink, double* flops, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1208,6 +1208,14 @@ int dv_compact(const uint8_t* masks, int n_frames, int n_tokens, int group_size,
     return DV_OK;
 }
 
+int dv_mfma_probe(int blocks, int iters, float* sink, double* flops, hipStream_t stream) {
+    if (!sink || !flops) return fail(DV_EINVAL, "NULL argument");
+    if (blocks < 1 || iters < 1 || blocks > (1 << 20)) return fail(DV_EINVAL, "blocks in [1, 2^20], iters >= 1");
+    *flops = launch_mfma_loop(blocks, iters, sink, stream);
+    HIP_TRY(hipGetLastError());
+    return DV_OK;
+}
+
 int dv_profile(dv_handle* h, unsigned stage_mask) {
     if (!h) return fail(DV_EINVAL, "handle is NULL");
     int rc = collect(h);

@@ -95,6 +95,9 @@ __host__ __device__ inline int gemm_head_rows(int M, int Nout, int hbm, int hbn,
 }
 
 void launch_gemm(Epi e, bool bf16, const GemmArgs& a, hipStream_t s);
+// Measurement probe: `blocks` blocks of 256 threads run `iters` rounds of four independent bf16
+// MFMA chains; returns the FLOPs the launch performs.  sink: blocks*256 floats.
+double launch_mfma_loop(int blocks, int iters, float* sink, hipStream_t s);
 
 // ---- attention -------------------------------------------------------------------------------
 struct AttnArgs {

@@ -70,6 +70,8 @@ def load(path=None):
         "dv_stream_reset": (ctypes.c_int, [_P]),
         "dv_stream_held": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int)]),
         "dv_stream_flush": (ctypes.c_int, [_P, _P, _P, _P, _P]),
+        "dv_mfma_probe": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, _P,
+                                         ctypes.POINTER(ctypes.c_double), _P]),
         "dv_profile": (ctypes.c_int, [_P, ctypes.c_uint]),
         "dv_profile_read": (ctypes.c_int, [_P, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_longlong)]),
@@ -168,6 +170,13 @@ def dv_stream_flush(handle, out_embeddings, out_masks, out_tokens, stream):
 def dv_compact(masks, n_frames, n_tokens, group_size, idx, pos, qoff, count, stream):
     _check(load().dv_compact(masks, n_frames, n_tokens, group_size, idx, pos, qoff, count,
                              stream))
+
+
+def dv_mfma_probe(blocks, iters, sink, stream):
+    """Enqueues the MFMA-loop probe; returns the FLOPs of the launch."""
+    fl = ctypes.c_double()
+    _check(load().dv_mfma_probe(blocks, iters, sink, ctypes.byref(fl), stream))
+    return fl.value
 
 
 DV_PROFILE_ALL = 0x3FFF

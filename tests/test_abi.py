@@ -132,6 +132,17 @@ def test_compact_rejects_bad_arguments():
     assert lib.dv_compact(1, 1 << 16, 1 << 16, 1, 1, 1, 1, 1, None) == dj.DV_EINVAL
 
 
+def test_mfma_probe_rejects_bad_arguments():
+    """Host validation only (no launch on error)."""
+    lib = dj.load()
+    fl = ctypes.c_double()
+    assert lib.dv_mfma_probe(1, 1, None, ctypes.byref(fl), None) == dj.DV_EINVAL
+    assert lib.dv_mfma_probe(1, 1, 1, None, None) == dj.DV_EINVAL
+    assert lib.dv_mfma_probe(0, 1, 1, ctypes.byref(fl), None) == dj.DV_EINVAL
+    assert lib.dv_mfma_probe(1, 0, 1, ctypes.byref(fl), None) == dj.DV_EINVAL
+    assert lib.dv_mfma_probe((1 << 20) + 1, 1, 1, ctypes.byref(fl), None) == dj.DV_EINVAL
+
+
 def test_profile_calls_reject_null_handle():
     lib = dj.load()
     ms, n = ctypes.c_double(), ctypes.c_longlong()
