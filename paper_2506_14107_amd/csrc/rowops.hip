@@ -8,8 +8,8 @@ namespace dv {
 namespace {
 
 constexpr int WAVE = 64;
-// float4 chunks of a row held per lane by the row kernels (template CK): 4 for D <= 1024, 8 for
-// D <= 2048
+// float4 chunks of a row held per lane by the row kernels (template CK): 4 for D <= 1024, 5 for
+// D <= 1280, 8 for D <= 2048
 
 // Sum over the 64 lanes, in every lane: DPP steps within rows of 16 lanes (quad swaps, then the
 // half-row and row mirrors), one LDS shuffle across rows, and the permlane32 swap across the two
@@ -739,33 +739,28 @@ void launch_cls_init(float* x, const float* cls, const float* pos, int F, int N,
                        pos, F, N, D);
 }
 
+template <int CK>
+void launch_gate_ck(int v, dim3 grid, dim3 block, const GateArgs& a, hipStream_t s) {
+    switch (v) {
+        case 0: hipLaunchKernelGGL((gate_k<false, false, false, CK>), grid, block, 0, s, a); break;
+        case 1: hipLaunchKernelGGL((gate_k<false, false, true, CK>), grid, block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((gate_k<false, true, false, CK>), grid, block, 0, s, a); break;
+        case 3: hipLaunchKernelGGL((gate_k<false, true, true, CK>), grid, block, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((gate_k<true, false, false, CK>), grid, block, 0, s, a); break;
+        case 5: hipLaunchKernelGGL((gate_k<true, false, true, CK>), grid, block, 0, s, a); break;
+        case 6: hipLaunchKernelGGL((gate_k<true, true, false, CK>), grid, block, 0, s, a); break;
+        default: hipLaunchKernelGGL((gate_k<true, true, true, CK>), grid, block, 0, s, a); break;
+    }
+}
+
 void launch_gate(bool bf16, const GateArgs& a, hipStream_t s) {
     const dim3 grid(a.F * gate_chunks(a.N)), block(256);
     const bool dec = a.dec != nullptr && a.mode == GATE_COS;
     const int v = (bf16 ? 4 : 0) + (dec ? 2 : 0) + (a.reorder ? 1 : 0);
-    if (a.D <= 1024) {   // at most 4 float4 chunks per lane: half the registers, twice the waves
-        switch (v) {
-            case 0: hipLaunchKernelGGL((gate_k<false, false, false, 4>), grid, block, 0, s, a); break;
-            case 1: hipLaunchKernelGGL((gate_k<false, false, true, 4>), grid, block, 0, s, a); break;
-            case 2: hipLaunchKernelGGL((gate_k<false, true, false, 4>), grid, block, 0, s, a); break;
-            case 3: hipLaunchKernelGGL((gate_k<false, true, true, 4>), grid, block, 0, s, a); break;
-            case 4: hipLaunchKernelGGL((gate_k<true, false, false, 4>), grid, block, 0, s, a); break;
-            case 5: hipLaunchKernelGGL((gate_k<true, false, true, 4>), grid, block, 0, s, a); break;
-            case 6: hipLaunchKernelGGL((gate_k<true, true, false, 4>), grid, block, 0, s, a); break;
-            default: hipLaunchKernelGGL((gate_k<true, true, true, 4>), grid, block, 0, s, a); break;
-        }
-        return;
-    }
-    switch (v) {
-        case 0: hipLaunchKernelGGL((gate_k<false, false, false, 8>), grid, block, 0, s, a); break;
-        case 1: hipLaunchKernelGGL((gate_k<false, false, true, 8>), grid, block, 0, s, a); break;
-        case 2: hipLaunchKernelGGL((gate_k<false, true, false, 8>), grid, block, 0, s, a); break;
-        case 3: hipLaunchKernelGGL((gate_k<false, true, true, 8>), grid, block, 0, s, a); break;
-        case 4: hipLaunchKernelGGL((gate_k<true, false, false, 8>), grid, block, 0, s, a); break;
-        case 5: hipLaunchKernelGGL((gate_k<true, false, true, 8>), grid, block, 0, s, a); break;
-        case 6: hipLaunchKernelGGL((gate_k<true, true, false, 8>), grid, block, 0, s, a); break;
-        default: hipLaunchKernelGGL((gate_k<true, true, true, 8>), grid, block, 0, s, a); break;
-    }
+    // as few float4 chunks per lane as the row needs: fewer registers, more waves per SIMD
+    if (a.D <= 1024) launch_gate_ck<4>(v, grid, block, a, s);
+    else if (a.D <= 1280) launch_gate_ck<5>(v, grid, block, a, s);
+    else launch_gate_ck<8>(v, grid, block, a, s);
 }
 
 void launch_count(const uint8_t* m, int F, int N, int G, int* cnt, hipStream_t s) {
@@ -813,8 +808,8 @@ void launch_ln_rows(bool bf16, const float* src, const int* gather, const int* M
                     int D, const float* g, const float* b, void* dst, hipStream_t s) {
     const int grid = grid_for((size_t)Mmax, 4, 65536);
     // rows of at most 1024 values: 4 float4 chunks per lane in registers, else up to 8
-    auto k = bf16 ? (D <= 1024 ? ln_rows_k<true, 4> : ln_rows_k<true, 8>)
-                  : (D <= 1024 ? ln_rows_k<false, 4> : ln_rows_k<false, 8>);
+    auto k = bf16 ? (D <= 1024 ? ln_rows_k<true, 4> : D <= 1280 ? ln_rows_k<true, 5> : ln_rows_k<true, 8>)
+                  : (D <= 1024 ? ln_rows_k<false, 4> : D <= 1280 ? ln_rows_k<false, 5> : ln_rows_k<false, 8>);
     hipLaunchKernelGGL(k, dim3(grid), dim3(256), 0, s, src, gather, Mdev, Mmax, D, g, b, dst);
 }
 

@@ -23,6 +23,10 @@ N577_BF16 = ModelConfig(336, 14, 1, 128, 2, 256, "bf16")
 DH80_BF16 = ModelConfig(64, 16, 2, 640, 8, 1280, "bf16")
 # head dim 80 with two key blocks per frame (N = 50): the per-frame attention kernel
 DH80_N50 = ModelConfig(112, 16, 2, 640, 8, 1280, "bf16")
+# widths past 1024 that the row kernels hold as five float4 chunks per lane: 1152 (the last
+# chunk on half of the lanes) and 1280 (the ViT-H/14-class width)
+W1152_BF16 = ModelConfig(64, 16, 2, 1152, 18, 2304, "bf16")
+W1280_BF16 = ModelConfig(64, 16, 2, 1280, 16, 2560, "bf16")
 
 
 def _video(m, n, seed=2000, sigma=0.01, speed=3.0, n_obj=2, size=None, pan=0.0):
@@ -240,8 +244,9 @@ def test_single_token_injection():
     check_close(t, r["tokens"], "bf16", "tokens")
 
 
-@pytest.mark.parametrize("m", [SMALL_BF16, MID_BF16, N257_BF16, DH80_BF16],
-                         ids=["small", "mid", "n257", "dh80"])
+@pytest.mark.parametrize("m", [SMALL_BF16, MID_BF16, N257_BF16, DH80_BF16, W1152_BF16,
+                               W1280_BF16],
+                         ids=["small", "mid", "n257", "dh80", "w1152", "w1280"])
 def test_bf16_gate_mode_parity(m):
     torch = require_gpu()
     blob = synth.make_blob(m, 26)
