@@ -368,8 +368,8 @@ def render(video, S, n, workers=8):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="vit_l14")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--frames", type=int, default=0,
@@ -559,30 +559,32 @@ def main():
         torch.cuda.synchronize()
         if profile_stage:
             enc.profile([profile_stage])
-        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        s.record()
-        for _ in range(steps):
+        # an event after every step: the whole region's time and each step's
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        evs[0].record()
+        for k in range(steps):
             for tau in tau_list:
                 encode_all(tau)
-        e.record()
+            evs[k + 1].record()
         torch.cuda.synchronize()
-        ms = s.elapsed_time(e)
+        ms = evs[0].elapsed_time(evs[-1])
+        per_step = [evs[k].elapsed_time(evs[k + 1]) for k in range(steps)]
         st = None
         if profile_stage:
             st = enc.profile_read()[profile_stage]
             enc.profile(False)
-        return ms, st
+        return ms, st, per_step
 
     per_level = []
     for lv in levels:
-        ms, _ = time_calls([lv["tau"]], max(2, args.steps), 1)
+        ms, _, _ = time_calls([lv["tau"]], max(2, args.steps), 1)
         per_level.append(S * F * max(2, args.steps) / ms * 1e3)
-    dense_ms, _ = time_calls([float("-inf")], max(2, args.steps), 1)
+    dense_ms, _, _ = time_calls([float("-inf")], max(2, args.steps), 1)
     dense_fps = S * F * max(2, args.steps) / dense_ms * 1e3
 
     # the timed region: K steps of the whole sweep, dominant stage timed with HIP events
-    total_ms, st = time_calls(taus, args.steps, args.warmup,
-                              profile_stage=dominant if S == 1 and K == 1 else None)
+    total_ms, st, step_ms = time_calls(taus, args.steps, args.warmup,
+                                       profile_stage=dominant if S == 1 and K == 1 else None)
     frames_done = S * F * len(taus) * args.steps
     value = frames_done / total_ms * 1e3
 
@@ -677,6 +679,8 @@ def main():
                   + " reuse; packed-GEMM MFMA util; speedup vs dense",
         "value": round(value, 2), "unit": "frames/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(total_ms / args.steps, 3),
+        "step_ms": {"median": round(float(np.median(step_ms)), 3),
+                    "min": round(min(step_ms), 3), "max": round(max(step_ms), 3)},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if m.dtype == "bf16" else "f32", "data": "synthetic",
         "config": {"workload": f"{w.name}: {m.image_size}px patch {m.patch} ({N} tokens), depth "
