@@ -9,7 +9,8 @@ tests/golden/make_operating_points.py; the bench runs at the same thresholds).  
 groups are recomputed by the CPU oracle replaying the GPU's reuse maps (teacher-forced
 decisions, then embeddings and the full last-layer token buffers to the bf16 bar: min cosine
 >= 0.999, per-frame relative error <= 2e-2).  With reuse off (tau = -inf) sampled groups are
-checked against the separately written dense ViT instead.
+checked against the separately written dense ViT instead.  One ViT-L/14 encode runs the largest
+batch a handle accepts (2039 frames), where the buffers reach the 32-bit offset bound.
 """
 import dataclasses
 import json
@@ -89,6 +90,49 @@ def test_full_size_parity(name, target, tau):
               f"rel {r_t:.2e}", flush=True)
         assert bad == 0, f"{bad} decisions differ outside the 1e-3 band"
         assert inside <= BAND_MAX, f"{inside:.1%} of the decisions inside the band"
+    enc.close()
+
+
+def test_largest_batch_the_handle_accepts():
+    """ViT-L/14 in one batch of 2039 frames, the largest whose workspace buffers all stay below
+    2^32 bytes (the MLP hidden rows, 524032 x 4096 bf16; one frame more is rejected, see
+    test_abi.py): the kernels address the far ends of every buffer with 32-bit offsets.  The
+    last two groups (8 frames, then a short group of 7) must come out bit for bit as they do
+    encoded on their own, and match the oracle replaying their reuse maps.  The clip is the
+    first 256 frames repeated (groups are independent, so any content serves)."""
+    torch = require_gpu()
+    name, B = "vit_l14", 2039
+    w, blob, fr256 = _inputs(name, 256)
+    m, G = w.model, w.group_size
+    fr = np.ascontiguousarray(np.concatenate([fr256] * 8)[:B])
+    tau = float(np.float32(OPS[name]["levels"][0]["tau"]))
+    enc = encoder(m, blob, B)
+    emb, masks, toks = enc.encode(dev(fr), G, tau, want_tokens=True)
+    torch.cuda.synchronize()
+    tail = slice(2024, B)
+    e_big, m_big, t_big = host(emb[tail]), host(masks[tail]), host(toks[tail])
+    del emb, toks
+    mg = host(masks)
+    print(f"[{name} batch {B}] GPU reuse {oracle.reuse_rate(mg, G):.4f}", flush=True)
+    small = encoder(m, blob, 16)
+    e_s, m_s, t_s = small.encode(dev(fr[tail]), G, tau, want_tokens=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(m_s), m_big), "maps differ from the same groups encoded alone"
+    assert np.array_equal(host(e_s), e_big), "embeddings differ from the same groups alone"
+    assert np.array_equal(host(t_s), t_big), "tokens differ from the same groups alone"
+    for g0 in (2024, 2032):
+        sl = slice(g0, min(g0 + G, B))
+        loc = slice(g0 - 2024, sl.stop - 2024)
+        t1 = time.time()
+        r = oracle.encode(fr[sl], blob, m.as_dict(), G, masks=m_big[loc])
+        bad, inside = mask_parity(m_big[loc], r["cos"], tau)
+        c_e, r_e = check_close(e_big[loc], r["emb"], "bf16", f"group {g0} embeddings")
+        c_t, r_t = check_close(t_big[loc], r["tokens"], "bf16", f"group {g0} tokens")
+        print(f"[{name} batch {B}] group {g0}: oracle {time.time() - t1:.1f}s, decisions off "
+              f"{bad}, in band {inside:.2%}, emb cos {c_e:.5f} rel {r_e:.2e}, tok cos {c_t:.5f} "
+              f"rel {r_t:.2e}", flush=True)
+        assert bad == 0, f"{bad} decisions differ outside the 1e-3 band"
+    small.close()
     enc.close()
 
 
