@@ -178,6 +178,42 @@ def test_batching_and_determinism_bitwise():
         assert np.array_equal(cat, ref[k])
 
 
+def test_live_handle_rejects_bad_arguments_without_launching():
+    """A live handle rejects an empty or negative frame count, a group size of 0 or above the
+    batch, a NaN tau and NULL buffers with DV_EINVAL, on the host: the output buffer keeps its
+    sentinel, and the handle encodes normally afterwards."""
+    torch = require_gpu()
+    from paper_2506_14107_amd import dejavu as dj
+    m = SMALL_BF16
+    blob = synth.make_blob(m, 30)
+    enc = encoder(m, blob, 8)
+    fr = dev(_video(m, 8, seed=3))
+    emb = torch.full((8, m.width), 7.0, dtype=torch.float32, device="cuda")
+    msk = torch.zeros((8, m.depth, m.n_tokens), dtype=torch.uint8, device="cuda")
+    lib, h = dj.load(), enc.handle
+    s = torch.cuda.current_stream().cuda_stream
+    f, e = fr.data_ptr(), emb.data_ptr()
+    rcs = {
+        "empty batch": lib.dv_encode(h, f, 0, 4, 0.9, e, None, s),
+        "negative count": lib.dv_encode(h, f, -3, 4, 0.9, e, None, s),
+        "group size 0": lib.dv_encode(h, f, 8, 0, 0.9, e, None, s),
+        "group above the batch": lib.dv_encode(h, f, 8, 9, 0.9, e, None, s),
+        "NaN tau": lib.dv_encode(h, f, 8, 4, float("nan"), e, None, s),
+        "NULL frames": lib.dv_encode(h, None, 8, 4, 0.9, e, None, s),
+        "NULL embeddings": lib.dv_encode(h, f, 8, 4, 0.9, None, None, s),
+        "NULL injected maps": lib.dv_encode_masked(h, f, 8, 4, None, e, None, s),
+        "empty injected batch": lib.dv_encode_masked(h, f, 0, 4, msk.data_ptr(), e, None, s),
+    }
+    torch.cuda.synchronize()
+    bad = {k: rc for k, rc in rcs.items() if rc != dj.DV_EINVAL}
+    assert not bad, f"expected DV_EINVAL: {bad}"
+    assert bool(torch.all(emb == 7.0)), "a rejected call wrote the output"
+    a, _, _ = enc.encode(fr, 4, 0.9)
+    b, _, _ = enc.encode(fr, 4, 0.9)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(a), host(b)) and np.isfinite(host(a)).all()
+
+
 def test_concurrent_handles_on_two_streams_bitwise():
     """Groups are independent: two handles encoding the two halves of a clip at the same time on
     two HIP streams give, bit for bit, the tokens, masks and embeddings of one encode of the whole
