@@ -133,8 +133,9 @@ __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, co
     const int tr_key = hl * 4 + (gi >> 2);
     const int tr_dim = (grp & 1) * 16 + (gi & 3) * 4;
 
-    // scores of key block kb against the query tile (raw, unscaled)
-    auto scores = [&](int kb) {
+    // scores of key block kb against the query tile (raw, unscaled); MK: the block may hold
+    // keys past N
+    auto scores = [&](int kb, auto mk) {
         f32x16 sc;
 #pragma unroll
         for (int r = 0; r < 16; ++r) sc[r] = 0.f;
@@ -144,7 +145,7 @@ __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, co
             const bf16x8 kf = *(const bf16x8*)(Ks + g.kofs(row, ks * 2 + hl));
             sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc, 0, 0, 0);
         }
-        if ((kb + 1) * 32 > N) {   // ragged last block: keys past N get -inf
+        if (decltype(mk)::value && (kb + 1) * 32 > N) {   // ragged last block: keys past N get -inf
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int key = kb * 32 + (r >> 2) * 8 + hl * 4 + (r & 3);
@@ -185,14 +186,18 @@ __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, co
         for (int r = 0; r < 16; ++r) o[b][r] = 0.f;
     m = -INFINITY;
     l = 0.f;
-    for (int kb = 0; kb < nkb; kb += 2) {
+    // One softmax step over key blocks kb and kb + 1.  MK: the step may hold the ragged last
+    // block or no second block; only the loop's tail steps do, so the others carry no per-key
+    // test (the arithmetic and its order are the same either way).
+    auto step = [&](int kb, auto mk) {
+        constexpr bool MK = decltype(mk)::value;
         stage(kb);
         const int kb1 = kb + 1;
-        const bool two = kb1 < nkb;
-        const f32x16 s0 = scores(kb);
+        const bool two = !MK || kb1 < nkb;
+        const f32x16 s0 = scores(kb, mk);
         f32x16 s1;
         if (two) {
-            s1 = scores(kb1);
+            s1 = scores(kb1, mk);
         } else {
 #pragma unroll
             for (int r = 0; r < 16; ++r) s1[r] = -INFINITY;
@@ -225,7 +230,11 @@ __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, co
         l += ps + other_half(ps);
         accumulate(kb, p0);
         if (two) accumulate(kb1, p1);
-    }
+    };
+    const int nfull = N / 32;   // key blocks with no key past N
+    int kb = 0;
+    for (; kb + 1 < nfull; kb += 2) step(kb, std::integral_constant<bool, false>());
+    for (; kb < nkb; kb += 2) step(kb, std::integral_constant<bool, true>());
 }
 
 // attend_tile for up to NQ query tiles of one frame at once (nq of them present): every step's
@@ -245,8 +254,9 @@ __device__ __forceinline__ void attend_tiles(const Geo& g, const uint16_t* Ks, c
     const int tr_key = hl * 4 + (gi >> 2);
     const int tr_dim = (grp & 1) * 16 + (gi & 3) * 4;
 
-    // scores of key block kb against the query tile (raw, unscaled)
-    auto scores = [&](int q, int kb) {
+    // scores of key block kb against the query tile (raw, unscaled); MK: the block may hold
+    // keys past N
+    auto scores = [&](int q, int kb, auto mk) {
         f32x16 sc;
 #pragma unroll
         for (int r = 0; r < 16; ++r) sc[r] = 0.f;
@@ -256,7 +266,7 @@ __device__ __forceinline__ void attend_tiles(const Geo& g, const uint16_t* Ks, c
             const bf16x8 kf = *(const bf16x8*)(Ks + g.kofs(row, ks * 2 + hl));
             sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[q][ks], sc, 0, 0, 0);
         }
-        if ((kb + 1) * 32 > N) {   // ragged last block: keys past N get -inf
+        if (decltype(mk)::value && (kb + 1) * 32 > N) {   // ragged last block: keys past N get -inf
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int key = kb * 32 + (r >> 2) * 8 + hl * 4 + (r & 3);
@@ -300,17 +310,19 @@ __device__ __forceinline__ void attend_tiles(const Geo& g, const uint16_t* Ks, c
         m[q] = -INFINITY;
         l[q] = 0.f;
     }
-    for (int kb = 0; kb < nkb; kb += 2) {
+    // one step over key blocks kb, kb + 1 for every tile; MK as in attend_tile
+    auto step = [&](int kb, auto mk) {
+        constexpr bool MK = decltype(mk)::value;
         stage(kb);
         const int kb1 = kb + 1;
-        const bool two = kb1 < nkb;
+        const bool two = !MK || kb1 < nkb;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             if (q >= nq) break;   // wave-uniform: the tile does not exist
-            const f32x16 s0 = scores(q, kb);
+            const f32x16 s0 = scores(q, kb, mk);
             f32x16 s1;
             if (two) {
-                s1 = scores(q, kb1);
+                s1 = scores(q, kb1, mk);
             } else {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) s1[r] = -INFINITY;
@@ -344,7 +356,11 @@ __device__ __forceinline__ void attend_tiles(const Geo& g, const uint16_t* Ks, c
             accumulate(q, kb, p0);
             if (two) accumulate(q, kb1, p1);
         }
-    }
+    };
+    const int nfull = N / 32;   // key blocks with no key past N
+    int kb = 0;
+    for (; kb + 1 < nfull; kb += 2) step(kb, std::integral_constant<bool, false>());
+    for (; kb < nkb; kb += 2) step(kb, std::integral_constant<bool, true>());
 }
 
 // o / l of a lane's query as bf16 to its output row (dims of this lane's register groups)
