@@ -202,9 +202,16 @@ __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, co
 #pragma unroll
             for (int r = 0; r < 16; ++r) s1[r] = -INFINITY;
         }
-        float bm = -INFINITY;
+        // block maximum and, below, the probability sum as pairwise trees (short dependency
+        // chains; the maximum is exact in any order)
+        float mx[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) bm = fmaxf(bm, fmaxf(s0[r], s1[r]));
+        for (int r = 0; r < 16; ++r) mx[r] = fmaxf(s0[r], s1[r]);
+#pragma unroll
+        for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+            for (int r = 0; r < w; ++r) mx[r] = fmaxf(mx[r], mx[r + w]);
+        float bm = mx[0];
         bm = fmaxf(bm, other_half(bm));
         if (__any(bm > m)) {   // rescale only when some lane's running max moved
             const float mn = fmaxf(m, bm);
@@ -217,16 +224,21 @@ __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, co
             m = mn;
         }
         const float nm = -m * sl2;
-        float ps = 0.f;
+        float sr[16];
         bf16x8 p0[2], p1[2];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], sl2, nm));
             const float e1 = __builtin_amdgcn_exp2f(fmaf(s1[r], sl2, nm));
-            ps += e0 + e1;
+            sr[r] = e0 + e1;
             p0[r >> 3][r & 7] = (__bf16)e0;
             p1[r >> 3][r & 7] = (__bf16)e1;
         }
+#pragma unroll
+        for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+            for (int r = 0; r < w; ++r) sr[r] += sr[r + w];
+        const float ps = sr[0];
         l += ps + other_half(ps);
         accumulate(kb, p0);
         if (two) accumulate(kb1, p1);
@@ -327,9 +339,14 @@ __device__ __forceinline__ void attend_tiles(const Geo& g, const uint16_t* Ks, c
 #pragma unroll
                 for (int r = 0; r < 16; ++r) s1[r] = -INFINITY;
             }
-            float bm = -INFINITY;
+            float mx[16];   // as in attend_tile: pairwise trees
 #pragma unroll
-            for (int r = 0; r < 16; ++r) bm = fmaxf(bm, fmaxf(s0[r], s1[r]));
+            for (int r = 0; r < 16; ++r) mx[r] = fmaxf(s0[r], s1[r]);
+#pragma unroll
+            for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+                for (int r = 0; r < w; ++r) mx[r] = fmaxf(mx[r], mx[r + w]);
+            float bm = mx[0];
             bm = fmaxf(bm, other_half(bm));
             if (__any(bm > m[q])) {   // rescale only when some lane's running max moved
                 const float mn = fmaxf(m[q], bm);
@@ -342,16 +359,21 @@ __device__ __forceinline__ void attend_tiles(const Geo& g, const uint16_t* Ks, c
                 m[q] = mn;
             }
             const float nm = -m[q] * sl2;
-            float ps = 0.f;
+            float sr[16];
             bf16x8 p0[2], p1[2];
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], sl2, nm));
                 const float e1 = __builtin_amdgcn_exp2f(fmaf(s1[r], sl2, nm));
-                ps += e0 + e1;
+                sr[r] = e0 + e1;
                 p0[r >> 3][r & 7] = (__bf16)e0;
                 p1[r >> 3][r & 7] = (__bf16)e1;
             }
+#pragma unroll
+            for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+                for (int r = 0; r < w; ++r) sr[r] += sr[r + w];
+            const float ps = sr[0];
             l[q] += ps + other_half(ps);
             accumulate(q, kb, p0);
             if (two) accumulate(q, kb1, p1);
