@@ -128,6 +128,7 @@ __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, co
     constexpr int DB = (DH + 31) / 32;   // 32-row blocks of O^T
     const int hl = lane >> 5, lr = lane & 31;
     const float sl2 = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(dh)
+    const float lazy = 8.0f / sl2;    // raw score units of a factor 2^8
     const int nkb = g.npad / 32;
     const int grp = lane >> 4, gi = lane & 15;    // 16-lane group of the transposing read
     const int tr_key = hl * 4 + (gi >> 2);
@@ -213,7 +214,10 @@ __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, co
             for (int r = 0; r < w; ++r) mx[r] = fmaxf(mx[r], mx[r + w]);
         float bm = mx[0];
         bm = fmaxf(bm, other_half(bm));
-        if (__any(bm > m)) {   // rescale only when some lane's running max moved
+        // rescale only when some lane's block maximum passes its reference maximum m by more
+        // than 8 in log2 units: probabilities stay below 2^8 (far inside the range of the fp32
+        // sums and bf16 products), and most steps after the first keep their scale
+        if (__any(bm > m + lazy)) {
             const float mn = fmaxf(m, bm);
             const float alpha = __builtin_amdgcn_exp2f((m - mn) * sl2);
             l *= alpha;
@@ -261,6 +265,7 @@ __device__ __forceinline__ void attend_tiles(const Geo& g, const uint16_t* Ks, c
     constexpr int DB = (DH + 31) / 32;   // 32-row blocks of O^T
     const int hl = lane >> 5, lr = lane & 31;
     const float sl2 = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(dh)
+    const float lazy = 8.0f / sl2;    // raw score units of a factor 2^8
     const int nkb = g.npad / 32;
     const int grp = lane >> 4, gi = lane & 15;    // 16-lane group of the transposing read
     const int tr_key = hl * 4 + (gi >> 2);
@@ -348,7 +353,7 @@ __device__ __forceinline__ void attend_tiles(const Geo& g, const uint16_t* Ks, c
                 for (int r = 0; r < w; ++r) mx[r] = fmaxf(mx[r], mx[r + w]);
             float bm = mx[0];
             bm = fmaxf(bm, other_half(bm));
-            if (__any(bm > m[q])) {   // rescale only when some lane's running max moved
+            if (__any(bm > m[q] + lazy)) {   // as in attend_tile
                 const float mn = fmaxf(m[q], bm);
                 const float alpha = __builtin_amdgcn_exp2f((m[q] - mn) * sl2);
                 l[q] *= alpha;
