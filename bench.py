@@ -110,10 +110,13 @@ KERNEL_SOURCE = {"qkv": "gemm.hip", "oproj": "gemm.hip", "fc1": "gemm.hip", "fc2
                  "ln2": "rowops.hip", "compact": "rowops.hip"}
 
 
-def measured_traffic(stage):
+def measured_traffic(stage, recorded_config):
     """HBM bytes per launch of `stage` from the committed counter record, if it was taken from
-    the current kernel source; else None."""
+    the current kernel source and this run is the configuration it was taken on (the default
+    ViT-L/14 sweep: `recorded_config`); else None."""
     import hashlib
+    if not recorded_config:
+        return None
     rec = os.path.join(ROOT, "profiles", f"{stage}_hbm_traffic.json")
     src = KERNEL_SOURCE.get(stage)
     if not src or not os.path.exists(rec):
@@ -602,7 +605,10 @@ def main():
         peak = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_FP32_TFLOPS
         algo_b = args.steps * sum(stage_bytes(dominant, m, Ml) for lv in levels for Ml in lv["Ml"])
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": measured_traffic(dominant),
+                "frac": round(achieved / peak, 4),
+                "traffic": measured_traffic(dominant, w.name == "vit_l14" and not (
+                    args.frames or args.restore or args.decision or args.reorder
+                    or args.stream_chunk)),
                 "measured_peak": peaks["mfma_bf16_tflops"] if m.dtype == "bf16" else None,
                 "frac_of_measured_peak": round(achieved / peaks["mfma_bf16_tflops"], 4)
                 if m.dtype == "bf16" else None,
