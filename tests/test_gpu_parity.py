@@ -214,6 +214,28 @@ def test_live_handle_rejects_bad_arguments_without_launching():
     assert np.array_equal(host(a), host(b)) and np.isfinite(host(a)).all()
 
 
+def test_mfma_probe_counts_its_work():
+    """The MFMA-loop probe (measurement support) reports the FLOPs its launch performs (4 chains
+    of 32x32x16 MFMAs, 32768 FLOP each, per wavefront and round), every lane writes a finite
+    value to the sink, and the rate it implies is a plausible fraction of the nominal peak."""
+    torch = require_gpu()
+    from paper_2506_14107_amd.dejavu import dv_mfma_probe
+    blocks, iters = 512, 2000
+    sink = torch.full((blocks * 256,), float("nan"), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    flops = dv_mfma_probe(blocks, iters, sink.data_ptr(), stream.cuda_stream)
+    assert flops == blocks * 4 * 4 * iters * 32768
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(sink).all())
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    dv_mfma_probe(blocks, iters, sink.data_ptr(), stream.cuda_stream)
+    e.record()
+    torch.cuda.synchronize()
+    tflops = flops / (s.elapsed_time(e) * 1e-3) / 1e12
+    assert 200 < tflops < 2600, f"{tflops:.0f} TFLOP/s"
+
+
 def test_concurrent_handles_on_two_streams_bitwise():
     """Groups are independent: two handles encoding the two halves of a clip at the same time on
     two HIP streams give, bit for bit, the tokens, masks and embeddings of one encode of the whole
