@@ -79,19 +79,25 @@ struct GemmArgs {
     // the others small tiles over [head, M), head = gemm_head_rows(M, Nout, BM, BN, slots);
     // slots = 0: one tiling for all rows
     int slots, head_grid;
+    bool mid_tail;       // a partial round of a quarter to half of the grid goes to 128 x 128 tiles
 };
 
 // Rows that large tiles take when the M rows are split between large tiles (hbm x hbn, `slots`
 // resident blocks) and small ones: the tile rows that fill whole rounds of the large-tile grid.
-// A remainder of more than a quarter of a round, or none, keeps every row in large tiles.  Each
-// output is the same dot product in the same k order in either tiling, so the split does not
-// change results.
-__host__ __device__ inline int gemm_head_rows(int M, int Nout, int hbm, int hbn, int slots) {
+// *kind: 1 for a remainder of at most a quarter of a round (64 x 64 tiles), 2 for at most half
+// a round when `mid` (128 x 128 tiles), 0 when every row stays in large tiles (no remainder, or
+// a larger one).  Each output is the same dot product in the same k order in any tiling, so the
+// split does not change results.
+__host__ __device__ inline int gemm_head_rows(int M, int Nout, int hbm, int hbn, int slots,
+                                              int* kind = nullptr, bool mid = false) {
     const int tn = Nout / hbn;
     const int mt = (M + hbm - 1) / hbm;
     const int mA = (mt * tn / slots) * slots / tn;   // whole tile rows inside the full rounds
-    if (mA == mt || (mt - mA) * tn * 4 > slots) return M;
-    return mA * hbm;
+    const int rem = (mt - mA) * tn;                  // large tiles of the partial round
+    int k = 0;
+    if (mA < mt) k = rem * 4 <= slots ? 1 : (mid && rem * 2 <= slots) ? 2 : 0;
+    if (kind) *kind = k;
+    return k ? mA * hbm : M;
 }
 
 void launch_gemm(Epi e, bool bf16, const GemmArgs& a, hipStream_t s);

@@ -446,11 +446,17 @@ constexpr size_t pipe_lds_bytes() {
 // slices in 3 or 8 stages measured slower), one per group of four wavefronts.
 constexpr int TBM = 64, TBN = 64, TBK = 64, TS = 4;
 constexpr size_t TAIL_LDS = pipe_lds_bytes<TBM, TBN, TBK, TS, 2, 2>();
+// Middle tail tiles (a partial round of a quarter to half of the grid): 128 x 128, a 2-stage
+// ring of 64-deep slices, one per group of four wavefronts.
+constexpr int MBM = 128, MBN = 128, MBK = 64, MS = 2;
+constexpr size_t MID_LDS = pipe_lds_bytes<MBM, MBN, MBK, MS, 2, 2>();
 
 // Block tiles BM x BN of WGM x WGN wavefronts.  With a.slots set, the launch is split: blocks
 // below a.head_grid take the rows [0, head) that fill whole rounds of the grid
-// (gemm_head_rows), and the blocks after them cut the remaining rows into 64 x 64 tiles, one per
-// group of four wavefronts, so that the last, partial round spreads over many compute units.
+// (gemm_head_rows), and the blocks after them cut the remaining rows into 64 x 64 tiles (a
+// partial round of at most a quarter of the grid) or 128 x 128 tiles (at most half, with
+// a.mid_tail), one per group of four wavefronts, so that the last, partial round spreads over
+// many compute units.
 template <Epi E, int BM, int BN, int BKD, int S, int WPE, int WGM, int WGN>
 __global__ __launch_bounds__(WGM * WGN * 64) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void gemm_bf16_pipe_k(GemmArgs a) {
@@ -462,7 +468,8 @@ void gemm_bf16_pipe_k(GemmArgs a) {
         pipe_tile<E, BM, BN, BKD, S, WGM, WGN>(a, (uint16_t*)smem, blockIdx.x, 0, M, wave);
         return;
     }
-    const int head = gemm_head_rows(M, a.Nout, BM, BN, a.slots);
+    int kind = 0;
+    const int head = gemm_head_rows(M, a.Nout, BM, BN, a.slots, &kind, a.mid_tail);
     if ((int)blockIdx.x < a.head_grid) {
         pipe_tile<E, BM, BN, BKD, S, WGM, WGN>(a, (uint16_t*)smem, blockIdx.x, 0, head, wave);
         return;
@@ -470,14 +477,18 @@ void gemm_bf16_pipe_k(GemmArgs a) {
     static_assert(NW % 4 == 0, "tail tiles take groups of four wavefronts");
     const int grp = wave / 4;
     const int tb = ((int)blockIdx.x - a.head_grid) * (NW / 4) + grp;
-    pipe_tile<E, TBM, TBN, TBK, TS, 2, 2>(a, (uint16_t*)(smem + grp * TAIL_LDS), tb, head, M,
-                                         wave % 4);
+    if (kind == 2)
+        pipe_tile<E, MBM, MBN, MBK, MS, 2, 2>(a, (uint16_t*)(smem + grp * MID_LDS), tb, head, M,
+                                             wave % 4);
+    else
+        pipe_tile<E, TBM, TBN, TBK, TS, 2, 2>(a, (uint16_t*)(smem + grp * TAIL_LDS), tb, head, M,
+                                             wave % 4);
 }
 
 template <Epi E, int BM, int BN, int BKD, int S, int WPE, int WGM, int WGN>
 constexpr size_t pipe_kernel_lds() {
     constexpr size_t t = pipe_lds_bytes<BM, BN, BKD, S, WGM, WGN>();
-    constexpr size_t tail = TAIL_LDS * (WGM * WGN / 4);
+    constexpr size_t tail = (TAIL_LDS > MID_LDS ? TAIL_LDS : MID_LDS) * (WGM * WGN / 4);
     return t > tail ? t : tail;
 }
 
@@ -516,11 +527,19 @@ void launch_pipe(const GemmArgs& a0, hipStream_t s, bool split = true) {
                            : 0;
     if (per_cu > 0) {
         a.slots = a.cus * per_cu;
-        // the tail holds at most a quarter round of large tiles: at most slots/4/tn tile rows
-        const int tail_rows = std::min(a.Mmax, (a.slots / 4 / tn + 1) * BM);
-        const int tail_tiles = ((tail_rows + TBM - 1) / TBM) * (a.Nout / TBN);
+        // 128 x 128 tiles for a partial round of a quarter to half of the grid where the output
+        // has at most four large tile columns (FC2, out-projection): ViT-B/16 (64 frames) FC2
+        // 1.05 -> 0.84 ms, out-projection 0.39 -> 0.33 ms per sweep, ViT-L/14 FC2 -2.4 %;
+        // the wider outputs, whose partial rounds are a smaller share, measured 0.5 % slower
+        a.mid_tail = a.Nout % MBN == 0 && tn <= 4;
+        // the tail holds at most a quarter round of large tiles in 64 x 64 tiles (slots/4/tn
+        // tile rows) or at most half a round in 128 x 128 tiles
+        const int rows64 = std::min(a.Mmax, (a.slots / 4 / tn + 1) * BM);
+        const int tiles64 = ((rows64 + TBM - 1) / TBM) * (a.Nout / TBN);
+        const int rows128 = std::min(a.Mmax, (a.slots / 2 / tn + 1) * BM);
+        const int tiles128 = a.mid_tail ? ((rows128 + MBM - 1) / MBM) * (a.Nout / MBN) : 0;
         constexpr int per_block = WGM * WGN / 4;
-        grid += (tail_tiles + per_block - 1) / per_block;
+        grid += (std::max(tiles64, tiles128) + per_block - 1) / per_block;
     }
     if (grid > 0) hipLaunchKernelGGL(k, dim3(grid), dim3(WGM * WGN * 64), lds, s, a);
 }
