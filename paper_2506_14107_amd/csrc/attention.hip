@@ -114,11 +114,11 @@ constexpr int UW = 12;   // wavefronts of a per-unit attention block
 
 // Online-softmax attention of one query tile (fragments qf, one query per lane) against the
 // staged K/V: key blocks taken two at a time in order (kb, kb + 1) -- two independent MFMA
-// chains and one rescale per step.  krow maps a key to its LDS row; stage(kb) runs before the
-// step of blocks kb, kb + 1 reads them (a kernel streaming K/V through LDS loads them there).
-// On return (m, l, o) hold the tile's running max (raw score units), sum and unnormalised
-// output.  The arithmetic and its order depend only on the key values, never on where the rows
-// sit.
+// chains and at most one rescale per step.  krow maps a key to its LDS row; stage(kb) runs
+// before the step of blocks kb, kb + 1 reads them (a kernel streaming K/V through LDS loads them
+// there).  On return (m, l, o) hold the maximum the tile's probabilities are scaled to (raw score
+// units; at most 8 / sl2 below the running maximum), their sum and the unnormalised output.  The
+// arithmetic and its order depend only on the key values, never on where the rows sit.
 template <int DH, class KRow, class Stage>
 __device__ __forceinline__ void attend_tile(const Geo& g, const uint16_t* Ks, const uint16_t* Vs,
                                             int N, int lane, const bf16x8 (&qf)[DH / 16],
@@ -497,7 +497,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, int f, int h, char*
     }
     lds_barrier();
 
-    float m, l;   // running max (raw score units) and sum
+    float m, l;   // the probabilities' scale (raw score units) and their sum
     f32x16 o[DB];
     for (int t = wave; t < ntile; t += AW) {
         const int myq = q0 + t * 32 + lr;
