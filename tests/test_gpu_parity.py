@@ -79,7 +79,7 @@ def test_compact_exact(F, N, G, p):
     assert np.array_equal(host(pos), e_pos)
 
 
-# ---------------------------------------------------------------- tiny fp32 model (configs[0])
+# ------------------------------------------------------------ tiny fp32 model (112 px, p16, D192)
 def test_tiny_gate_mode_parity():
     torch = require_gpu()
     m, blob, fr = _tiny()
