@@ -439,32 +439,49 @@ __global__ __launch_bounds__(256) void compact_k(const uint8_t* cur, const int* 
     __shared__ int wtot[4];
     int pre_f = 0, pre_r = 0;   // counts of the frames before f and before r
     if (cnt) {
-        int a = 0, b = 0;
-        for (int e = tid; e < f * per; e += 256) {
-            const int v = cnt[e];
-            a += v;
-            b += e < r * per ? v : 0;
+        // eight independent loads per thread per pass: the last frames' blocks sum thousands of
+        // counts, and one load in flight per pass would put a memory latency per 256 of them on
+        // the kernel's critical path.  a: frames before f, b: before r, c: up to lim (the last
+        // block also takes its own frame's counts, for the total)
+        constexpr int U = 8;
+        const int lim = (f == F - 1 ? f + 1 : f) * per;
+        int a = 0, b = 0, c = 0;
+        for (int e0 = 0; e0 < lim; e0 += 256 * U) {
+            int v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int e = e0 + u * 256 + tid;
+                v[u] = e < lim ? cnt[e] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int e = e0 + u * 256 + tid;
+                a += e < f * per ? v[u] : 0;
+                b += e < r * per ? v[u] : 0;
+                c += v[u];
+            }
         }
         for (int o = 32; o >= 1; o >>= 1) {
             a += __shfl_xor(a, o, WAVE);
             b += __shfl_xor(b, o, WAVE);
+            c += __shfl_xor(c, o, WAVE);
         }
-        if (lane == 0) wtot[wave] = a;
+        __shared__ int wsum3[3][4];
+        if (lane == 0) {
+            wsum3[0][wave] = a;
+            wsum3[1][wave] = b;
+            wsum3[2][wave] = c;
+        }
         __syncthreads();
-        pre_f = wtot[0] + wtot[1] + wtot[2] + wtot[3];
-        __syncthreads();
-        if (lane == 0) wtot[wave] = b;
-        __syncthreads();
-        pre_r = wtot[0] + wtot[1] + wtot[2] + wtot[3];
-        __syncthreads();
+        pre_f = wsum3[0][0] + wsum3[0][1] + wsum3[0][2] + wsum3[0][3];
+        pre_r = wsum3[1][0] + wsum3[1][1] + wsum3[1][2] + wsum3[1][3];
         if (tid == 0) {
             qoff_w[f] = pre_f;
             if (f == F - 1) {
-                int last = 0;
-                for (int k = 0; k < per; ++k) last += cnt[(size_t)f * per + k];
-                qoff_w[F] = pre_f + last;
-                M[0] = pre_f + last;
-                if (tokens > 0) M[1] = tokens - (pre_f + last);
+                const int total = wsum3[2][0] + wsum3[2][1] + wsum3[2][2] + wsum3[2][3];
+                qoff_w[F] = total;
+                M[0] = total;
+                if (tokens > 0) M[1] = tokens - total;
             }
         }
     }
