@@ -30,6 +30,14 @@ __device__ inline float wave_sum(float v) {
     return v + __builtin_bit_cast(float, (threadIdx.x & 32) ? r[0] : r[1]);
 }
 
+// Buffer descriptor over `bytes` bytes at p: a load whose 32-bit byte offset falls past `bytes`
+// returns zeros without a memory access (the hardware range check), so a load that is not
+// needed can still be issued, which keeps the count of loads in flight the same on every path.
+__device__ inline __amdgpu_buffer_rsrc_t row_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+constexpr uint32_t ROW_SKIP = 0xFFFFFFF0u;   // an offset past every row buffer (all < 2^32 bytes)
+
 // --- patch gather: A[f*P + k, e] = frame[f][c][py*p+ky][px*p+kx], e = (c, ky, kx); zero pad to Kp
 // bf16: a thread writes 8 consecutive elements of a row with one 16-byte store (Kp is a multiple
 // of 64), walking (c, ky, kx) from the chunk's first element; 32-bit indices (F*P*Kp/8 < 2^31
@@ -187,174 +195,297 @@ __global__ __launch_bounds__(256) void gate_k(GateArgs a) {
             if (rfut >= 0) rq_k[k] = a.root[(size_t)rfut * N + i];
         }
     }
-    int k = 0;
-    for (int i = ch * GATE_TOK + wave; i < i_end; i += nwaves, ++k) {
-        const size_t row = (size_t)f * N + i;
-        float4* xf = (float4*)(a.x + row * D);
-        const float4* xo = xf;   // the token's current row (reordered: through its root)
-        int reuse = 0, from_fut = 0;
-        bool loaded = false;
-        float4 v[CK];
-        // cosine of this token's row (loaded into v on the first call) with reference row xr
-        auto cosine = [&](const float4* xr) {
-            float dot = 0.f, na = 0.f, nb = 0.f;
-            int eq = 1;
+    // Cosine gate or reuse off, without restoration: the wavefront's tokens in order, the rows of
+    // token kk + 1 loaded while token kk is decided and normalised (the loads of one token alone
+    // leave a memory latency per token on the path).  Per token the same loads are made, or
+    // skipped, and the same arithmetic in the same order as in the general loop below.
+    bool fast = false;
+    if constexpr (!DEC && !REORD && CK <= 5) {
+        fast = (a.mode == GATE_COS || a.mode == GATE_NONE) && a.d_out == nullptr &&
+               nwaves * TPW == GATE_TOK;
+        if (fast) {
+            const auto rx = row_rsrc(a.x, (uint32_t)((size_t)a.F * N * D * sizeof(float)));
+            float4 vb[2][CK], wb[2][CK];   // the token's own row and its reference's row
+            // the LN1 gain and shift in LDS: read from global memory next to a token's output,
+            // their wait would also wait for the next token's rows
+            __shared__ float4 sg[5 * WAVE], sb[5 * WAVE];
+            for (int c = threadIdx.x; c < nchunk; c += blockDim.x) {
+                sg[c] = g4[c];
+                sb[c] = b4[c];
+            }
+            // a token reused at the previous layer has a cosine of exactly 1: its own row is read
+            // only if it is recomputed all the same (tau > 1), its reference's row never
+            auto fetch = [&](int kk, float4 (&vv)[CK], float4 (&ww)[CK]) {
+                const int i = ch * GATE_TOK + wave + kk * nwaves;
+                const bool in = i < i_end;
+                const bool gated = in && a.mode == GATE_COS && ftype != 0 && i != 0;
+                const bool same = gated && a.prev && pv[kk];
+                const bool own = in && (!same || a.tau > 1.0f), ref = gated && !same;
+                const uint32_t ob = (uint32_t)(((size_t)f * N + i) * D * sizeof(float));
+                const uint32_t rb = (uint32_t)(((size_t)r * N + i) * D * sizeof(float));
 #pragma unroll
-            for (int k = 0; k < CK; ++k) {
-                const int c = lane + k * WAVE;
-                if (c < nchunk) {
-                    if (!loaded) v[k] = xo[c];
-                    const float4 u = v[k], w = xr[c];
-                    dot += u.x * w.x + u.y * w.y + u.z * w.z + u.w * w.w;
-                    na += u.x * u.x + u.y * u.y + u.z * u.z + u.w * u.w;
-                    nb += w.x * w.x + w.y * w.y + w.z * w.z + w.w * w.w;
-                    eq &= (u.x == w.x) & (u.y == w.y) & (u.z == w.z) & (u.w == w.w);
+                for (int k = 0; k < CK; ++k) {
+                    const int c = lane + k * WAVE;
+                    const bool cin = c < nchunk;
+                    vv[k] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                        rx, (int)(own && cin ? ob + c * 16 : ROW_SKIP), 0, 0));
+                    ww[k] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                        rx, (int)(ref && cin ? rb + c * 16 : ROW_SKIP), 0, 0));
+                }
+            };
+            fetch(0, vb[0], wb[0]);
+            __syncthreads();
+#pragma unroll
+            for (int kk = 0; kk < TPW; ++kk) {
+                const int i = ch * GATE_TOK + wave + kk * nwaves;
+                if (i >= i_end) break;
+                if (kk + 1 < TPW) fetch(kk + 1, vb[(kk + 1) & 1], wb[(kk + 1) & 1]);
+                const float4(&v)[CK] = vb[kk & 1];
+                const float4(&w)[CK] = wb[kk & 1];
+                const size_t row = (size_t)f * N + i;
+                int reuse = 0;
+                if (a.mode == GATE_COS && ftype != 0 && i != 0) {
+                    if (a.prev && pv[kk]) {
+                        reuse = a.tau <= 1.0f;
+                    } else {
+                        float dot = 0.f, na = 0.f, nb = 0.f;
+                        int eq = 1;
+#pragma unroll
+                        for (int k = 0; k < CK; ++k) {
+                            if (lane + k * WAVE < nchunk) {
+                                const float4 u = v[k], q = w[k];
+                                dot += u.x * q.x + u.y * q.y + u.z * q.z + u.w * q.w;
+                                na += u.x * u.x + u.y * u.y + u.z * u.z + u.w * u.w;
+                                nb += q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
+                                eq &= (u.x == q.x) & (u.y == q.y) & (u.z == q.z) & (u.w == q.w);
+                            }
+                        }
+                        dot = wave_sum(dot);
+                        na = wave_sum(na);
+                        nb = wave_sum(nb);
+                        const bool same = __all(eq);
+                        float cs = dot / fmaxf(sqrtf(na) * sqrtf(nb), 1e-8f);
+                        cs = fminf(1.0f, fmaxf(-1.0f, cs));
+                        reuse = (same ? 1.0f : cs) >= a.tau;
+                    }
+                }
+                if (!reuse && a.ln_out) {   // as in the general loop
+                    float sum = 0.f;
+#pragma unroll
+                    for (int k = 0; k < CK; ++k)
+                        if (lane + k * WAVE < nchunk) sum += (v[k].x + v[k].y) + (v[k].z + v[k].w);
+                    const float mean = wave_sum(sum) / (float)D;
+                    float sq = 0.f;
+#pragma unroll
+                    for (int k = 0; k < CK; ++k) {
+                        if (lane + k * WAVE < nchunk) {
+                            const float a0 = v[k].x - mean, a1 = v[k].y - mean,
+                                        a2 = v[k].z - mean, a3 = v[k].w - mean;
+                            sq += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+                        }
+                    }
+                    const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + 1e-5f);
+#pragma unroll
+                    for (int k = 0; k < CK; ++k) {
+                        const int c = lane + k * WAVE;
+                        if (c < nchunk) {
+                            const float4 gg = sg[c], bb = sb[c];
+                            float4 o;
+                            o.x = (v[k].x - mean) * rstd * gg.x + bb.x;
+                            o.y = (v[k].y - mean) * rstd * gg.y + bb.y;
+                            o.z = (v[k].z - mean) * rstd * gg.z + bb.z;
+                            o.w = (v[k].w - mean) * rstd * gg.w + bb.w;
+                            if (BF) {
+                                uint2 pk;
+                                pk.x = (uint32_t)f32_to_bf16(o.x) |
+                                       ((uint32_t)f32_to_bf16(o.y) << 16);
+                                pk.y = (uint32_t)f32_to_bf16(o.z) |
+                                       ((uint32_t)f32_to_bf16(o.w) << 16);
+                                ((uint2*)a.ln_out)[row * nchunk + c] = pk;
+                            } else {
+                                ((float4*)a.ln_out)[row * nchunk + c] = o;
+                            }
+                        }
+                    }
+                }
+                if (lane == 0) {
+                    if (a.cur) a.cur[row] = (uint8_t)reuse;
+                    if (om) om[i] = (uint8_t)(reuse ? 1 : 0);
+                    active += !reuse;
                 }
             }
-            loaded = true;
-            dot = wave_sum(dot);
-            na = wave_sum(na);
-            nb = wave_sum(nb);
-            const bool same = __all(eq);
-            float cs = dot / fmaxf(sqrtf(na) * sqrtf(nb), 1e-8f);
-            cs = fminf(1.0f, fmaxf(-1.0f, cs));
-            return same ? 1.0f : cs;
-        };
-        if (ftype != 0 && i != 0) {
-            if (a.mode == GATE_INJECT && !REORD) {
-                reuse = a.inj[((size_t)(f - a.skip) * a.L + a.layer) * N + i] != 0;
-            } else if (a.mode == GATE_ALL && !REORD) {
-                reuse = 1;
-            } else if (a.mode != GATE_NONE) {
-                if (a.prev && pv[k]) {
-                    // a reused token stands for the reference's row: cosine exactly 1
-                    if constexpr (DEC) {
-                        reuse = decision(1.0f, i) > a.tau;
-                        if (!reuse) {   // recomputed again: its row becomes the reference's
-                            const float4* xr = (const float4*)(a.x + ((size_t)r * N + i) * D);
-#pragma unroll
+        }
+    }
+    if (!fast) {
+        int k = 0;
+        for (int i = ch * GATE_TOK + wave; i < i_end; i += nwaves, ++k) {
+            const size_t row = (size_t)f * N + i;
+            float4* xf = (float4*)(a.x + row * D);
+            const float4* xo = xf;   // the token's current row (reordered: through its root)
+            int reuse = 0, from_fut = 0;
+            bool loaded = false;
+            float4 v[CK];
+            // cosine of this token's row (loaded into v on the first call) with reference row xr
+            auto cosine = [&](const float4* xr) {
+                float dot = 0.f, na = 0.f, nb = 0.f;
+                int eq = 1;
+    #pragma unroll
+                for (int k = 0; k < CK; ++k) {
+                    const int c = lane + k * WAVE;
+                    if (c < nchunk) {
+                        if (!loaded) v[k] = xo[c];
+                        const float4 u = v[k], w = xr[c];
+                        dot += u.x * w.x + u.y * w.y + u.z * w.z + u.w * w.w;
+                        na += u.x * u.x + u.y * u.y + u.z * u.z + u.w * u.w;
+                        nb += w.x * w.x + w.y * w.y + w.z * w.z + w.w * w.w;
+                        eq &= (u.x == w.x) & (u.y == w.y) & (u.z == w.z) & (u.w == w.w);
+                    }
+                }
+                loaded = true;
+                dot = wave_sum(dot);
+                na = wave_sum(na);
+                nb = wave_sum(nb);
+                const bool same = __all(eq);
+                float cs = dot / fmaxf(sqrtf(na) * sqrtf(nb), 1e-8f);
+                cs = fminf(1.0f, fmaxf(-1.0f, cs));
+                return same ? 1.0f : cs;
+            };
+            if (ftype != 0 && i != 0) {
+                if (a.mode == GATE_INJECT && !REORD) {
+                    reuse = a.inj[((size_t)(f - a.skip) * a.L + a.layer) * N + i] != 0;
+                } else if (a.mode == GATE_ALL && !REORD) {
+                    reuse = 1;
+                } else if (a.mode != GATE_NONE) {
+                    if (a.prev && pv[k]) {
+                        // a reused token stands for the reference's row: cosine exactly 1
+                        if constexpr (DEC) {
+                            reuse = decision(1.0f, i) > a.tau;
+                            if (!reuse) {   // recomputed again: its row becomes the reference's
+                                const float4* xr = (const float4*)(a.x + ((size_t)r * N + i) * D);
+    #pragma unroll
+                                for (int k = 0; k < CK; ++k) {
+                                    const int c = lane + k * WAVE;
+                                    if (c < nchunk) {
+                                        v[k] = xr[c];
+                                        xf[c] = v[k];
+                                    }
+                                }
+                                loaded = true;
+                            }
+                        } else {
+                            reuse = a.tau <= 1.0f;
+                        }
+                    } else {
+                        // reordered: rows are read through the previous layer's roots (a token reused
+                        // there is the row of the frame that recomputed it); one root, one row, and
+                        // a cosine of exactly 1 without reading it
+                        const int own = own_k[k], rp = rp_k[k], rq = rq_k[k];
+                        if (REORD && a.root) xo = (const float4*)(a.x + ((size_t)own * N + i) * D);
+                        float cs = own == rp ? 1.0f
+                                             : cosine((const float4*)(a.x + ((size_t)rp * N + i) * D));
+                        // the better of the two references; a past cosine of exactly 1 (the same
+                        // root) already wins, a tie going to the past one, so the future one is
+                        // not needed
+                        if (REORD && rfut >= 0 && own != rp) {
+                            const float c2 =
+                                own == rq ? 1.0f
+                                          : cosine((const float4*)(a.x + ((size_t)rq * N + i) * D));
+                            from_fut = c2 > cs;
+                            cs = fmaxf(cs, c2);
+                        }
+                        if (a.mode == GATE_INJECT) {
+                            reuse = a.inj[((size_t)(f - a.skip) * a.L + a.layer) * N + i] != 0;
+                        } else if (a.mode == GATE_ALL) {
+                            reuse = 1;
+                        } else if constexpr (DEC) {
+                            reuse = decision(cs, i) > a.tau;
+                        } else {
+                            reuse = cs >= a.tau;
+                        }
+                        if (REORD && !reuse && own != f) {   // recomputed after being reused: the
+    #pragma unroll                                           // token gets its root's row back
                             for (int k = 0; k < CK; ++k) {
                                 const int c = lane + k * WAVE;
                                 if (c < nchunk) {
-                                    v[k] = xr[c];
+                                    if (!loaded) v[k] = xo[c];
                                     xf[c] = v[k];
                                 }
                             }
                             loaded = true;
                         }
-                    } else {
-                        reuse = a.tau <= 1.0f;
-                    }
-                } else {
-                    // reordered: rows are read through the previous layer's roots (a token reused
-                    // there is the row of the frame that recomputed it); one root, one row, and
-                    // a cosine of exactly 1 without reading it
-                    const int own = own_k[k], rp = rp_k[k], rq = rq_k[k];
-                    if (REORD && a.root) xo = (const float4*)(a.x + ((size_t)own * N + i) * D);
-                    float cs = own == rp ? 1.0f
-                                         : cosine((const float4*)(a.x + ((size_t)rp * N + i) * D));
-                    // the better of the two references; a past cosine of exactly 1 (the same
-                    // root) already wins, a tie going to the past one, so the future one is
-                    // not needed
-                    if (REORD && rfut >= 0 && own != rp) {
-                        const float c2 =
-                            own == rq ? 1.0f
-                                      : cosine((const float4*)(a.x + ((size_t)rq * N + i) * D));
-                        from_fut = c2 > cs;
-                        cs = fmaxf(cs, c2);
-                    }
-                    if (a.mode == GATE_INJECT) {
-                        reuse = a.inj[((size_t)(f - a.skip) * a.L + a.layer) * N + i] != 0;
-                    } else if (a.mode == GATE_ALL) {
-                        reuse = 1;
-                    } else if constexpr (DEC) {
-                        reuse = decision(cs, i) > a.tau;
-                    } else {
-                        reuse = cs >= a.tau;
-                    }
-                    if (REORD && !reuse && own != f) {   // recomputed after being reused: the
-#pragma unroll                                           // token gets its root's row back
-                        for (int k = 0; k < CK; ++k) {
-                            const int c = lane + k * WAVE;
-                            if (c < nchunk) {
-                                if (!loaded) v[k] = xo[c];
-                                xf[c] = v[k];
-                            }
-                        }
-                        loaded = true;
                     }
                 }
             }
-        }
-        if (reuse && a.d_out) {   // reused (restoration): x_f - x_ref into the token-indexed buffer
-            const int rs = from_fut ? rfut : r;   // the reference that supplies the token
-            const float4* xr = (const float4*)(a.x + ((size_t)rs * N + i) * D);
-#pragma unroll
-            for (int k = 0; k < CK; ++k) {
-                const int c = lane + k * WAVE;
-                if (c < nchunk) {
-                    const float4 u = loaded ? v[k] : xf[c], w = xr[c];
-                    const float4 o = {u.x - w.x, u.y - w.y, u.z - w.z, u.w - w.w};
-                    if (BF) {
-                        uint2 pk;
-                        pk.x = (uint32_t)f32_to_bf16(o.x) | ((uint32_t)f32_to_bf16(o.y) << 16);
-                        pk.y = (uint32_t)f32_to_bf16(o.z) | ((uint32_t)f32_to_bf16(o.w) << 16);
-                        ((uint2*)a.d_out)[row * nchunk + c] = pk;
-                    } else {
-                        ((float4*)a.d_out)[row * nchunk + c] = o;
-                    }
-                }
-            }
-        }
-        if (!reuse && a.ln_out) {   // recomputed: LN1 of the row into the token-indexed buffer
-            if (!loaded) {
-#pragma unroll
+            if (reuse && a.d_out) {   // reused (restoration): x_f - x_ref into the token-indexed buffer
+                const int rs = from_fut ? rfut : r;   // the reference that supplies the token
+                const float4* xr = (const float4*)(a.x + ((size_t)rs * N + i) * D);
+    #pragma unroll
                 for (int k = 0; k < CK; ++k) {
                     const int c = lane + k * WAVE;
-                    if (c < nchunk) v[k] = xo[c];
-                }
-            }
-            float sum = 0.f;
-#pragma unroll
-            for (int k = 0; k < CK; ++k)
-                if (lane + k * WAVE < nchunk) sum += (v[k].x + v[k].y) + (v[k].z + v[k].w);
-            const float mean = wave_sum(sum) / (float)D;
-            float sq = 0.f;
-#pragma unroll
-            for (int k = 0; k < CK; ++k) {
-                if (lane + k * WAVE < nchunk) {
-                    const float a0 = v[k].x - mean, a1 = v[k].y - mean, a2 = v[k].z - mean,
-                                a3 = v[k].w - mean;
-                    sq += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
-                }
-            }
-            const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + 1e-5f);
-#pragma unroll
-            for (int k = 0; k < CK; ++k) {
-                const int c = lane + k * WAVE;
-                if (c < nchunk) {
-                    const float4 gg = g4[c], bb = b4[c];
-                    float4 o;
-                    o.x = (v[k].x - mean) * rstd * gg.x + bb.x;
-                    o.y = (v[k].y - mean) * rstd * gg.y + bb.y;
-                    o.z = (v[k].z - mean) * rstd * gg.z + bb.z;
-                    o.w = (v[k].w - mean) * rstd * gg.w + bb.w;
-                    if (BF) {
-                        uint2 pk;
-                        pk.x = (uint32_t)f32_to_bf16(o.x) | ((uint32_t)f32_to_bf16(o.y) << 16);
-                        pk.y = (uint32_t)f32_to_bf16(o.z) | ((uint32_t)f32_to_bf16(o.w) << 16);
-                        ((uint2*)a.ln_out)[row * nchunk + c] = pk;
-                    } else {
-                        ((float4*)a.ln_out)[row * nchunk + c] = o;
+                    if (c < nchunk) {
+                        const float4 u = loaded ? v[k] : xf[c], w = xr[c];
+                        const float4 o = {u.x - w.x, u.y - w.y, u.z - w.z, u.w - w.w};
+                        if (BF) {
+                            uint2 pk;
+                            pk.x = (uint32_t)f32_to_bf16(o.x) | ((uint32_t)f32_to_bf16(o.y) << 16);
+                            pk.y = (uint32_t)f32_to_bf16(o.z) | ((uint32_t)f32_to_bf16(o.w) << 16);
+                            ((uint2*)a.d_out)[row * nchunk + c] = pk;
+                        } else {
+                            ((float4*)a.d_out)[row * nchunk + c] = o;
+                        }
                     }
                 }
             }
-        }
-        if (lane == 0) {
-            if (a.cur) a.cur[row] = (uint8_t)reuse;
-            if (REORD) a.src[row] = (uint8_t)from_fut;
-            if (om) om[i] = (uint8_t)(reuse ? 1 + from_fut : 0);   // 2: from the future anchor
-            active += !reuse;
+            if (!reuse && a.ln_out) {   // recomputed: LN1 of the row into the token-indexed buffer
+                if (!loaded) {
+    #pragma unroll
+                    for (int k = 0; k < CK; ++k) {
+                        const int c = lane + k * WAVE;
+                        if (c < nchunk) v[k] = xo[c];
+                    }
+                }
+                float sum = 0.f;
+    #pragma unroll
+                for (int k = 0; k < CK; ++k)
+                    if (lane + k * WAVE < nchunk) sum += (v[k].x + v[k].y) + (v[k].z + v[k].w);
+                const float mean = wave_sum(sum) / (float)D;
+                float sq = 0.f;
+    #pragma unroll
+                for (int k = 0; k < CK; ++k) {
+                    if (lane + k * WAVE < nchunk) {
+                        const float a0 = v[k].x - mean, a1 = v[k].y - mean, a2 = v[k].z - mean,
+                                    a3 = v[k].w - mean;
+                        sq += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+                    }
+                }
+                const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + 1e-5f);
+    #pragma unroll
+                for (int k = 0; k < CK; ++k) {
+                    const int c = lane + k * WAVE;
+                    if (c < nchunk) {
+                        const float4 gg = g4[c], bb = b4[c];
+                        float4 o;
+                        o.x = (v[k].x - mean) * rstd * gg.x + bb.x;
+                        o.y = (v[k].y - mean) * rstd * gg.y + bb.y;
+                        o.z = (v[k].z - mean) * rstd * gg.z + bb.z;
+                        o.w = (v[k].w - mean) * rstd * gg.w + bb.w;
+                        if (BF) {
+                            uint2 pk;
+                            pk.x = (uint32_t)f32_to_bf16(o.x) | ((uint32_t)f32_to_bf16(o.y) << 16);
+                            pk.y = (uint32_t)f32_to_bf16(o.z) | ((uint32_t)f32_to_bf16(o.w) << 16);
+                            ((uint2*)a.ln_out)[row * nchunk + c] = pk;
+                        } else {
+                            ((float4*)a.ln_out)[row * nchunk + c] = o;
+                        }
+                    }
+                }
+            }
+            if (lane == 0) {
+                if (a.cur) a.cur[row] = (uint8_t)reuse;
+                if (REORD) a.src[row] = (uint8_t)from_fut;
+                if (om) om[i] = (uint8_t)(reuse ? 1 + from_fut : 0);   // 2: from the future anchor
+                active += !reuse;
+            }
         }
     }
     if (lane == 0) wcount[wave] = active;
