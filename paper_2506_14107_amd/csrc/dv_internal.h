@@ -75,8 +75,9 @@ struct GemmArgs {
     int P, N;            // Patch: patches and tokens per frame (Restore: N)
     int G;               // Restore: group size
     int cus;             // compute units of the device (0: no split of the last round)
-    // set by the launcher: blocks below head_grid run large tiles over the rows [0, head),
-    // the others small tiles over [head, M), head = gemm_head_rows(M, Nout, BM, BN, slots);
+    // set by the launcher: the blocks below head_grid (persistent, at most one per slot) run
+    // large tiles over the rows [0, head), the others small tiles over [head, M),
+    // head = gemm_head_rows(M, Nout, BM, BN, slots);
     // slots = 0: one tiling for all rows
     int slots, head_grid;
     bool mid_tail;       // a partial round of a quarter to half of the grid goes to 128 x 128 tiles

@@ -257,9 +257,9 @@ __device__ __forceinline__ void tile_coords(int bid, int mt, int tilesN, int& tm
 // right after it, into the slot every wave finished reading before that barrier.  The tile is
 // number `bid` of the rows [m0, M); `sm` is the group's LDS and `wave` its index in the group.
 // Every wavefront of the workgroup passes the same barriers (a group without a tile has left).
-template <Epi E, int BM, int BN, int BKD, int S, int WGM, int WGN>
+template <Epi E, int BM, int BN, int BKD, int S, int WGM, int WGN, bool PERSIST = false>
 __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int bid, int m0, int M,
-                                          int wave) {
+                                          int wave, int stride = 0) {
     constexpr int NW = WGM * WGN;                 // wavefronts, WGM x WGN over the block tile
     constexpr int WM = BM / WGM, WN = BN / WGN, TI = WM / 32, TJ = WN / 32;
     constexpr int CPR = BKD / 8;
@@ -277,7 +277,6 @@ __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int b
     const int active = mt * tilesN;
     if (bid >= active) return;
     int tm, tn;
-    tile_coords(bid, mt, tilesN, tm, tn);
 
     const int lane = threadIdx.x & 63;
     const int wm = wave / WGN, wn = wave % WGN;
@@ -288,22 +287,27 @@ __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int b
     // bytes); the k-slice advance rides in the scalar offset of buffer_load ... lds
     const int lrow = lane / CPR, lslot = lane % CPR;
     uint32_t goffA[LA], goffB[LB];
+    auto setup = [&](int b, int& tm_, int& tn_) {
+        tile_coords(b, mt, tilesN, tm_, tn_);
 #pragma unroll
-    for (int t = 0; t < LA; ++t) {
-        const int r = (wave * LA + t) * RPI + lrow;
-        const int c = lslot ^ ((r >> SH) & (CPR - 1));
-        const int grow = m0 + tm * BM + r;
-        const int arow = a.a_idx ? (grow < M ? a.a_idx[grow] : 0) : grow;   // gathered A rows
-        goffA[t] = ((uint32_t)arow * K + c * 8) * 2;
-    }
+        for (int t = 0; t < LA; ++t) {
+            const int r = (wave * LA + t) * RPI + lrow;
+            const int c = lslot ^ ((r >> SH) & (CPR - 1));
+            const int grow = m0 + tm_ * BM + r;
+            const int arow = a.a_idx ? (grow < M ? a.a_idx[grow] : 0) : grow;   // gathered A rows
+            goffA[t] = ((uint32_t)arow * K + c * 8) * 2;
+        }
 #pragma unroll
-    for (int t = 0; t < LB; ++t) {
-        const int r = (wave * LB + t) * RPI + lrow;
-        const int c = lslot ^ ((r >> SH) & (CPR - 1));
-        goffB[t] = ((uint32_t)(tn * BN + r) * K + c * 8) * 2;
-    }
+        for (int t = 0; t < LB; ++t) {
+            const int r = (wave * LB + t) * RPI + lrow;
+            const int c = lslot ^ ((r >> SH) & (CPR - 1));
+            goffB[t] = ((uint32_t)(tn_ * BN + r) * K + c * 8) * 2;
+        }
+    };
+    setup(bid, tm, tn);
     const auto rA = buf_rsrc(a.A, BUF_ANY);
     const auto rW = buf_rsrc(a.W, BUF_ANY);
+    const auto rB_ = buf_rsrc(a.bias, BUF_ANY);
     auto issue = [&](int kt) {
         uint16_t* st = sm + (kt % S) * STAGE;
         const int soff = kt * BKD * 2;
@@ -317,6 +321,21 @@ __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int b
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rW,
                 (__attribute__((address_space(3))) void*)(st + BM * BKD + (wave * LB + t) * RPI * BKD), 16,
                 (int)goffB[t], soff, 0, 0);
+    };
+    // persistent tiles: the tile's bias (BN floats) goes to LDS past the slabs with the DMA of its
+    // first slice, so that setting the accumulators waits on no vector memory operation (a
+    // global load there would also wait for the previous epilogue's stores)
+    constexpr size_t RING_B = (size_t)S * STAGE * 2;
+    constexpr size_t SLAB_END = (size_t)STAGE * 2 + (size_t)NW * 32 * (TJ * 32 + 4) * 4;
+    float* const bias_lds = (float*)((char*)sm + (RING_B > SLAB_END ? RING_B : SLAB_END));
+    auto issue_bias = [&](int tn_) {
+        if constexpr (PERSIST) {
+            static_assert(BN % 64 == 0 && BN / 64 <= NW, "one 64-float piece per wavefront");
+            if (wave < BN / 64)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rB_,
+                    (__attribute__((address_space(3))) void*)(bias_lds + wave * 64), 4,
+                    (int)((tn_ * BN + wave * 64 + lane) * 4), 0, 0, 0);
+        }
     };
     // per-lane LDS element offsets of the fragments (row part; the chunk is XORed per k-step)
     int offA[TI], offB[TJ], swA[TI], swB[TJ];
@@ -341,30 +360,15 @@ __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int b
         for (int j = 0; j < TJ; ++j) xb[j] = *(const bf16x8*)(st + offB[j] + (c ^ swB[j]) * 8);
     };
 
-    // the accumulators start at the bias of their column (lane l, register r of MFMA tile j:
-    // column (r/4)*8 + (l/32)*4 + r%4 of the tile), so the epilogue does not add it
     f32x16 acc[TI][TJ];
-#pragma unroll
-    for (int j = 0; j < TJ; ++j) {
-        f32x16 b;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const f32x4 v = *(const f32x4*)(a.bias + tn * BN + wn * WN + j * 32 + g * 8 + hl * 4);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) b[g * 4 + e] = v[e];
-        }
-#pragma unroll
-        for (int i = 0; i < TI; ++i) acc[i][j] = b;
-    }
-
     const int nk = K / BKD;
 #pragma unroll
     for (int p = 0; p < S - 1; ++p)
         if (p < nk) issue(p);
+    issue_bias(tn);
     wait_vm<0>();
     bare_barrier();
     bf16x8 fa[2][TI], fb[2][TJ];
-    frag(0, 0, fa[0], fb[0]);
     // one k-slice: MFMAs on the fragments in hand while the next fragments are read.  NEXT:
     // whether the following slice's first fragments are read at the end (after its barrier);
     // WAITN: vmcnt that guarantees the following slice has landed.  The three uses below are
@@ -420,17 +424,59 @@ __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int b
     };
     using T_ = std::integral_constant<bool, true>;
     using F_ = std::integral_constant<bool, false>;
-    int kt = 0;
-    for (; kt + S - 1 < nk; ++kt) {   // steady state: a new slice enters the ring every step
-        issue(kt + S - 1);            // slot of slice kt-1: every wave read it before a barrier
-        slice(kt, T_(), std::integral_constant<int, (S - 2) * L>());
-    }
-    for (; kt + 1 < nk; ++kt) slice(kt, T_(), std::integral_constant<int, 0>());   // drain
-    slice(kt, F_(), std::integral_constant<int, 0>());                              // last slice
+    for (;;) {   // one tile; persistent head blocks go on to tile bid + stride
+        // the accumulators start at the bias of their column (lane l, register r of MFMA tile j:
+        // column (r/4)*8 + (l/32)*4 + r%4 of the tile), so the epilogue does not add it
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+            f32x16 b;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int bc = wn * WN + j * 32 + g * 8 + hl * 4;
+                const f32x4 v = PERSIST ? *(const f32x4*)(bias_lds + bc)
+                                        : *(const f32x4*)(a.bias + tn * BN + bc);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) b[g * 4 + e] = v[e];
+            }
+#pragma unroll
+            for (int i = 0; i < TI; ++i) acc[i][j] = b;
+        }
 
-    __syncthreads();   // every wave is done with the LDS ring
-    epilogue_lds<E, TI, TJ>(a, acc, (float*)sm + wave * (32 * (TJ * 32 + 4)),
-                            m0 + tm * BM + wm * WM, tn * BN + wn * WN, M, lane);
+        frag(0, 0, fa[0], fb[0]);
+        int kt = 0;
+        for (; kt + S - 1 < nk; ++kt) {   // steady state: a new slice enters the ring every step
+            issue(kt + S - 1);            // slot of slice kt-1: every wave read it before a barrier
+            slice(kt, T_(), std::integral_constant<int, (S - 2) * L>());
+        }
+        for (; kt + 1 < nk; ++kt) slice(kt, T_(), std::integral_constant<int, 0>());   // drain
+        // persistent: the block's next tile takes its first slice into slot 0 now -- every wave
+        // finished reading slot 0 (slice nk - 2) before the last barrier -- so that it lands while
+        // this tile's last slice and epilogue run
+        const int nbid = bid + stride;
+        const bool more = PERSIST && S == 2 && nk % 2 == 0 && nbid < active;
+        int ntm = 0, ntn = 0;
+        if (more) {
+            setup(nbid, ntm, ntn);
+            issue(0);
+            issue_bias(ntn);
+        }
+        slice(kt, F_(), std::integral_constant<int, 0>());   // last slice
+
+        __syncthreads();   // every wave is done with the LDS ring
+        // (persistent: the slabs sit past slot 0, which holds the next tile's first slice)
+        float* const slabs = (float*)(PERSIST ? sm + STAGE : sm);
+        epilogue_lds<E, TI, TJ>(a, acc, slabs + wave * (32 * (TJ * 32 + 4)),
+                                m0 + tm * BM + wm * WM, tn * BN + wn * WN, M, lane);
+        if (!more) break;
+        bid = nbid;
+        tm = ntm;
+        tn = ntn;
+        // the next tile's first slice and bias have landed -- every epilogue issues at least its
+        // TI * NQ stores after their copies, and the stores need not be waited for -- and every
+        // wave is done with its slab
+        wait_vm<TI * (32 / (64 / (TJ * 8)))>();
+        bare_barrier();
+    }
 }
 
 // LDS of one block tile: the DMA ring, reused by the epilogue's per-wave slabs
@@ -451,12 +497,14 @@ constexpr size_t TAIL_LDS = pipe_lds_bytes<TBM, TBN, TBK, TS, 2, 2>();
 constexpr int MBM = 128, MBN = 128, MBK = 64, MS = 2;
 constexpr size_t MID_LDS = pipe_lds_bytes<MBM, MBN, MBK, MS, 2, 2>();
 
-// Block tiles BM x BN of WGM x WGN wavefronts.  With a.slots set, the launch is split: blocks
-// below a.head_grid take the rows [0, head) that fill whole rounds of the grid
-// (gemm_head_rows), and the blocks after them cut the remaining rows into 64 x 64 tiles (a
-// partial round of at most a quarter of the grid) or 128 x 128 tiles (at most half, with
-// a.mid_tail), one per group of four wavefronts, so that the last, partial round spreads over
-// many compute units.
+// Block tiles BM x BN of WGM x WGN wavefronts.  With a.slots set, the launch is split: the
+// a.head_grid blocks below it (at most one per slot) are persistent and take the tiles of the
+// rows [0, head) that fill whole rounds of the grid (gemm_head_rows) -- tile bid, bid +
+// head_grid, ... -- each tile's first k-slice and bias arriving during the previous tile's
+// epilogue; the blocks after them cut the remaining rows into 64 x 64 tiles (a partial round of
+// at most a quarter of the grid) or 128 x 128 tiles (at most half, with a.mid_tail), one per
+// group of four wavefronts, so that the last, partial round spreads over many compute units.
+// A tile's outputs are the same whichever block takes it (one k order per output).
 template <Epi E, int BM, int BN, int BKD, int S, int WPE, int WGM, int WGN>
 __global__ __launch_bounds__(WGM * WGN * 64) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void gemm_bf16_pipe_k(GemmArgs a) {
@@ -471,7 +519,8 @@ void gemm_bf16_pipe_k(GemmArgs a) {
     int kind = 0;
     const int head = gemm_head_rows(M, a.Nout, BM, BN, a.slots, &kind, a.mid_tail);
     if ((int)blockIdx.x < a.head_grid) {
-        pipe_tile<E, BM, BN, BKD, S, WGM, WGN>(a, (uint16_t*)smem, blockIdx.x, 0, head, wave);
+        pipe_tile<E, BM, BN, BKD, S, WGM, WGN, true>(a, (uint16_t*)smem, blockIdx.x, 0, head, wave,
+                                                     a.head_grid);
         return;
     }
     static_assert(NW % 4 == 0, "tail tiles take groups of four wavefronts");
@@ -487,7 +536,12 @@ void gemm_bf16_pipe_k(GemmArgs a) {
 
 template <Epi E, int BM, int BN, int BKD, int S, int WPE, int WGM, int WGN>
 constexpr size_t pipe_kernel_lds() {
-    constexpr size_t t = pipe_lds_bytes<BM, BN, BKD, S, WGM, WGN>();
+    constexpr size_t t0 = pipe_lds_bytes<BM, BN, BKD, S, WGM, WGN>();
+    constexpr size_t ring_b = (size_t)S * (BM + BN) * BKD * 2;
+    constexpr size_t slab_end =
+        (size_t)(BM + BN) * BKD * 2 + (size_t)WGM * WGN * 32 * (BN / WGN + 4) * 4;
+    constexpr size_t tp = (ring_b > slab_end ? ring_b : slab_end) + (size_t)BN * 4;
+    constexpr size_t t = t0 > tp ? t0 : tp;
     constexpr size_t tail = (TAIL_LDS > MID_LDS ? TAIL_LDS : MID_LDS) * (WGM * WGN / 4);
     return t > tail ? t : tail;
 }
@@ -527,6 +581,10 @@ void launch_pipe(const GemmArgs& a0, hipStream_t s, bool split = true) {
                            : 0;
     if (per_cu > 0) {
         a.slots = a.cus * per_cu;
+        // persistent head blocks: a multiple of the 8 XCDs, so that tile bid + k * head_grid
+        // lands on the XCD tile_coords assigns it
+        a.head_grid = std::min(a.head_grid, a.slots);
+        grid = a.head_grid;
         // 128 x 128 tiles for a partial round of a quarter to half of the grid where the output
         // has at most four large tile columns (FC2, out-projection): ViT-B/16 (64 frames) FC2
         // 1.05 -> 0.84 ms, out-projection 0.39 -> 0.33 ms per sweep, ViT-L/14 FC2 -2.4 %;
