@@ -257,6 +257,9 @@ __device__ __forceinline__ void tile_coords(int bid, int mt, int tilesN, int& tm
 // right after it, into the slot every wave finished reading before that barrier.  The tile is
 // number `bid` of the rows [m0, M); `sm` is the group's LDS and `wave` its index in the group.
 // Every wavefront of the workgroup passes the same barriers (a group without a tile has left).
+// PERSIST: the block goes on to tiles bid + stride, bid + 2 stride, ... of the same rows; when a
+// tile's last k-slice starts, the next tile's first slice and bias are copied into the ring slot
+// that is then free, and the epilogue's slabs sit past that slot.
 template <Epi E, int BM, int BN, int BKD, int S, int WGM, int WGN, bool PERSIST = false>
 __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int bid, int m0, int M,
                                           int wave, int stride = 0) {
@@ -307,7 +310,7 @@ __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int b
     setup(bid, tm, tn);
     const auto rA = buf_rsrc(a.A, BUF_ANY);
     const auto rW = buf_rsrc(a.W, BUF_ANY);
-    const auto rB_ = buf_rsrc(a.bias, BUF_ANY);
+    const auto rBias = buf_rsrc(a.bias, BUF_ANY);
     auto issue = [&](int kt) {
         uint16_t* st = sm + (kt % S) * STAGE;
         const int soff = kt * BKD * 2;
@@ -332,7 +335,7 @@ __device__ __forceinline__ void pipe_tile(const GemmArgs& a, uint16_t* sm, int b
         if constexpr (PERSIST) {
             static_assert(BN % 64 == 0 && BN / 64 <= NW, "one 64-float piece per wavefront");
             if (wave < BN / 64)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rB_,
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rBias,
                     (__attribute__((address_space(3))) void*)(bias_lds + wave * 64), 4,
                     (int)((tn_ * BN + wave * 64 + lane) * 4), 0, 0, 0);
         }
