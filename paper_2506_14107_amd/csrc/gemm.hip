@@ -584,9 +584,11 @@ void launch_pipe(const GemmArgs& a0, hipStream_t s, bool split = true) {
                            : 0;
     if (per_cu > 0) {
         a.slots = a.cus * per_cu;
-        // persistent head blocks: a multiple of the 8 XCDs, so that tile bid + k * head_grid
-        // lands on the XCD tile_coords assigns it
-        a.head_grid = std::min(a.head_grid, a.slots);
+        // persistent head blocks where tiles can follow one another (a 2-stage ring and an even
+        // number of k-slices: pipe_tile's `more`); their number is a multiple of the 8 XCDs, so
+        // that tile bid + k * head_grid lands on the XCD tile_coords assigns it.  Otherwise one
+        // block per head tile, as each block then takes a single tile.
+        if (S == 2 && (a.K / BKD) % 2 == 0) a.head_grid = std::min(a.head_grid, a.slots);
         grid = a.head_grid;
         // 128 x 128 tiles for a partial round of a quarter to half of the grid where the output
         // has at most four large tile columns (FC2, out-projection): ViT-B/16 (64 frames) FC2

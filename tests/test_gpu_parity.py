@@ -178,6 +178,25 @@ def test_batching_and_determinism_bitwise():
         assert np.array_equal(cat, ref[k])
 
 
+def test_batching_bitwise_past_one_round_of_narrow_tiles():
+    """Width 1152 with 257 tokens: QKV (3456 outputs), the out-projection and FC2 (1152) take the
+    256 x 128 tiling, whose blocks each run one tile.  A 32-frame batch gives them well over one
+    round of head tiles (QKV: 27 tile columns); the same frames encoded 8 at a time stay under one
+    round.  Every output must be the same bit for bit, gated and with reuse off."""
+    torch = require_gpu()
+    m = ModelConfig(224, 14, 1, 1152, 18, 2304, "bf16")
+    blob = synth.make_blob(m, 41)
+    fr = _video(m, 32, seed=9)
+    big = encoder(m, blob, 32)
+    small = encoder(m, blob, 8)
+    for tau in (0.9, float("-inf")):
+        a = big.encode(dev(fr), 8, tau, want_tokens=True)
+        b = small.encode(dev(fr), 8, tau, want_tokens=True)
+        torch.cuda.synchronize()
+        for x, y in zip(a, b):
+            assert np.array_equal(host(x), host(y)), f"tau {tau}"
+
+
 def test_live_handle_rejects_bad_arguments_without_launching():
     """A live handle rejects an empty or negative frame count, a group size of 0 or above the
     batch, a NaN tau and NULL buffers with DV_EINVAL, on the host: the output buffer keeps its
